@@ -1,0 +1,254 @@
+/*
+ * instantmimic.h -- C ABI of the MI355X environment-plus-policy step.
+ *
+ * The library implements, for a batch of independent environments, the part
+ * of a DeepMimic-style PPO rollout step that runs outside the physics solver
+ * (InstantMimic, arXiv 2609.09821): Sec. 3 / Fig. 3 gives the loop
+ *     action = policy(obs); <physics>; reward, terminated, truncated =
+ *     eval_reward_and_dones(); reset_envs(terminated | truncated);
+ *     obs = build_obs()
+ * and Sec. 4 makes every post-physics stage a fused GPU kernel that reads
+ * the simulator's arrays in place (Sec. 4.2) with an unconditional reset
+ * restricted by a device-side mask (Sec. 4.2).
+ *
+ * Entry points:
+ *   im_env_step_fused  reward + termination + masked reset + observation
+ *                      (Sec. 4.1 Fig. 4 reward and dones, Sec. 4.2 reset,
+ *                      Sec. 6.1 observation), one kernel launch;
+ *   im_policy_act      Gaussian MLP policy forward and action sampling
+ *                      (Fig. 3 "policy(obs)", Sec. 6.1 / backflip table:
+ *                      state-independent log-std);
+ *   im_reset_envs      forced reset of the envs selected by a device mask
+ *                      (start of a rollout, host-requested resets).
+ *
+ * Conventions.  Quaternions are (w, x, y, z), Hamilton product (Fig. 2a
+ * converts the simulator's quaternions to wxyz).  World up is +z; a root's
+ * local +x axis is its forward direction.  Body 0 is the root (free joint);
+ * parent[b] < b.
+ *
+ * Memory.  Every per-env buffer is device memory owned by the caller; the
+ * library never keeps caller pointers between calls.  Per-env arrays are
+ * structure-of-arrays with a leading dimension `ld` (>= n_envs): component
+ * c of body b of env e is at  base[(b * NC + c) * ld + e].  A context owns
+ * its device copies of the skeleton, clip and weight tables and a policy
+ * workspace sized for `max_envs` at creation.
+ *
+ * Hot calls (im_env_step_fused, im_policy_act, im_reset_envs,
+ * im_standin_physics) allocate nothing, read no device memory on the host
+ * and never synchronise: they validate their arguments on the host in O(1),
+ * enqueue kernels on `stream` (a hipStream_t; NULL = the default stream) and
+ * return.  Device faults surface at the caller's next synchronisation.
+ * They may be captured into a HIP graph.
+ *
+ * Errors.  Every function returns an im_status and never throws;
+ * im_last_error() returns a message for the calling thread's last failure.
+ */
+#ifndef INSTANTMIMIC_H
+#define INSTANTMIMIC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    IM_OK = 0,
+    IM_ERR_INVALID_ARG = 1,  /* NULL pointer, bad size, inconsistent description */
+    IM_ERR_UNSUPPORTED = 2,  /* valid but beyond this build's limits (e.g. > 64 bodies) */
+    IM_ERR_OOM = 3,          /* device allocation failed at creation */
+    IM_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
+} im_status;
+
+enum {
+    IM_JOINT_FREE = 0,       /* the root only */
+    IM_JOINT_SPHERICAL = 1,  /* 3 rotational DoF */
+    IM_JOINT_REVOLUTE = 2,   /* 1 DoF about `axis` */
+    IM_JOINT_FIXED = 3       /* no DoF; its clip rotations must be identity */
+};
+
+enum { IM_DTYPE_F32 = 0, IM_DTYPE_BF16 = 1 };
+
+#define IM_MAX_BODIES 64
+#define IM_MAX_DEPTH 16
+
+typedef struct im_ctx im_ctx;
+
+/*
+ * Step configuration.  Reward (Sec. 4.1, Fig. 4, with the end-effector
+ * position term of the DeepMimic reward that Sec. 6.1 builds on):
+ *   r = c_pose exp(-(w_pos e_pos + w_ee e_ee)) + c_vel exp(-w_vel e_vel)
+ *       + c_com exp(-w_com e_com)
+ * with e_pos / e_vel the sums over bodies of squared position / linear
+ * velocity errors, e_ee the position errors summed over leaf bodies and
+ * e_com the squared error of the mass-weighted centre of the body origins.
+ * Fig. 4's printed form is c = (0.60, 0.25, 0.15), w = (4, 0.25, 8), w_ee = 0.
+ * Termination (Fig. 4, strict "<"; grace steps from the backflip table):
+ *   terminated = (t + 1 > grace) && (root_z < h_term || !(r >= r_min)).
+ * Truncation: the clip phase reaches 1.
+ */
+typedef struct {
+    double dt;        /* control step in seconds (> 0) */
+    float h_term;     /* root-height termination threshold (m) */
+    float r_min;      /* reward termination threshold */
+    int32_t grace;    /* steps after a reset during which no env terminates (>= 0) */
+    float c_pose, w_pos, w_ee;
+    float c_vel, w_vel;
+    float c_com, w_com;
+    uint64_t seed;    /* Philox4x32-10 key (low word, high word) */
+} im_config;
+
+/* Host arrays; copied at creation. */
+typedef struct {
+    int32_t n_bodies;        /* B, 1..IM_MAX_BODIES */
+    const int32_t *parent;   /* [B]; parent[0] = -1, 0 <= parent[b] < b */
+    const int32_t *jtype;    /* [B]; jtype[0] = FREE, others SPHERICAL/REVOLUTE/FIXED */
+    const float *axis;       /* [B][3]; unit revolute axis in the parent frame */
+    const float *offset;     /* [B][3]; joint (= body origin) in the parent frame, m */
+    const float *mass;       /* [B]; > 0, kg (point mass at the body origin) */
+} im_skeleton;
+
+/* One reference clip, host arrays; copied at creation. */
+typedef struct {
+    int32_t n_frames;        /* F >= 2 */
+    float fps;               /* frames per second (> 0) */
+    const float *root_pos;   /* [F][3] world root position */
+    const float *root_quat;  /* [F][4] world root orientation, unit (|q| within 1e-3) */
+    const float *local_quat; /* [F][B-1][4] rotation of body b = 1..B-1 in its parent frame */
+} im_clip;
+
+/*
+ * Gaussian MLP policy.  dims[0] must be the observation width 15*B+1 and
+ * dims[L] is the action width A.  Hidden layers: ReLU; last layer linear
+ * (the mean).  BF16: observation and hidden activations are rounded to bf16
+ * (nearest even), weights are bf16, products accumulate in fp32.  Actions:
+ * a = mean + exp(log_std) * z, z ~ N(0, 1) from Philox4x32-10 with counter
+ * (env, env_n, j, 0) for the four actions 4j..4j+3 (Box-Muller on the two
+ * word pairs); logp = -sum_a (z_a^2/2 + log_std_a + ln(2 pi)/2).
+ */
+typedef struct {
+    int32_t n_layers;              /* L >= 1 */
+    const int32_t *dims;           /* [L+1] */
+    int32_t dtype;                 /* IM_DTYPE_F32 or IM_DTYPE_BF16 */
+    const void *const *weight;     /* [L] host pointers, W_l [dims[l+1]][dims[l]] row-major:
+                                      float for F32, uint16 bf16 bit patterns for BF16 */
+    const float *const *bias;      /* [L] host pointers, b_l [dims[l+1]] */
+    const float *log_std;          /* [A] */
+} im_policy;
+
+/*
+ * Per-env device buffers (caller-owned), ld >= n_envs.
+ *   body_pos    [B][3][ld]  world body-origin position (m); read by the step,
+ *                           written for reset envs (reference state)
+ *   body_quat   [B][4][ld]  world orientation (w,x,y,z)
+ *   body_linvel [B][3][ld]  world linear velocity of the body origin (m/s)
+ *   body_angvel [B][3][ld]  world angular velocity (rad/s)
+ *   env_clip    [ld] int32  reference clip of the env          (read/write)
+ *   env_phase   [ld] float  clip phase in [0, 1]               (read/write)
+ *   env_t       [ld] int32  steps since the last reset         (read/write)
+ *   env_n       [ld] uint32 step counter of the env's random streams
+ *   reward      [ld] float, terminated [ld] uint8, truncated [ld] uint8
+ *   obs         [D][ld] float, D = 15*B + 1: per body b at rows 15b..15b+14
+ *               heading-frame position (3), first two columns of the
+ *               heading-frame rotation matrix (6), heading-frame linear (3)
+ *               and angular (3) velocity; row 15B = phase (Sec. 6.1)
+ *   ref_frame   [ld] int32 or NULL: reference frame index used this step
+ */
+typedef struct {
+    float *body_pos;
+    float *body_quat;
+    float *body_linvel;
+    float *body_angvel;
+    int32_t *env_clip;
+    float *env_phase;
+    int32_t *env_t;
+    uint32_t *env_n;
+    float *reward;
+    uint8_t *terminated;
+    uint8_t *truncated;
+    float *obs;
+    int32_t *ref_frame;
+    int64_t n_envs;
+    int64_t ld;
+} im_env_bufs;
+
+typedef struct {
+    int32_t n_bodies, obs_dim, action_dim, n_clips, n_layers, policy_dtype, max_depth;
+    int64_t max_envs;
+    int64_t device_bytes;    /* device memory held by the context */
+} im_info;
+
+/*
+ * Create a context on the current HIP device.  Validates everything
+ * (topology, joint types, unit quaternions, clip lengths, layer widths) and
+ * uploads/packs the tables; max_envs bounds n_envs of im_policy_act.
+ * On failure *out is NULL and nothing is leaked.
+ */
+im_status im_create(const im_config *cfg, const im_skeleton *skel, const im_clip *clips,
+                    int32_t n_clips, const im_policy *policy, int64_t max_envs, im_ctx **out);
+
+im_status im_destroy(im_ctx *ctx);
+
+im_status im_get_info(const im_ctx *ctx, im_info *info);
+
+/*
+ * Fused environment step (Fig. 3 post-physics phase, Sec. 4).  For each env
+ * e < n_envs, on the sim state the physics left in the buffers:
+ *  1. phase' = phase + dphi_k (fp32, dphi_k = float(dt * fps_k / (F_k - 1)));
+ *     t' = t + 1; n' = n + 1; truncated = phase' >= 1;
+ *  2. reference at min(phase', 1): s = phase * (F-1), i0 = min(floor(s), F-2),
+ *     alpha = s - i0; root position lerp, root and joint rotations slerp
+ *     between frames i0 and i0+1, forward kinematics over the tree, reference
+ *     velocities = exact time derivatives of that path;
+ *  3. reward and terminated (im_config) against the sim state;
+ *  4. envs with terminated | truncated are reset: Philox counter
+ *     (e, n', 0, 1) gives clip = (x0 * n_clips) >> 32 and phase =
+ *     (x1 >> 8) * 2^-24, t = 0, and the sim state of every body is set to
+ *     the reference state there (reference state initialisation);
+ *     other envs keep clip and sim state and take phase', t';
+ *  5. obs is built from the post-reset sim state; env_n = n' for all envs.
+ * reward/terminated/truncated describe the pre-reset state.
+ */
+im_status im_env_step_fused(im_ctx *ctx, const im_env_bufs *bufs, void *stream);
+
+/*
+ * Policy forward and sampling for envs e < n_envs.
+ *   obs    [D][ld_obs] float (device), env_n [ld_obs] uint32 (device: the
+ *          counter before the step that will consume the action)
+ *   mean, action [n_envs][A] float (device), logp [n_envs] float or NULL.
+ * n_envs <= max_envs.  Uses the context's workspace: calls on one context
+ * must be ordered (same stream or synchronised).
+ */
+im_status im_policy_act(im_ctx *ctx, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                        int64_t n_envs, float *mean, float *action, float *logp, void *stream);
+
+/*
+ * Forced reset of the envs whose mask byte is non-zero (all envs when mask
+ * is NULL; mask is a device array [n_envs]).  Draws clip and phase with the
+ * Philox counter (e, env_n, 0, 4), sets t = 0, writes the reference state to
+ * the sim buffers and the observation.  env_n is not advanced.
+ */
+im_status im_reset_envs(im_ctx *ctx, const im_env_bufs *bufs, const uint8_t *mask, void *stream);
+
+/*
+ * Benchmark/test harness, not part of the step: a kinematic stand-in for
+ * the physics solver.  Writes to the sim buffers the reference state at each
+ * env's next phase (phase + dphi) with Gaussian rotation noise (std
+ * sigma_joint rad per DoF) composed on the right of the root orientation and
+ * of every non-fixed joint, and velocities = reference + N(0, sigma_vel^2)
+ * per component.  Normals: Philox counter (e, env_n, j/4, 3), lane j%4 of
+ * the Box-Muller block; j runs over the root rotation (3), then each body
+ * 1..B-1's DoFs in index order, then each body's linear (3) and angular (3)
+ * velocity in index order.
+ */
+im_status im_standin_physics(im_ctx *ctx, const im_env_bufs *bufs, float sigma_joint,
+                             float sigma_vel, void *stream);
+
+const char *im_status_str(im_status s);
+const char *im_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INSTANTMIMIC_H */

@@ -1,0 +1,285 @@
+"""ctypes binding of libinstantmimic.so (C ABI in include/instantmimic.h).
+
+Argument marshalling only: every stage of the step runs in the HIP kernels of
+the library.  PyTorch supplies device memory and the stream handle.  There is
+no fallback: if the library is not built, loading raises.
+
+Module-level functions carry the C names (im_create, im_env_step_fused,
+im_policy_act, im_reset_envs, ...).  `Context` and `EnvBuffers` are small
+conveniences over them for tensors.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libinstantmimic.so")
+
+IM_OK, IM_ERR_INVALID_ARG, IM_ERR_UNSUPPORTED, IM_ERR_OOM, IM_ERR_HIP = range(5)
+IM_DTYPE_F32, IM_DTYPE_BF16 = 0, 1
+
+
+class ImConfig(C.Structure):
+    _fields_ = [("dt", C.c_double), ("h_term", C.c_float), ("r_min", C.c_float),
+                ("grace", C.c_int32), ("c_pose", C.c_float), ("w_pos", C.c_float),
+                ("w_ee", C.c_float), ("c_vel", C.c_float), ("w_vel", C.c_float),
+                ("c_com", C.c_float), ("w_com", C.c_float), ("seed", C.c_uint64)]
+
+
+class ImSkeleton(C.Structure):
+    _fields_ = [("n_bodies", C.c_int32), ("parent", C.POINTER(C.c_int32)),
+                ("jtype", C.POINTER(C.c_int32)), ("axis", C.POINTER(C.c_float)),
+                ("offset", C.POINTER(C.c_float)), ("mass", C.POINTER(C.c_float))]
+
+
+class ImClip(C.Structure):
+    _fields_ = [("n_frames", C.c_int32), ("fps", C.c_float), ("root_pos", C.POINTER(C.c_float)),
+                ("root_quat", C.POINTER(C.c_float)), ("local_quat", C.POINTER(C.c_float))]
+
+
+class ImPolicy(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("dims", C.POINTER(C.c_int32)), ("dtype", C.c_int32),
+                ("weight", C.POINTER(C.c_void_p)), ("bias", C.POINTER(C.POINTER(C.c_float))),
+                ("log_std", C.POINTER(C.c_float))]
+
+
+class ImEnvBufs(C.Structure):
+    _fields_ = [("body_pos", C.c_void_p), ("body_quat", C.c_void_p), ("body_linvel", C.c_void_p),
+                ("body_angvel", C.c_void_p), ("env_clip", C.c_void_p), ("env_phase", C.c_void_p),
+                ("env_t", C.c_void_p), ("env_n", C.c_void_p), ("reward", C.c_void_p),
+                ("terminated", C.c_void_p), ("truncated", C.c_void_p), ("obs", C.c_void_p),
+                ("ref_frame", C.c_void_p), ("n_envs", C.c_int64), ("ld", C.c_int64)]
+
+
+class ImInfo(C.Structure):
+    _fields_ = [("n_bodies", C.c_int32), ("obs_dim", C.c_int32), ("action_dim", C.c_int32),
+                ("n_clips", C.c_int32), ("n_layers", C.c_int32), ("policy_dtype", C.c_int32),
+                ("max_depth", C.c_int32), ("max_envs", C.c_int64), ("device_bytes", C.c_int64)]
+
+
+EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_policy_act",
+            "im_reset_envs", "im_standin_physics", "im_status_str", "im_last_error"]
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libinstantmimic.so is not built (run python -m "
+                           "paper_2609_09821_amd.build); there is no fallback path")
+    L = C.CDLL(LIB_PATH)
+    st = C.c_int
+    L.im_create.argtypes = [C.POINTER(ImConfig), C.POINTER(ImSkeleton), C.POINTER(ImClip),
+                            C.c_int32, C.POINTER(ImPolicy), C.c_int64, C.POINTER(C.c_void_p)]
+    L.im_create.restype = st
+    L.im_destroy.argtypes = [C.c_void_p]
+    L.im_destroy.restype = st
+    L.im_get_info.argtypes = [C.c_void_p, C.POINTER(ImInfo)]
+    L.im_get_info.restype = st
+    L.im_env_step_fused.argtypes = [C.c_void_p, C.POINTER(ImEnvBufs), C.c_void_p]
+    L.im_env_step_fused.restype = st
+    L.im_policy_act.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int64,
+                                C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.im_policy_act.restype = st
+    L.im_reset_envs.argtypes = [C.c_void_p, C.POINTER(ImEnvBufs), C.c_void_p, C.c_void_p]
+    L.im_reset_envs.restype = st
+    L.im_standin_physics.argtypes = [C.c_void_p, C.POINTER(ImEnvBufs), C.c_float, C.c_float,
+                                     C.c_void_p]
+    L.im_standin_physics.restype = st
+    L.im_status_str.argtypes = [C.c_int]
+    L.im_status_str.restype = C.c_char_p
+    L.im_last_error.argtypes = []
+    L.im_last_error.restype = C.c_char_p
+    _lib = L
+    return L
+
+
+class ImError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("%s: %s" % (lib().im_status_str(status).decode(), msg))
+        self.status = status
+
+
+def _check(status):
+    if status != IM_OK:
+        raise ImError(status, lib().im_last_error().decode())
+
+
+# ------------------------------------------------------------- C-named calls
+def im_create(cfg, skel, clips, n_clips, policy, max_envs):
+    out = C.c_void_p()
+    _check(lib().im_create(C.byref(cfg), C.byref(skel), clips, n_clips, C.byref(policy),
+                           int(max_envs), C.byref(out)))
+    return out
+
+
+def im_destroy(ctx):
+    _check(lib().im_destroy(ctx))
+
+
+def im_get_info(ctx):
+    info = ImInfo()
+    _check(lib().im_get_info(ctx, C.byref(info)))
+    return info
+
+
+def im_env_step_fused(ctx, bufs, stream=None):
+    _check(lib().im_env_step_fused(ctx, C.byref(bufs), stream))
+
+
+def im_policy_act(ctx, obs_ptr, ld_obs, env_n_ptr, n_envs, mean_ptr, action_ptr, logp_ptr,
+                  stream=None):
+    _check(lib().im_policy_act(ctx, obs_ptr, int(ld_obs), env_n_ptr, int(n_envs), mean_ptr,
+                               action_ptr, logp_ptr, stream))
+
+
+def im_reset_envs(ctx, bufs, mask_ptr=None, stream=None):
+    _check(lib().im_reset_envs(ctx, C.byref(bufs), mask_ptr, stream))
+
+
+def im_standin_physics(ctx, bufs, sigma_joint, sigma_vel, stream=None):
+    _check(lib().im_standin_physics(ctx, C.byref(bufs), float(sigma_joint), float(sigma_vel),
+                                    stream))
+
+
+# ------------------------------------------------------------- conveniences
+def _f32(a):
+    return np.ascontiguousarray(a, np.float32)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, np.int32)
+
+
+def _ptr(a, ct):
+    return a.ctypes.data_as(C.POINTER(ct))
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _dptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+class EnvBuffers:
+    """Device buffers of a batch of envs (torch tensors) in the library layout."""
+
+    def __init__(self, n_bodies, n_envs, ld=None, device="cuda"):
+        import torch
+        B = n_bodies
+        ld = int(ld if ld is not None else n_envs)
+        self.B, self.n_envs, self.ld = B, int(n_envs), ld
+        f = dict(device=device, dtype=torch.float32)
+        self.body_pos = torch.zeros((B, 3, ld), **f)
+        self.body_quat = torch.zeros((B, 4, ld), **f)
+        self.body_linvel = torch.zeros((B, 3, ld), **f)
+        self.body_angvel = torch.zeros((B, 3, ld), **f)
+        self.env_clip = torch.zeros(ld, device=device, dtype=torch.int32)
+        self.env_phase = torch.zeros(ld, **f)
+        self.env_t = torch.zeros(ld, device=device, dtype=torch.int32)
+        self.env_n = torch.zeros(ld, device=device, dtype=torch.int32)  # uint32 bits
+        self.reward = torch.zeros(ld, **f)
+        self.terminated = torch.zeros(ld, device=device, dtype=torch.uint8)
+        self.truncated = torch.zeros(ld, device=device, dtype=torch.uint8)
+        self.obs = torch.zeros((15 * B + 1, ld), **f)
+        self.ref_frame = torch.zeros(ld, device=device, dtype=torch.int32)
+
+    def struct(self, with_ref_frame=True):
+        return ImEnvBufs(
+            self.body_pos.data_ptr(), self.body_quat.data_ptr(), self.body_linvel.data_ptr(),
+            self.body_angvel.data_ptr(), self.env_clip.data_ptr(), self.env_phase.data_ptr(),
+            self.env_t.data_ptr(), self.env_n.data_ptr(), self.reward.data_ptr(),
+            self.terminated.data_ptr(), self.truncated.data_ptr(), self.obs.data_ptr(),
+            self.ref_frame.data_ptr() if with_ref_frame else None, self.n_envs, self.ld)
+
+    SIM = ("body_pos", "body_quat", "body_linvel", "body_angvel")
+    ENV = ("env_clip", "env_phase", "env_t", "env_n")
+
+
+class Context:
+    """A library context built from a synthetic world description."""
+
+    def __init__(self, desc, max_envs):
+        sk = desc["skeleton"]
+        cfg = desc["config"]
+        pol = desc["policy"]
+        keep = self._keep = []
+
+        def k(a):
+            keep.append(a)
+            return a
+
+        self.cfg = ImConfig(float(cfg["dt"]), float(cfg["h_term"]), float(cfg["r_min"]),
+                            int(cfg["grace"]), float(cfg["c_pose"]), float(cfg["w_pos"]),
+                            float(cfg["w_ee"]), float(cfg["c_vel"]), float(cfg["w_vel"]),
+                            float(cfg["c_com"]), float(cfg["w_com"]), int(cfg["seed"]))
+        self.skel = ImSkeleton(int(sk["n_bodies"]), _ptr(k(_i32(sk["parent"])), C.c_int32),
+                               _ptr(k(_i32(sk["jtype"])), C.c_int32),
+                               _ptr(k(_f32(sk["axis"])), C.c_float),
+                               _ptr(k(_f32(sk["offset"])), C.c_float),
+                               _ptr(k(_f32(sk["mass"])), C.c_float))
+        clips = desc["clips"]
+        arr = (ImClip * len(clips))()
+        for i, c in enumerate(clips):
+            arr[i] = ImClip(int(c["n_frames"]), float(c["fps"]),
+                            _ptr(k(_f32(c["root_pos"])), C.c_float),
+                            _ptr(k(_f32(c["root_quat"])), C.c_float),
+                            _ptr(k(_f32(c["local_quat"])), C.c_float))
+        self.clips = arr
+        L = len(pol["W"])
+        dims = k(_i32(pol["dims"]))
+        bf16 = bool(pol["bf16"])
+        wptrs = (C.c_void_p * L)()
+        bptrs = (C.POINTER(C.c_float) * L)()
+        for l in range(L):
+            w = _f32(pol["W"][l])
+            if bf16:
+                w = k(np.ascontiguousarray((w.view(np.uint32) >> 16).astype(np.uint16)))
+            else:
+                w = k(w)
+            wptrs[l] = w.ctypes.data
+            bptrs[l] = _ptr(k(_f32(pol["b"][l])), C.c_float)
+        self.policy = ImPolicy(L, _ptr(dims, C.c_int32), IM_DTYPE_BF16 if bf16 else IM_DTYPE_F32,
+                               wptrs, bptrs, _ptr(k(_f32(pol["log_std"])), C.c_float))
+        self.ptr = im_create(self.cfg, self.skel, self.clips, len(clips), self.policy, max_envs)
+        self.info = im_get_info(self.ptr)
+
+    def close(self):
+        if getattr(self, "ptr", None):
+            im_destroy(self.ptr)
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- calls on tensors
+    def buffers(self, n_envs, ld=None):
+        return EnvBuffers(self.info.n_bodies, n_envs, ld)
+
+    def env_step_fused(self, bufs, stream=None, with_ref_frame=True):
+        im_env_step_fused(self.ptr, bufs.struct(with_ref_frame), _stream(stream))
+
+    def reset_envs(self, bufs, mask=None, stream=None):
+        im_reset_envs(self.ptr, bufs.struct(), _dptr(mask), _stream(stream))
+
+    def standin_physics(self, bufs, sigma_joint, sigma_vel, stream=None):
+        im_standin_physics(self.ptr, bufs.struct(), sigma_joint, sigma_vel, _stream(stream))
+
+    def policy_act(self, obs, env_n, n_envs, mean, action, logp=None, stream=None):
+        im_policy_act(self.ptr, _dptr(obs), obs.shape[1], _dptr(env_n), n_envs, _dptr(mean),
+                      _dptr(action), _dptr(logp), _stream(stream))

@@ -1,0 +1,560 @@
+// api.hip -- the C ABI: validation, table preparation and kernel dispatch.
+//
+// Creation may allocate and synchronise; the hot calls only validate their
+// arguments on the host and enqueue kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/instantmimic.h"
+#include "launch.h"
+
+using namespace im;
+
+// Parked frames of nested branch points live in LDS (20 floats per slot and
+// thread in the stand-in, 256 threads per block): 3 slots keep a block within
+// 64 KB.  Humanoid trees need 2.
+#define IM_MAX_BRANCH_NESTING 3
+
+struct im_ctx {
+    int device = -1;
+    int B = 0, D = 0, A = 0, n_clips = 0, L = 0, dtype = 0, n_slots = 0, max_depth = 0;
+    int64_t max_envs = 0;
+    im_config cfg{};
+    SkelTab *d_skel = nullptr;
+    ClipTab *d_clips = nullptr;
+    float4 *d_seg = nullptr;
+    std::vector<int> dims, M_pad, K_pad;
+    std::vector<void *> d_w;
+    std::vector<float *> d_b;
+    float *d_log_std = nullptr;
+    void *d_ws[2] = {nullptr, nullptr};
+    int64_t device_bytes = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+im_status fail(im_status s, const std::string &msg)
+{
+    g_err = msg;
+    return s;
+}
+
+im_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(IM_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+bool finite_f(float x) { return std::isfinite(x); }
+
+bool unit_quat(const float *q, double tol)
+{
+    const double n = std::sqrt((double)q[0] * q[0] + (double)q[1] * q[1] + (double)q[2] * q[2] +
+                               (double)q[3] * q[3]);
+    return std::isfinite(n) && std::fabs(n - 1.0) <= tol;
+}
+
+void free_ctx(im_ctx *c)
+{
+    if (!c) return;
+    hipFree(c->d_skel);
+    hipFree(c->d_clips);
+    hipFree(c->d_seg);
+    for (void *p : c->d_w) hipFree(p);
+    for (float *p : c->d_b) hipFree(p);
+    hipFree(c->d_log_std);
+    hipFree(c->d_ws[0]);
+    hipFree(c->d_ws[1]);
+    delete c;
+}
+
+template <class T>
+hipError_t dev_alloc(im_ctx *c, T **p, size_t bytes)
+{
+    hipError_t e = hipMalloc((void **)p, bytes);
+    if (e == hipSuccess) c->device_bytes += (int64_t)bytes;
+    return e;
+}
+
+// Preorder tables of the skeleton (host).  Returns an error message or "".
+std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
+{
+    const int B = sk->n_bodies;
+    std::memset(t, 0, sizeof(*t));
+    std::vector<std::vector<int>> ch(B);
+    for (int b = 1; b < B; ++b) ch[sk->parent[b]].push_back(b);
+    std::vector<int> order, depth(B, 0);
+    std::vector<int> st{0};
+    while (!st.empty()) {
+        const int b = st.back();
+        st.pop_back();
+        order.push_back(b);
+        for (auto it = ch[b].rbegin(); it != ch[b].rend(); ++it) {
+            depth[*it] = depth[b] + 1;
+            st.push_back(*it);
+        }
+    }
+    // nesting level of branch points = number of branch-point proper ancestors
+    std::vector<int> nest(B, 0), slot(B, -1);
+    int n_slots = 0;
+    for (int b = 1; b < B; ++b) {
+        const int p = sk->parent[b];
+        nest[b] = nest[p] + (ch[p].size() >= 2 ? 1 : 0);
+    }
+    for (int b = 0; b < B; ++b)
+        if (ch[b].size() >= 2) {
+            slot[b] = nest[b];
+            n_slots = std::max(n_slots, nest[b] + 1);
+        }
+    // rotational DoFs in body index order (stand-in noise indices)
+    std::vector<int> zrot(B, -1);
+    int z = 3;
+    for (int b = 1; b < B; ++b) {
+        if (sk->jtype[b] == IM_JOINT_SPHERICAL) {
+            zrot[b] = z;
+            z += 3;
+        } else if (sk->jtype[b] == IM_JOINT_REVOLUTE) {
+            zrot[b] = z;
+            z += 1;
+        }
+    }
+    double msum = 0.0;
+    for (int b = 0; b < B; ++b) msum += (double)sk->mass[b];
+    t->B = B;
+    t->n_slots = n_slots;
+    t->n_dof = z - 3;
+    *max_depth = 0;
+    for (int i = 0; i < B; ++i) {
+        const int b = order[i];
+        t->body[i] = b;
+        t->depth[i] = depth[b];
+        *max_depth = std::max(*max_depth, depth[b]);
+        t->bslot[i] = slot[b];
+        t->pslot[i] = -1;
+        if (i > 0 && sk->parent[b] != order[i - 1]) {
+            const int p = sk->parent[b];
+            if (slot[p] < 0) return "internal: preorder parent is not a branch point";
+            t->pslot[i] = slot[p];
+        }
+        t->jtype[i] = sk->jtype[b];
+        t->leaf[i] = ch[b].empty() ? 1 : 0;
+        t->zrot[i] = zrot[b];
+        for (int c = 0; c < 3; ++c) {
+            t->offset[i][c] = sk->offset[3 * b + c];
+            t->axis[i][c] = sk->axis[3 * b + c];
+        }
+        t->massw[i] = (float)((double)sk->mass[b] / msum);
+    }
+    return "";
+}
+
+std::string validate(const im_config *cfg, const im_skeleton *sk, const im_clip *clips,
+                     int32_t n_clips, const im_policy *pol, int64_t max_envs, im_status *code)
+{
+    *code = IM_ERR_INVALID_ARG;
+    if (!cfg || !sk || !clips || !pol) return "NULL description pointer";
+    if (!(cfg->dt > 0.0) || !std::isfinite(cfg->dt)) return "dt must be positive and finite";
+    if (!finite_f(cfg->h_term) || !finite_f(cfg->r_min)) return "thresholds must be finite";
+    if (cfg->grace < 0) return "grace must be >= 0";
+    const float wts[7] = {cfg->c_pose, cfg->w_pos, cfg->w_ee, cfg->c_vel,
+                          cfg->w_vel,  cfg->c_com, cfg->w_com};
+    for (float w : wts)
+        if (!finite_f(w)) return "reward weights must be finite";
+    const int B = sk->n_bodies;
+    if (B < 1) return "n_bodies must be >= 1";
+    if (B > IM_MAX_BODIES) {
+        *code = IM_ERR_UNSUPPORTED;
+        return "more than IM_MAX_BODIES bodies";
+    }
+    if (!sk->parent || !sk->jtype || !sk->axis || !sk->offset || !sk->mass)
+        return "NULL skeleton array";
+    if (sk->parent[0] != -1) return "parent[0] must be -1";
+    if (sk->jtype[0] != IM_JOINT_FREE) return "body 0 must have a free joint";
+    for (int b = 0; b < B; ++b) {
+        if (b > 0 && (sk->parent[b] < 0 || sk->parent[b] >= b))
+            return "parent[b] must satisfy 0 <= parent[b] < b (body " + std::to_string(b) + ")";
+        if (b > 0 && sk->jtype[b] != IM_JOINT_SPHERICAL && sk->jtype[b] != IM_JOINT_REVOLUTE &&
+            sk->jtype[b] != IM_JOINT_FIXED)
+            return "invalid joint type at body " + std::to_string(b);
+        if (!(sk->mass[b] > 0.0f) || !finite_f(sk->mass[b])) return "masses must be positive";
+        for (int c = 0; c < 3; ++c)
+            if (!finite_f(sk->offset[3 * b + c]) || !finite_f(sk->axis[3 * b + c]))
+                return "offsets/axes must be finite";
+        if (b > 0 && sk->jtype[b] == IM_JOINT_REVOLUTE) {
+            const float *a = sk->axis + 3 * b;
+            const double n = std::sqrt((double)a[0] * a[0] + (double)a[1] * a[1] + (double)a[2] * a[2]);
+            if (std::fabs(n - 1.0) > 1e-3) return "revolute axis must be unit";
+        }
+    }
+    if (n_clips < 1) return "n_clips must be >= 1";
+    for (int k = 0; k < n_clips; ++k) {
+        const im_clip &c = clips[k];
+        if (c.n_frames < 2) return "clip " + std::to_string(k) + ": n_frames must be >= 2";
+        if (!(c.fps > 0.0f) || !finite_f(c.fps)) return "clip fps must be positive";
+        if (!c.root_pos || !c.root_quat || (B > 1 && !c.local_quat)) return "NULL clip array";
+        for (int f = 0; f < c.n_frames; ++f) {
+            for (int i = 0; i < 3; ++i)
+                if (!finite_f(c.root_pos[3 * f + i])) return "clip root positions must be finite";
+            if (!unit_quat(c.root_quat + 4 * f, 1e-3)) return "clip root quaternion not unit";
+            for (int b = 1; b < B; ++b) {
+                const float *q = c.local_quat + 4 * ((int64_t)f * (B - 1) + (b - 1));
+                if (sk->jtype[b] == IM_JOINT_FIXED) {
+                    if (std::fabs(std::fabs(q[0]) - 1.0f) > 1e-3f || std::fabs(q[1]) > 1e-3f ||
+                        std::fabs(q[2]) > 1e-3f || std::fabs(q[3]) > 1e-3f)
+                        return "fixed joint with a non-identity clip rotation";
+                } else if (!unit_quat(q, 1e-3)) {
+                    return "clip joint quaternion not unit (clip " + std::to_string(k) + ")";
+                }
+            }
+        }
+    }
+    const int L = pol->n_layers;
+    if (L < 1 || !pol->dims || !pol->weight || !pol->bias || !pol->log_std)
+        return "policy description incomplete";
+    if (pol->dtype != IM_DTYPE_F32 && pol->dtype != IM_DTYPE_BF16) return "invalid policy dtype";
+    if (pol->dims[0] != 15 * B + 1) return "policy input width must be 15*B+1";
+    for (int l = 0; l <= L; ++l)
+        if (pol->dims[l] < 1 || pol->dims[l] > 16384) return "layer widths must be in [1, 16384]";
+    if (pol->dims[L] > 128) {
+        *code = IM_ERR_UNSUPPORTED;
+        return "action width above 128";
+    }
+    for (int l = 0; l < L; ++l)
+        if (!pol->weight[l] || !pol->bias[l]) return "NULL weight or bias";
+    for (int a = 0; a < pol->dims[L]; ++a)
+        if (!finite_f(pol->log_std[a])) return "log_std must be finite";
+    if (max_envs < 1 || max_envs > (int64_t)0xFFFFFFFF) return "max_envs must be in [1, 2^32)";
+    *code = IM_OK;
+    return "";
+}
+
+im_status check_device(const im_ctx *c)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != c->device) return fail(IM_ERR_INVALID_ARG, "call made on another device than the context's");
+    return IM_OK;
+}
+
+im_status check_env_bufs(const im_ctx *c, const im_env_bufs *b, bool need_outputs)
+{
+    if (!b) return fail(IM_ERR_INVALID_ARG, "NULL buffers");
+    if (b->n_envs < 0 || b->n_envs > (int64_t)0xFFFFFFFF) return fail(IM_ERR_INVALID_ARG, "bad n_envs");
+    if (b->ld < b->n_envs || b->ld < 1) return fail(IM_ERR_INVALID_ARG, "ld must be >= n_envs and >= 1");
+    if (!b->body_pos || !b->body_quat || !b->body_linvel || !b->body_angvel || !b->env_clip ||
+        !b->env_phase || !b->env_t || !b->env_n || !b->obs)
+        return fail(IM_ERR_INVALID_ARG, "NULL env buffer");
+    if (need_outputs && (!b->reward || !b->terminated || !b->truncated))
+        return fail(IM_ERR_INVALID_ARG, "NULL output buffer");
+    (void)c;
+    return IM_OK;
+}
+
+EnvArgs env_args(const im_ctx *c, const im_env_bufs *b)
+{
+    EnvArgs a{};
+    a.sk = c->d_skel;
+    a.clips = c->d_clips;
+    a.seg = c->d_seg;
+    a.pos = b->body_pos;
+    a.quat = b->body_quat;
+    a.linvel = b->body_linvel;
+    a.angvel = b->body_angvel;
+    a.env_clip = b->env_clip;
+    a.env_phase = b->env_phase;
+    a.env_t = b->env_t;
+    a.env_n = b->env_n;
+    a.reward = b->reward;
+    a.term = b->terminated;
+    a.trunc = b->truncated;
+    a.obs = b->obs;
+    a.ref_frame = b->ref_frame;
+    a.mask = nullptr;
+    a.n = b->n_envs;
+    a.ld = b->ld;
+    a.seed = c->cfg.seed;
+    a.n_clips = c->n_clips;
+    a.grace = c->cfg.grace;
+    a.h_term = c->cfg.h_term;
+    a.r_min = c->cfg.r_min;
+    a.c_pose = c->cfg.c_pose;
+    a.w_pos = c->cfg.w_pos;
+    a.w_ee = c->cfg.w_ee;
+    a.c_vel = c->cfg.c_vel;
+    a.w_vel = c->cfg.w_vel;
+    a.c_com = c->cfg.c_com;
+    a.w_com = c->cfg.w_com;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *im_status_str(im_status s)
+{
+    switch (s) {
+        case IM_OK: return "IM_OK";
+        case IM_ERR_INVALID_ARG: return "IM_ERR_INVALID_ARG";
+        case IM_ERR_UNSUPPORTED: return "IM_ERR_UNSUPPORTED";
+        case IM_ERR_OOM: return "IM_ERR_OOM";
+        case IM_ERR_HIP: return "IM_ERR_HIP";
+    }
+    return "unknown im_status";
+}
+
+const char *im_last_error(void) { return g_err.c_str(); }
+
+im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *clips,
+                    int32_t n_clips, const im_policy *pol, int64_t max_envs, im_ctx **out)
+{
+    if (!out) return fail(IM_ERR_INVALID_ARG, "NULL out pointer");
+    *out = nullptr;
+    im_status code;
+    std::string msg = validate(cfg, sk, clips, n_clips, pol, max_envs, &code);
+    if (code != IM_OK) return fail(code, msg);
+
+    SkelTab tab;
+    int max_depth = 0;
+    msg = build_skeleton(sk, &tab, &max_depth);
+    if (!msg.empty()) return fail(IM_ERR_INVALID_ARG, msg);
+    if (tab.n_slots > IM_MAX_BRANCH_NESTING)
+        return fail(IM_ERR_UNSUPPORTED, "branch points nested deeper than " +
+                                            std::to_string(IM_MAX_BRANCH_NESTING));
+
+    im_ctx *c = new im_ctx();
+    hipError_t e = hipGetDevice(&c->device);
+    if (e != hipSuccess) {
+        free_ctx(c);
+        return hip_fail(e, "hipGetDevice");
+    }
+    c->B = sk->n_bodies;
+    c->D = 15 * c->B + 1;
+    c->L = pol->n_layers;
+    c->A = pol->dims[c->L];
+    c->n_clips = n_clips;
+    c->dtype = pol->dtype;
+    c->n_slots = tab.n_slots;
+    c->max_depth = max_depth;
+    c->max_envs = max_envs;
+    c->cfg = *cfg;
+
+#define IM_TRY_ALLOC(ptr, bytes)                                                              \
+    do {                                                                                      \
+        if (dev_alloc(c, &(ptr), (bytes)) != hipSuccess) {                                    \
+            free_ctx(c);                                                                      \
+            return fail(IM_ERR_OOM, "device allocation failed (" + std::to_string(bytes) +    \
+                                        " bytes)");                                           \
+        }                                                                                     \
+    } while (0)
+#define IM_TRY_HIP(call, what)                                                                \
+    do {                                                                                      \
+        hipError_t e_ = (call);                                                               \
+        if (e_ != hipSuccess) {                                                               \
+            im_status s_ = hip_fail(e_, what);                                                \
+            free_ctx(c);                                                                      \
+            return s_;                                                                        \
+        }                                                                                     \
+    } while (0)
+
+    // skeleton and per-clip tables
+    IM_TRY_ALLOC(c->d_skel, sizeof(SkelTab));
+    IM_TRY_HIP(hipMemcpy(c->d_skel, &tab, sizeof(SkelTab), hipMemcpyHostToDevice), "upload skeleton");
+    std::vector<ClipTab> ct(n_clips);
+    int64_t seg_total = 0;
+    const int stride = seg_stride(c->B);
+    for (int k = 0; k < n_clips; ++k) {
+        const int F = clips[k].n_frames;
+        ct[k].F = F;
+        ct[k].dphi = (float)(cfg->dt * (double)clips[k].fps / (double)(F - 1));
+        ct[k].fm1 = (float)(F - 1);
+        if (seg_total > (int64_t)0x7FFFFFFF) {
+            free_ctx(c);
+            return fail(IM_ERR_UNSUPPORTED, "segment table too large");
+        }
+        ct[k].seg_base = (int32_t)seg_total;
+        seg_total += (int64_t)(F - 1) * stride;
+    }
+    IM_TRY_ALLOC(c->d_clips, sizeof(ClipTab) * n_clips);
+    IM_TRY_HIP(hipMemcpy(c->d_clips, ct.data(), sizeof(ClipTab) * n_clips, hipMemcpyHostToDevice),
+               "upload clip table");
+    IM_TRY_ALLOC(c->d_seg, sizeof(float4) * seg_total);
+
+    // reference segments: upload each clip's frames and pack them on the device
+    for (int k = 0; k < n_clips; ++k) {
+        const int F = clips[k].n_frames;
+        const size_t nrp = 3 * (size_t)F, nrq = 4 * (size_t)F,
+                     nlq = 4 * (size_t)F * (size_t)std::max(c->B - 1, 1);
+        float *tmp = nullptr;
+        if (hipMalloc((void **)&tmp, sizeof(float) * (nrp + nrq + nlq)) != hipSuccess) {
+            free_ctx(c);
+            return fail(IM_ERR_OOM, "device allocation failed (clip staging)");
+        }
+        hipError_t err = hipMemcpy(tmp, clips[k].root_pos, sizeof(float) * nrp, hipMemcpyHostToDevice);
+        if (err == hipSuccess)
+            err = hipMemcpy(tmp + nrp, clips[k].root_quat, sizeof(float) * nrq, hipMemcpyHostToDevice);
+        if (err == hipSuccess && c->B > 1)
+            err = hipMemcpy(tmp + nrp + nrq, clips[k].local_quat,
+                            sizeof(float) * 4 * (size_t)F * (size_t)(c->B - 1), hipMemcpyHostToDevice);
+        if (err == hipSuccess)
+            err = launch_pack_segments(c->d_skel, F, (double)clips[k].fps, tmp, tmp + nrp,
+                                       tmp + nrp + nrq, c->d_seg + ct[k].seg_base, nullptr);
+        if (err == hipSuccess) err = hipDeviceSynchronize();
+        hipFree(tmp);
+        if (err != hipSuccess) {
+            free_ctx(c);
+            return hip_fail(err, "pack reference segments");
+        }
+    }
+
+    // policy: zero-padded weight layout [M_pad][K_pad], biases [M_pad]
+    const size_t esz = pol->dtype == IM_DTYPE_BF16 ? 2 : 4;
+    c->dims.assign(pol->dims, pol->dims + c->L + 1);
+    c->M_pad.resize(c->L);
+    c->K_pad.resize(c->L);
+    int64_t ws_width = 0;
+    for (int l = 0; l < c->L; ++l) {
+        const bool last = l == c->L - 1;
+        c->M_pad[l] = (int)round_up(c->dims[l + 1], last ? 32 : 128);
+        c->K_pad[l] = l == 0 ? (int)round_up(c->dims[0], 32) : c->M_pad[l - 1];
+        if (!last) ws_width = std::max<int64_t>(ws_width, c->M_pad[l]);
+        const int M = c->dims[l + 1], K = c->dims[l];
+        std::vector<uint8_t> wbuf((size_t)c->M_pad[l] * c->K_pad[l] * esz, 0);
+        for (int m = 0; m < M; ++m)
+            std::memcpy(wbuf.data() + ((size_t)m * c->K_pad[l]) * esz,
+                        (const uint8_t *)pol->weight[l] + (size_t)m * K * esz, (size_t)K * esz);
+        std::vector<float> bbuf(c->M_pad[l], 0.0f);
+        std::memcpy(bbuf.data(), pol->bias[l], sizeof(float) * M);
+        void *dw = nullptr;
+        float *db = nullptr;
+        IM_TRY_ALLOC(dw, wbuf.size());
+        c->d_w.push_back(dw);
+        IM_TRY_ALLOC(db, sizeof(float) * bbuf.size());
+        c->d_b.push_back(db);
+        IM_TRY_HIP(hipMemcpy(dw, wbuf.data(), wbuf.size(), hipMemcpyHostToDevice), "upload weights");
+        IM_TRY_HIP(hipMemcpy(db, bbuf.data(), sizeof(float) * bbuf.size(), hipMemcpyHostToDevice),
+                   "upload biases");
+    }
+    IM_TRY_ALLOC(c->d_log_std, sizeof(float) * c->A);
+    IM_TRY_HIP(hipMemcpy(c->d_log_std, pol->log_std, sizeof(float) * c->A, hipMemcpyHostToDevice),
+               "upload log_std");
+    if (c->L >= 2) {
+        const size_t wsb = (size_t)max_envs * (size_t)ws_width * esz;
+        IM_TRY_ALLOC(c->d_ws[0], wsb);
+        if (c->L >= 3) IM_TRY_ALLOC(c->d_ws[1], wsb);
+    }
+#undef IM_TRY_ALLOC
+#undef IM_TRY_HIP
+    *out = c;
+    return IM_OK;
+}
+
+im_status im_destroy(im_ctx *ctx)
+{
+    if (!ctx) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    free_ctx(ctx);
+    return IM_OK;
+}
+
+im_status im_get_info(const im_ctx *c, im_info *info)
+{
+    if (!c || !info) return fail(IM_ERR_INVALID_ARG, "NULL argument");
+    info->n_bodies = c->B;
+    info->obs_dim = c->D;
+    info->action_dim = c->A;
+    info->n_clips = c->n_clips;
+    info->n_layers = c->L;
+    info->policy_dtype = c->dtype;
+    info->max_depth = c->max_depth;
+    info->max_envs = c->max_envs;
+    info->device_bytes = c->device_bytes;
+    return IM_OK;
+}
+
+im_status im_env_step_fused(im_ctx *c, const im_env_bufs *b, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_env_bufs(c, b, true);
+    if (s != IM_OK) return s;
+    if ((s = check_device(c)) != IM_OK) return s;
+    const EnvArgs a = env_args(c, b);
+    hipError_t e = launch_env_step(c->n_slots, a, (hipStream_t)stream);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "env_step launch");
+}
+
+im_status im_reset_envs(im_ctx *c, const im_env_bufs *b, const uint8_t *mask, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_env_bufs(c, b, false);
+    if (s != IM_OK) return s;
+    if ((s = check_device(c)) != IM_OK) return s;
+    EnvArgs a = env_args(c, b);
+    a.mask = mask;
+    hipError_t e = launch_reset(c->n_slots, a, (hipStream_t)stream);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "reset launch");
+}
+
+im_status im_standin_physics(im_ctx *c, const im_env_bufs *b, float sigma_joint, float sigma_vel,
+                             void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_env_bufs(c, b, false);
+    if (s != IM_OK) return s;
+    if (!finite_f(sigma_joint) || !finite_f(sigma_vel) || sigma_joint < 0.0f || sigma_vel < 0.0f)
+        return fail(IM_ERR_INVALID_ARG, "sigmas must be finite and >= 0");
+    if ((s = check_device(c)) != IM_OK) return s;
+    EnvArgs a = env_args(c, b);
+    a.sigma_joint = sigma_joint;
+    a.sigma_vel = sigma_vel;
+    hipError_t e = launch_standin(c->n_slots, a, (hipStream_t)stream);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "stand-in launch");
+}
+
+im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                        int64_t n_envs, float *mean, float *action, float *logp, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (!obs || !env_n || !mean || !action) return fail(IM_ERR_INVALID_ARG, "NULL buffer");
+    if (n_envs < 0 || n_envs > c->max_envs) return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
+    if (ld_obs < n_envs || ld_obs < 1) return fail(IM_ERR_INVALID_ARG, "ld_obs must be >= n_envs");
+    im_status s = check_device(c);
+    if (s != IM_OK) return s;
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    for (int l = 0; l < c->L; ++l) {
+        GemmArgs g{};
+        const bool last = l == c->L - 1;
+        g.x = l == 0 ? (const void *)obs : c->d_ws[(l - 1) & 1];
+        g.ld_x = l == 0 ? ld_obs : c->M_pad[l - 1];
+        g.w = c->d_w[l];
+        g.bias = c->d_b[l];
+        g.K_pad = c->K_pad[l];
+        g.K_valid = l == 0 ? c->D : c->K_pad[l];
+        g.N = n_envs;
+        if (!last) {
+            g.y = c->d_ws[l & 1];
+            g.ld_y = c->M_pad[l];
+        } else {
+            g.mean = mean;
+            g.action = action;
+            g.logp = logp;
+            g.env_n = env_n;
+            g.log_std = c->d_log_std;
+            g.A = c->A;
+            g.seed = c->cfg.seed;
+        }
+        hipError_t e = launch_policy_layer(bf16, l == 0, last, g, c->M_pad[l], (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "policy layer launch");
+    }
+    return IM_OK;
+}
+
+}  // extern "C"

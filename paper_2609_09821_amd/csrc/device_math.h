@@ -1,0 +1,125 @@
+// device_math.h -- fp32 vector/quaternion algebra, counter-based random
+// numbers and small polynomial kernels used by the env and policy kernels.
+// Quaternions are (w, x, y, z), Hamilton product, active rotations.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace im {
+
+struct f3 {
+    float x, y, z;
+};
+struct q4 {
+    float w, x, y, z;
+};
+
+__device__ __forceinline__ f3 mk3(float x, float y, float z) { return f3{x, y, z}; }
+__device__ __forceinline__ f3 operator+(f3 a, f3 b) { return f3{a.x + b.x, a.y + b.y, a.z + b.z}; }
+__device__ __forceinline__ f3 operator-(f3 a, f3 b) { return f3{a.x - b.x, a.y - b.y, a.z - b.z}; }
+__device__ __forceinline__ f3 operator*(float s, f3 a) { return f3{s * a.x, s * a.y, s * a.z}; }
+__device__ __forceinline__ float dot3(f3 a, f3 b) { return a.x * b.x + a.y * b.y + a.z * b.z; }
+__device__ __forceinline__ f3 cross3(f3 a, f3 b)
+{
+    return f3{a.y * b.z - a.z * b.y, a.z * b.x - a.x * b.z, a.x * b.y - a.y * b.x};
+}
+
+__device__ __forceinline__ q4 qmul(q4 a, q4 b)
+{
+    return q4{a.w * b.w - a.x * b.x - a.y * b.y - a.z * b.z,
+              a.w * b.x + a.x * b.w + a.y * b.z - a.z * b.y,
+              a.w * b.y - a.x * b.z + a.y * b.w + a.z * b.x,
+              a.w * b.z + a.x * b.y - a.y * b.x + a.z * b.w};
+}
+
+// R(q) v for a unit q: v + w t + u x t with t = 2 u x v.
+__device__ __forceinline__ f3 qrot(q4 q, f3 v)
+{
+    f3 u{q.x, q.y, q.z};
+    f3 t = 2.0f * cross3(u, v);
+    return v + q.w * t + cross3(u, t);
+}
+
+// sin and cos on [0, pi/2] from their Taylor series (truncation error below
+// 1e-9 there), evaluated with Horner's rule.  Slerp only needs angles in
+// this range: after the hemisphere flip the angle between two unit
+// quaternions is at most pi/2 and the blend weight is in [0, 1].
+__device__ __forceinline__ void sincos_q1(float x, float *s, float *c)
+{
+    const float x2 = x * x;
+    float ps = 1.0f / 6227020800.0f;          // 1/13!
+    ps = ps * x2 - 1.0f / 39916800.0f;        // 1/11!
+    ps = ps * x2 + 1.0f / 362880.0f;          // 1/9!
+    ps = ps * x2 - 1.0f / 5040.0f;            // 1/7!
+    ps = ps * x2 + 1.0f / 120.0f;             // 1/5!
+    ps = ps * x2 - 1.0f / 6.0f;               // 1/3!
+    *s = x + (x * x2) * ps;
+    float pc = -1.0f / 87178291200.0f;        // 1/14!
+    pc = pc * x2 + 1.0f / 479001600.0f;       // 1/12!
+    pc = pc * x2 - 1.0f / 3628800.0f;         // 1/10!
+    pc = pc * x2 + 1.0f / 40320.0f;           // 1/8!
+    pc = pc * x2 - 1.0f / 720.0f;             // 1/6!
+    pc = pc * x2 + 1.0f / 24.0f;              // 1/4!
+    pc = pc * x2 - 0.5f;                      // 1/2!
+    *c = 1.0f + x2 * pc;
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the
+// two-multiplier round function, Weyl-sequence key schedule.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint4 philox4x32_10(uint4 ctr, uint32_t k0, uint32_t k1)
+{
+    uint32_t c0 = ctr.x, c1 = ctr.y, c2 = ctr.z, c3 = ctr.w;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+        const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return make_uint4(c0, c1, c2, c3);
+}
+
+// Word -> (0, 1): odd multiples of 2^-24 (exact in fp32).
+__device__ __forceinline__ float uniform_open(uint32_t x)
+{
+    return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
+}
+
+// Box-Muller: two words -> two standard normals (cos, sin branch).
+__device__ __forceinline__ void box_muller(uint32_t a, uint32_t b, float *z0, float *z1)
+{
+    const float u = uniform_open(a), v = uniform_open(b);
+    const float r = sqrtf(-2.0f * logf(u));
+    float s, c;
+    sincospif(2.0f * v, &s, &c);
+    *z0 = r * c;
+    *z1 = r * s;
+}
+
+__device__ __forceinline__ void normals4(uint64_t seed, uint32_t e, uint32_t n, uint32_t blk,
+                                         uint32_t tag, float z[4])
+{
+    const uint4 x = philox4x32_10(make_uint4(e, n, blk, tag), (uint32_t)seed,
+                                  (uint32_t)(seed >> 32));
+    box_muller(x.x, x.y, &z[0], &z[1]);
+    box_muller(x.z, x.w, &z[2], &z[3]);
+}
+
+// fp32 -> bf16 bits, round to nearest even (inputs are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+}  // namespace im

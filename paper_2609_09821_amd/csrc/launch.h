@@ -1,0 +1,38 @@
+// launch.h -- argument blocks and host launchers shared by the C ABI layer
+// and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tables.h"
+
+namespace im {
+
+struct GemmArgs {
+    const void *x;       // layer input: obs [K][ld_x] fp32 (first layer) or [N][ld_x] of T
+    int64_t ld_x;
+    const void *w;       // [M_pad][K_pad] of T
+    const float *bias;   // [M_pad]
+    int K_pad, K_valid;  // K_valid: rows of the observation that exist
+    int64_t N;
+    void *y;             // hidden output [N][ld_y] of T
+    int64_t ld_y;
+    // sampling epilogue
+    float *mean, *action, *logp;
+    const uint32_t *env_n;
+    const float *log_std;
+    int A;
+    uint64_t seed;
+};
+
+hipError_t launch_env_step(int n_slots, const EnvArgs &a, hipStream_t s);
+hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s);
+hipError_t launch_standin(int n_slots, const EnvArgs &a, hipStream_t s);
+hipError_t launch_pack_segments(const SkelTab *sk, int F, double fps, const float *root_pos,
+                                const float *root_quat, const float *local_quat, float4 *seg,
+                                hipStream_t s);
+hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmArgs &g, int M_pad,
+                               hipStream_t s);
+
+}  // namespace im

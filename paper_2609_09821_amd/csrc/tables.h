@@ -1,0 +1,75 @@
+// tables.h -- device-resident tables owned by a context and the argument
+// blocks of the env kernels.
+#pragma once
+
+#include <stdint.h>
+
+#include "../../include/instantmimic.h"
+
+namespace im {
+
+// Skeleton, reordered into depth-first preorder: a body's parent is then
+// either the previous body or a branch point whose frame was parked.  Read
+// with wave-uniform loads.
+struct SkelTab {
+    int32_t B;          // bodies
+    int32_t n_slots;    // parked-frame slots needed (nested branch points)
+    int32_t n_dof;      // rotational DoFs of the joints (stand-in noise)
+    int32_t body[IM_MAX_BODIES];   // body index at preorder position i
+    int32_t depth[IM_MAX_BODIES];  // its depth (root 0)
+    int32_t bslot[IM_MAX_BODIES];  // LDS slot of its frame if it has >= 2 children, else -1
+    int32_t pslot[IM_MAX_BODIES];  // slot of its parent if the parent is not the
+                                   // previous body in preorder, else -1
+    int32_t jtype[IM_MAX_BODIES];
+    int32_t leaf[IM_MAX_BODIES];
+    int32_t zrot[IM_MAX_BODIES];   // first stand-in normal of its rotation noise
+    float offset[IM_MAX_BODIES][4];
+    float axis[IM_MAX_BODIES][4];
+    float massw[IM_MAX_BODIES];    // m_b / sum m
+};
+
+// Per clip.  seg_base: float4 index of segment 0 in the segment table.
+struct ClipTab {
+    int32_t F;
+    float dphi;   // float(dt * fps / (F - 1))
+    float fm1;    // float(F - 1)
+    int32_t seg_base;
+};
+
+// Segment table: for every clip k and segment i0 in [0, F-2], a record of
+// 6 + 3 (B - 1) float4 in preorder:
+//   root   [0] = (A.x, A.y, A.z, d.x)     anchor A = root position of frame i0
+//          [1] = (d.y, d.z, v.x, v.y)     d = P(i0+1) - P(i0), v = d * fps
+//          [2] = (v.z, w.x, w.y, w.z)     w = rotvec(Q1 Q0^-1) * fps (world)
+//          [3] = a                        slerp basis: q(alpha) = cos(alpha W) a
+//          [4] = u                                           + sin(alpha W) u
+//          [5] = (W, 0, 0, 0)
+//   joint  [0] = a, [1] = u, [2] = (w.x, w.y, w.z, W)  (w in the parent frame)
+// a = q0/|q0|, b = +-q1/|q1| on a's hemisphere, W = angle between a and b,
+// u = unit component of b orthogonal to a.
+__host__ __device__ inline int seg_stride(int B) { return 6 + 3 * (B - 1); }
+
+struct EnvArgs {
+    const SkelTab *sk;
+    const ClipTab *clips;
+    const float4 *seg;
+    float *pos, *quat, *linvel, *angvel;
+    int32_t *env_clip;
+    float *env_phase;
+    int32_t *env_t;
+    uint32_t *env_n;
+    float *reward;
+    uint8_t *term, *trunc;
+    float *obs;
+    int32_t *ref_frame;
+    const uint8_t *mask;
+    int64_t n, ld;
+    uint64_t seed;
+    int32_t n_clips;
+    int32_t grace;
+    float h_term, r_min;
+    float c_pose, w_pos, w_ee, c_vel, w_vel, c_com, w_com;
+    float sigma_joint, sigma_vel;
+};
+
+}  // namespace im

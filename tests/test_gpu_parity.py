@@ -1,0 +1,121 @@
+"""GPU parity of the fused step, the reset and the policy against the oracle.
+
+Teacher forcing: each step's sim input comes from the oracle's kinematic
+stand-in evaluated on the oracle's env state (bit-identical to the GPU's), it
+is uploaded, and both implementations step from it.  Sizes span several
+256-env blocks with a ragged tail.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_09821_amd import binding, synth
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+SIZES = {1: 64, 2: 1000, 3: 1300, 4: 700, 5: 1100}
+STEPS = {1: 1, 2: 6, 3: 6, 4: 4, 5: 6}
+
+
+def _setup(cfg, N, ld=None, **over):
+    d = synth.make_world(cfg, n_envs=N, **over)
+    w = oracle.World(d)
+    ctx = binding.Context(d, max_envs=max(N, 1))
+    bufs = ctx.buffers(N, ld)
+    return d, w, ctx, bufs
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_reset_envs_parity(cfg):
+    N = SIZES[cfg]
+    d, w, ctx, bufs = _setup(cfg, N)
+    st = oracle.State(w.B, N)
+    st.n[:] = (np.arange(N, dtype=np.uint32) * 2654435761) & 0xFFFF
+    H.upload_state(st, bufs)
+    ctx.reset_envs(bufs)
+    w.reset_envs(st)
+    g = H.download(bufs, N)
+    for name in ("clip", "phase", "t", "n"):
+        assert np.array_equal(getattr(g, name), getattr(st, name)), name
+    H.compare_sim_obs(g, st, np.ones(N, bool), "reset")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_env_step_parity(cfg):
+    N, T = SIZES[cfg], STEPS[cfg]
+    d, w, ctx, bufs = _setup(cfg, N)
+    c = d["config"]
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    H.upload_state(st, bufs)
+    ctx.reset_envs(bufs)
+    live = np.ones(N, bool)
+    n_done = 0
+    for t in range(T):
+        w.standin(st, d["sigma_joint"], d["sigma_vel"])
+        H.upload_state(st, bufs, env=False)
+        t_next = st.t + 1
+        z_root = st.pos[0, 2].copy()
+        ctx.env_step_fused(bufs)
+        w.env_step(st)
+        g = H.download(bufs, N)
+        live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, live)
+        H.compare_sim_obs(g, st, live, "step %d" % t)
+        n_done += int((st.terminated | st.truncated).sum())
+    assert live.mean() > 0.99
+    print("cfg %d: %d resets over %d steps, %d envs excluded at ties" % (cfg, n_done, T,
+                                                                         int((~live).sum())))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+def test_standin_parity(cfg):
+    N = SIZES[cfg]
+    d, w, ctx, bufs = _setup(cfg, N)
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    st.n[:] += 3
+    H.upload_state(st, bufs)
+    ctx.standin_physics(bufs, d["sigma_joint"], d["sigma_vel"])
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    g = H.download(bufs, N)
+    live = np.ones(N, bool)
+    H.assert_close(g.pos, st.pos, 2e-5, "standin pos")
+    H.assert_quat_close(g.quat, st.quat, 2e-5, "standin quat")
+    H.assert_close(g.linvel, st.linvel, 2e-5, "standin linvel")
+    H.assert_close(g.angvel, st.angvel, 2e-5, "standin angvel")
+    del live
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_policy_parity(cfg):
+    N = SIZES[cfg]
+    d, w, ctx, bufs = _setup(cfg, N)
+    pol = d["policy"]
+    st = oracle.State(w.B, N)
+    st.n[:] = np.arange(N, dtype=np.uint32) * 3 + 11
+    w.reset_envs(st)
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    w.env_step(st)
+    obs = torch.from_numpy(st.obs).cuda()
+    env_n = torch.from_numpy(st.n.view(np.int32)).cuda()
+    A = pol["dims"][-1]
+    mean = torch.zeros((N, A), device="cuda")
+    act = torch.zeros((N, A), device="cuda")
+    logp = torch.zeros(N, device="cuda")
+    ctx.policy_act(obs, env_n, N, mean, act, logp)
+    torch.cuda.synchronize()
+    om, oa, olp = oracle.policy(pol, d["config"]["seed"], st.obs, st.n)
+    tol = 2e-2 if pol["bf16"] else 1e-4
+    for name, gg, oo in (("mean", mean.cpu().numpy(), om), ("action", act.cpu().numpy(), oa)):
+        err = np.linalg.norm(gg - oo, axis=1) / np.linalg.norm(oo, axis=1)
+        assert err.max() <= tol, "%s: worst per-env relative error %.3e" % (name, err.max())
+        print("cfg %d %s: max rel err %.2e" % (cfg, name, err.max()))
+    glp = logp.cpu().numpy()
+    assert np.all(np.abs(glp - olp) <= 1e-5 * np.abs(olp) + 1e-4), np.abs(glp - olp).max()
+    # the noise itself matches tightly: (a - mean)/sigma from each side
+    sig = np.exp(pol["log_std"].astype(np.float64))
+    zg = (act.cpu().numpy() - mean.cpu().numpy()) / sig
+    zo = (oa.astype(np.float64) - om) / sig
+    assert np.abs(zg - zo).max() < 1e-3
