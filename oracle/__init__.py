@@ -84,8 +84,14 @@ def lib():
     L.or_policy.argtypes = [
         C.c_int, _i32p, C.c_int, _f32p, _f32p, _f32p, C.c_uint64, C.c_int64, _f32p, C.c_int64,
         _u32p, _i64p_opt, C.c_int64, _f32p, _f32p, _f32p_opt]
+    L.or_num_threads.argtypes = []
+    L.or_num_threads.restype = C.c_int
     _lib = L
     return L
+
+
+def num_threads():
+    return int(lib().or_num_threads())
 
 
 # ---------------------------------------------------------------- primitives

@@ -976,3 +976,11 @@ void or_policy(int L, const int *dims, int bf16, const float *Wall, const float 
         free(y);
     }
 }
+
+/* Number of OpenMP threads the batch functions use (for timing reports). */
+#ifdef _OPENMP
+#include <omp.h>
+int or_num_threads(void) { return omp_get_max_threads(); }
+#else
+int or_num_threads(void) { return 1; }
+#endif

@@ -424,8 +424,10 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     int64_t ws_width = 0;
     for (int l = 0; l < c->L; ++l) {
         const bool last = l == c->L - 1;
-        c->M_pad[l] = (int)round_up(c->dims[l + 1], last ? 32 : 128);
-        c->K_pad[l] = l == 0 ? (int)round_up(c->dims[0], 32) : c->M_pad[l - 1];
+        // hidden widths padded to the 256-feature macro tile, the action width
+        // to one MFMA tile row (32); K to the 64-element GEMM step
+        c->M_pad[l] = (int)round_up(c->dims[l + 1], last ? 32 : 256);
+        c->K_pad[l] = l == 0 ? (int)round_up(c->dims[0], 64) : c->M_pad[l - 1];
         if (!last) ws_width = std::max<int64_t>(ws_width, c->M_pad[l]);
         const int M = c->dims[l + 1], K = c->dims[l];
         std::vector<uint8_t> wbuf((size_t)c->M_pad[l] * c->K_pad[l] * esz, 0);
@@ -529,11 +531,23 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
     im_status s = check_device(c);
     if (s != IM_OK) return s;
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    const uint64_t esz = bf16 ? 2 : 4;
+    // buffer loads address with 32-bit byte offsets
+    for (int l = 0; l < c->L; ++l) {
+        const uint64_t xb = l == 0 ? (uint64_t)c->D * (uint64_t)ld_obs * 4
+                                   : (uint64_t)n_envs * (uint64_t)c->M_pad[l - 1] * esz;
+        if (xb > 0xFFFFFFF0ull)
+            return fail(IM_ERR_UNSUPPORTED, "policy input of layer " + std::to_string(l) +
+                                                " exceeds 4 GiB");
+    }
     for (int l = 0; l < c->L; ++l) {
         GemmArgs g{};
         const bool last = l == c->L - 1;
         g.x = l == 0 ? (const void *)obs : c->d_ws[(l - 1) & 1];
         g.ld_x = l == 0 ? ld_obs : c->M_pad[l - 1];
+        g.x_bytes = (uint32_t)(l == 0 ? (uint64_t)c->D * (uint64_t)ld_obs * 4
+                                      : (uint64_t)n_envs * (uint64_t)c->M_pad[l - 1] * esz);
+        g.w_bytes = (uint32_t)((uint64_t)c->M_pad[l] * (uint64_t)c->K_pad[l] * esz);
         g.w = c->d_w[l];
         g.bias = c->d_b[l];
         g.K_pad = c->K_pad[l];

@@ -24,6 +24,9 @@ struct GemmArgs {
     const float *log_std;
     int A;
     uint64_t seed;
+    int M_blocks;        // feature blocks of the grid (set by the launcher)
+    uint32_t w_bytes;    // extent of w in bytes (buffer-load bound)
+    uint32_t x_bytes;    // extent of x in bytes: N * ld_x * elem, or D * ld_x * 4 for the observation
 };
 
 hipError_t launch_env_step(int n_slots, const EnvArgs &a, hipStream_t s);

@@ -216,6 +216,256 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_layer_kernel(GemmArgs g)
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 layer GEMM for large batches.  Macro tile BM x BN (features x envs),
+// K step BK; WM x WN waves, each owning a (BM/WM) x (BN/WN) block of 32x32
+// MFMA tiles.  Two LDS stages: while the waves run the MFMAs of stage k from
+// LDS, the 16-byte global loads of stage k+1 (issued one stage earlier) are
+// written into the other LDS buffer and those of stage k+2 are issued.  Rows
+// are padded by 16 bytes so that the 8-lane phases of ds_read_b128 and
+// ds_write_b128 hit distinct banks.  Blocks are renumbered so that the
+// feature blocks sharing one env block run on the same XCD (workgroups are
+// dealt to the 8 XCDs round-robin) and share its L2.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN, bool IN_OBS, bool SAMPLE>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
+{
+    constexpr int NTHR = 64 * WM * WN;
+    constexpr int KQ = BK / 8;                  // 16-byte chunks per row
+    constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+    constexpr int LDK = BK + 8;                 // bf16 elements per LDS row (144 bytes)
+    constexpr int STAGE = (BM + BN) * LDK;      // elements per stage
+    constexpr int A_CHUNKS = BM * KQ / NTHR;    // 16-byte chunks of the weight tile per thread
+    static_assert(BM * KQ % NTHR == 0, "weight tile split");
+    // activation tile: bf16 rows (hidden input) or fp32 observation rows
+    constexpr int B_CHUNKS = BN * KQ / NTHR;    // hidden: 16-byte chunks per thread
+    constexpr int B_TASKS = KQ * (BN / 4) / NTHR;  // obs: 8 k x 4 n blocks per thread
+    static_assert(IN_OBS ? (KQ * (BN / 4) % NTHR == 0) : (BN * KQ % NTHR == 0), "split");
+
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    // XCD-aware renumbering of the 1-D grid
+    const int mblocks = g.M_blocks;
+    const int nblk = gridDim.x;
+    int bid = blockIdx.x;
+    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+    const int64_t m0 = (int64_t)(bid % mblocks) * BM;
+    const int64_t n0 = (int64_t)(bid / mblocks) * BN;
+
+    const uint16_t *W = (const uint16_t *)g.w;
+    const int nk = g.K_pad / BK;
+
+    // Raw buffer descriptors: loads past num_records return zero, which pads
+    // the env tail (rows n >= N) and the observation rows k >= D for free.
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.w, (short)0, (int)g.w_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
+
+    uint4 ra[A_CHUNKS];
+    uint4 rb[IN_OBS ? 1 : B_CHUNKS];
+    float4 ro[IN_OBS ? B_TASKS * 8 : 1];
+    uint32_t a_off[A_CHUNKS], b_off[IN_OBS ? B_TASKS : B_CHUNKS];
+#pragma unroll
+    for (int c = 0; c < A_CHUNKS; ++c) {
+        const int v = tid + c * NTHR;
+        a_off[c] = (uint32_t)(((m0 + v / KQ) * g.K_pad + (v % KQ) * 8) * 2);
+    }
+    if constexpr (!IN_OBS) {
+#pragma unroll
+        for (int c = 0; c < B_CHUNKS; ++c) {
+            const int v = tid + c * NTHR;
+            b_off[c] = (uint32_t)(((n0 + v / KQ) * g.ld_x + (v % KQ) * 8) * 2);
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < B_TASKS; ++t) {
+            const int v = tid + t * NTHR;
+            b_off[t] = (uint32_t)((((int64_t)(v % KQ) * 8) * g.ld_x + n0 + (v / KQ) * 4) * 4);
+        }
+    }
+
+    auto load_global = [&](int kt) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int c = 0; c < A_CHUNKS; ++c)
+            ra[c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, a_off[c], k0 * 2, 0));
+        if constexpr (!IN_OBS) {
+#pragma unroll
+            for (int c = 0; c < B_CHUNKS; ++c)
+                rb[c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[c], k0 * 2, 0));
+        } else {
+            const uint32_t row = (uint32_t)(g.ld_x * 4);
+            const uint32_t kofs = (uint32_t)k0 * row;
+#pragma unroll
+            for (int t = 0; t < B_TASKS; ++t)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    ro[t * 8 + j] = __builtin_bit_cast(
+                        float4, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[t] + j * row, kofs, 0));
+        }
+    };
+
+    auto store_lds = [&](int buf) {
+        uint16_t *As = lds + buf * STAGE;
+        uint16_t *Bs = As + BM * LDK;
+#pragma unroll
+        for (int c = 0; c < A_CHUNKS; ++c) {
+            const int v = tid + c * NTHR;
+            const int r = v / KQ, q = v % KQ;
+            *(uint4 *)(As + r * LDK + q * 8) = ra[c];
+        }
+        if constexpr (!IN_OBS) {
+#pragma unroll
+            for (int c = 0; c < B_CHUNKS; ++c) {
+                const int v = tid + c * NTHR;
+                const int r = v / KQ, q = v % KQ;
+                *(uint4 *)(Bs + r * LDK + q * 8) = rb[c];
+            }
+        } else {
+#pragma unroll
+            for (int t = 0; t < B_TASKS; ++t) {
+                const int v = tid + t * NTHR;
+                const int kg = v % KQ, ng = v / KQ;
+                const float4 *o = ro + t * 8;
+                // env ng*4+e gets the 8 consecutive k values kg*8..kg*8+7 (16 bytes)
+#define IM_PACK(e, comp)                                                                   \
+    {                                                                                      \
+        uint4 w;                                                                           \
+        w.x = (uint32_t)f32_to_bf16_rne(o[0].comp) | ((uint32_t)f32_to_bf16_rne(o[1].comp) << 16); \
+        w.y = (uint32_t)f32_to_bf16_rne(o[2].comp) | ((uint32_t)f32_to_bf16_rne(o[3].comp) << 16); \
+        w.z = (uint32_t)f32_to_bf16_rne(o[4].comp) | ((uint32_t)f32_to_bf16_rne(o[5].comp) << 16); \
+        w.w = (uint32_t)f32_to_bf16_rne(o[6].comp) | ((uint32_t)f32_to_bf16_rne(o[7].comp) << 16); \
+        *(uint4 *)(Bs + (ng * 4 + e) * LDK + kg * 8) = w;                                   \
+    }
+                IM_PACK(0, x) IM_PACK(1, y) IM_PACK(2, z) IM_PACK(3, w)
+#undef IM_PACK
+            }
+        }
+    };
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    auto compute = [&](int buf) {
+        const uint16_t *As = lds + buf * STAGE;
+        const uint16_t *Bs = As + BM * LDK;
+        const int arow = wm * (TM * 32) + (lane & 31);
+        const int brow = wn * (TN * 32) + (lane & 31);
+        const int kof = 8 * (lane >> 5);
+#pragma unroll
+        for (int s = 0; s < BK / 16; ++s) {
+            bf16x8_t a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                a[i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    load_global(0);
+    store_lds(0);
+    __syncthreads();
+    if (nk > 1) load_global(1);
+    for (int kt = 0; kt < nk; ++kt) {
+        compute(kt & 1);
+        if (kt + 1 < nk) store_lds((kt + 1) & 1);
+        if (kt + 2 < nk) load_global(kt + 2);
+        __syncthreads();
+    }
+
+    if constexpr (!SAMPLE) {
+        uint16_t *Y = (uint16_t *)g.y;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t n = n0 + wn * (TN * 32) + j * 32 + (lane & 31);
+                if (n >= g.N) continue;
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) {
+                    const int64_t m = m0 + wm * (TM * 32) + i * 32 + 8 * grp + 4 * (lane >> 5);
+                    const float4 bb = *(const float4 *)(g.bias + m);
+                    const float v0 = fmaxf(acc[i][j][4 * grp + 0] + bb.x, 0.0f);
+                    const float v1 = fmaxf(acc[i][j][4 * grp + 1] + bb.y, 0.0f);
+                    const float v2 = fmaxf(acc[i][j][4 * grp + 2] + bb.z, 0.0f);
+                    const float v3 = fmaxf(acc[i][j][4 * grp + 3] + bb.w, 0.0f);
+                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+                    *(uint2 *)(Y + n * g.ld_y + m) = make_uint2(lo, hi);
+                }
+            }
+    } else {
+        // every action of an env lies in one wave (WM == 1, m0 == 0)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t n = n0 + wn * (TN * 32) + j * 32 + (lane & 31);
+            const bool valid_n = n < g.N;
+            const uint32_t en = valid_n ? g.env_n[n] : 0u;
+            float lp = 0.0f;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) {
+                    const int mb = i * 32 + 8 * grp + 4 * (lane >> 5);
+                    if (!valid_n || mb >= g.A) continue;
+                    float z[4];
+                    normals4(g.seed, (uint32_t)n, en, (uint32_t)(mb >> 2), 0u, z);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int m = mb + q;
+                        if (m < g.A) {
+                            const float mu = acc[i][j][4 * grp + q] + g.bias[m];
+                            const float ls = g.log_std[m];
+                            g.mean[n * g.A + m] = mu;
+                            g.action[n * g.A + m] = mu + expf(ls) * z[q];
+                            lp += 0.5f * z[q] * z[q] + ls + HALF_LOG_2PI;
+                        }
+                    }
+                }
+            lp += __shfl_xor(lp, 32);
+            if (valid_n && lane < 32 && g.logp) g.logp[n] = -lp;
+        }
+    }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool IN_OBS, bool SAMPLE>
+static hipError_t launch_bf16(GemmArgs g, int M_pad, hipStream_t s)
+{
+    g.M_blocks = M_pad / BM;
+    const int64_t nb = (g.N + BN - 1) / BN;
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WM, WN, IN_OBS, SAMPLE>),
+                       dim3((unsigned)(nb * g.M_blocks)), dim3(64 * WM * WN), 0, s, g);
+    return hipGetLastError();
+}
+
+template <bool IN_OBS>
+static hipError_t launch_bf16_sample(const GemmArgs &g, int M_pad, hipStream_t s)
+{
+    switch (M_pad / 32) {
+        case 1: return launch_bf16<32, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
+        case 2: return launch_bf16<64, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
+        case 3: return launch_bf16<96, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
+        default: return launch_bf16<128, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
+    }
+}
+
 template <bool BF16, bool IN_OBS>
 static hipError_t launch_hidden(const GemmArgs &g, int M_pad, hipStream_t s)
 {
@@ -253,11 +503,14 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
                                hipStream_t s)
 {
     if (g.N <= 0) return hipSuccess;
-    if (!sample) {
-        if (bf16) return in_obs ? launch_hidden<true, true>(g, M_pad, s) : launch_hidden<true, false>(g, M_pad, s);
-        return in_obs ? launch_hidden<false, true>(g, M_pad, s) : launch_hidden<false, false>(g, M_pad, s);
+    if (bf16) {
+        if (!sample)
+            return in_obs ? launch_bf16<256, 256, 32, 2, 2, true, false>(g, M_pad, s)
+                          : launch_bf16<256, 256, 32, 2, 2, false, false>(g, M_pad, s);
+        return in_obs ? launch_bf16_sample<true>(g, M_pad, s) : launch_bf16_sample<false>(g, M_pad, s);
     }
-    if (bf16) return in_obs ? launch_sample<true, true>(g, M_pad, s) : launch_sample<true, false>(g, M_pad, s);
+    if (!sample)
+        return in_obs ? launch_hidden<false, true>(g, M_pad, s) : launch_hidden<false, false>(g, M_pad, s);
     return in_obs ? launch_sample<false, true>(g, M_pad, s) : launch_sample<false, false>(g, M_pad, s);
 }
 
