@@ -362,21 +362,36 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
         const int arow = wm * (TM * 32) + (lane & 31);
         const int brow = wn * (TN * 32) + (lane & 31);
         const int kof = 8 * (lane >> 5);
+        constexpr int NS = BK / 16;
+        bf16x8_t a[NS][TM], b[NS][TN];
 #pragma unroll
-        for (int s = 0; s < BK / 16; ++s) {
-            bf16x8_t a[TM], b[TN];
+        for (int s = 0; s < NS; ++s) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                a[i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
+                a[s][i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+                b[s][j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+        }
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][i], b[s][j], acc[i][j], 0, 0, 0);
+        // fragments of substep 0 first; the reads of each later substep are
+        // spread over the MFMAs of the substep before it
+        constexpr int F = TM + TN, MM = TM * TN;
+        __builtin_amdgcn_sched_group_barrier(0x100, F, 0);
+#pragma unroll
+        for (int s = 0; s + 1 < NS; ++s)
+#pragma unroll
+            for (int x = 0; x < F; ++x) {
+                __builtin_amdgcn_sched_group_barrier(0x008, (MM + F - 1) / F, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+        __builtin_amdgcn_sched_group_barrier(0x008, MM, 0);
     };
 
     load_global(0);
