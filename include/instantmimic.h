@@ -13,7 +13,7 @@
  *
  * Entry points:
  *   im_env_step_fused  reward + termination + masked reset + observation
- *                      (Sec. 4.1 Fig. 4 reward and dones, Sec. 4.2 reset,
+ *                      (Sec. 4.1 Fig. 5 reward and dones, Sec. 4.2 reset,
  *                      Sec. 6.1 observation), one kernel launch;
  *   im_policy_act      Gaussian MLP policy forward and action sampling
  *                      (Fig. 3 "policy(obs)", Sec. 6.1 / backflip table:
@@ -21,7 +21,7 @@
  *   im_reset_envs      forced reset of the envs selected by a device mask
  *                      (start of a rollout, host-requested resets).
  *
- * Conventions.  Quaternions are (w, x, y, z), Hamilton product (Fig. 2a
+ * Conventions.  Quaternions are (w, x, y, z), Hamilton product (Fig. 4a
  * converts the simulator's quaternions to wxyz).  World up is +z; a root's
  * local +x axis is its forward direction.  Body 0 is the root (free joint);
  * parent[b] < b.
@@ -75,15 +75,15 @@ enum { IM_DTYPE_F32 = 0, IM_DTYPE_BF16 = 1 };
 typedef struct im_ctx im_ctx;
 
 /*
- * Step configuration.  Reward (Sec. 4.1, Fig. 4, with the end-effector
+ * Step configuration.  Reward (Sec. 4.1, Fig. 5, with the end-effector
  * position term of the DeepMimic reward that Sec. 6.1 builds on):
  *   r = c_pose exp(-(w_pos e_pos + w_ee e_ee)) + c_vel exp(-w_vel e_vel)
  *       + c_com exp(-w_com e_com)
  * with e_pos / e_vel the sums over bodies of squared position / linear
  * velocity errors, e_ee the position errors summed over leaf bodies and
  * e_com the squared error of the mass-weighted centre of the body origins.
- * Fig. 4's printed form is c = (0.60, 0.25, 0.15), w = (4, 0.25, 8), w_ee = 0.
- * Termination (Fig. 4, strict "<"; grace steps from the backflip table):
+ * Fig. 5's printed form is c = (0.60, 0.25, 0.15), w = (4, 0.25, 8), w_ee = 0.
+ * Termination (Fig. 5, strict "<"; grace steps from the backflip table):
  *   terminated = (t + 1 > grace) && (root_z < h_term || !(r >= r_min)).
  * Truncation: the clip phase reaches 1.
  */

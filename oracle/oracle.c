@@ -17,7 +17,7 @@
  *   - the rollout step of the PPO loop [Sec. 3, Fig. 3]: reward and dones
  *     are evaluated on the post-physics state, then terminated/truncated envs
  *     are reset, then the observation is built;
- *   - the tracking reward and termination flag [Sec. 4.1, Fig. 4]: body
+ *   - the tracking reward and termination flag [Sec. 4.1, Fig. 5]: body
  *     position, body velocity and centre-of-mass errors summed over bodies,
  *     exponentiated and combined, plus an end-effector position term taken
  *     from the DeepMimic reward that Sec. 6.1 builds on (weight 0 gives the
@@ -36,7 +36,7 @@
  * (the composition of the whole step) are "parity unpinned" beyond the
  * component pins.
  *
- * Conventions: quaternions are (w,x,y,z) Hamilton [Sec. 3.2, Fig. 2a converts
+ * Conventions: quaternions are (w,x,y,z) Hamilton [Sec. 3.2, Fig. 4a converts
  * to wxyz], active rotations, world up = +z, root forward = +x.
  */
 #include <math.h>
@@ -527,12 +527,12 @@ void or_fk(const or_world *w, const double *root_p, const double *root_q, const 
 }
 
 /* ------------------------------------------------------------------ */
-/* Reward [Sec. 4.1, Fig. 4] with the end-effector term.               */
+/* Reward [Sec. 4.1, Fig. 5] with the end-effector term.               */
 /* ------------------------------------------------------------------ */
 typedef struct { double e_pos, e_vel, e_ee, e_com, r; } or_reward_t;
 
 /*
- * Errors are sums over bodies of squared distances (Fig. 4 sums over the
+ * Errors are sums over bodies of squared distances (Fig. 5 sums over the
  * body and coordinate axes): e_pos over all bodies' positions, e_vel over
  * their linear velocities, e_ee over end effectors (bodies without
  * children), e_com on the mass-weighted centre of body origins.
@@ -579,7 +579,7 @@ void or_reward(const or_world *w, const double *P, const double *V, const double
 }
 
 /*
- * Termination [Fig. 4, strict "<"]: after the grace steps, an env
+ * Termination [Fig. 5, strict "<"]: after the grace steps, an env
  * terminates when the root is below h_term or the fp32 reward is not at
  * least r_min (a NaN reward terminates).
  */

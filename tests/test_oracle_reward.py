@@ -83,8 +83,8 @@ def test_rigid_translation_moves_only_position_terms(world):
     assert r["e_com"] == pytest.approx(x, rel=1e-9)
 
 
-def test_without_ee_weight_equals_fig4_reward():
-    # The paper's printed tensor code (Fig. 4a), transcribed; with the EE weight at
+def test_without_ee_weight_equals_fig5_reward():
+    # The paper's printed tensor code (Fig. 5a), transcribed; with the EE weight at
     # zero the oracle's reward is that three-term form.
     d = synth.make_world(2, n_envs=1, w_ee=0.0)
     w = oracle.World(d)
