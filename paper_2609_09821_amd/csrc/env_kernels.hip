@@ -112,30 +112,79 @@ __device__ __forceinline__ Frame child_frame(const Frame &p, const float4 *rec, 
     return f;
 }
 
-// Forward kinematics of one reference segment record; visit(i, body, frame,
-// anchor) is called for every preorder position i.
-template <class Visit>
-__device__ __forceinline__ void walk(const SkelTab *__restrict__ sk, const float4 *rec, float alpha,
-                                     Visit &&visit)
+// Forward kinematics of one reference segment record in preorder;
+// visit(i, body, frame, anchor, data) is called for every position i.  A
+// depth-2 software prefetch keeps the segment record and the per-body data
+// returned by load(body) for positions i+1 and i+2 in flight while body i is
+// processed, so the memory latency of one body overlaps the arithmetic of
+// the previous ones.
+struct NoData {
+};
+
+template <class D, class Load, class Visit>
+__device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, const float4 *rec,
+                                              float alpha, Load &&load, Visit &&visit)
 {
     const LdsStack<13> st{im_lds + threadIdx.x, (int)blockDim.x};
     float buf[13];
+    const int B = sk->B;
+    const float4 *jr = rec + 6;
+    // position 0 (root) and prefetch of positions 1, 2
+    D d0 = load(0);
+    D d1{}, d2{};
+    float4 a1{}, u1{}, w1{}, a2{}, u2{}, w2{};
+    if (B > 1) {
+        d1 = load(sk->body[1]);
+        a1 = jr[0];
+        u1 = jr[1];
+        w1 = jr[2];
+    }
+    if (B > 2) {
+        d2 = load(sk->body[2]);
+        a2 = jr[3];
+        u2 = jr[4];
+        w2 = jr[5];
+    }
     f3 A;
     Frame cur = root_frame(rec, alpha, &A);
-    visit(0, 0, cur, A);
+    visit(0, 0, cur, A, d0);
     if (sk->bslot[0] >= 0) {
         pack_frame(cur, buf);
         st.put(sk->bslot[0], buf);
     }
-    const int B = sk->B;
     for (int i = 1; i < B; ++i) {
-        if (sk->pslot[i] >= 0) {  // parent is an earlier branch point
+        const D d = d1;
+        const float4 ra = a1, ru = u1, rw = w1;
+        d1 = d2;
+        a1 = a2;
+        u1 = u2;
+        w1 = w2;
+        if (i + 2 < B) {
+            d2 = load(sk->body[i + 2]);
+            const float4 *p = jr + 3 * (i + 1);
+            a2 = p[0];
+            u2 = p[1];
+            w2 = p[2];
+        }
+        if (sk->pslot[i] >= 0) {
             st.get(sk->pslot[i], buf);
             cur = unpack_frame(buf);
         }
         const f3 off = mk3(sk->offset[i][0], sk->offset[i][1], sk->offset[i][2]);
-        cur = child_frame(cur, rec + 6 + 3 * (i - 1), alpha, off, sk->jtype[i]);
-        visit(i, sk->body[i], cur, A);
+        // child frame from the prefetched record (same arithmetic as child_frame)
+        Frame c;
+        const f3 r = qrot(cur.Q, off);
+        c.P = cur.P + r;
+        c.V = cur.V + cross3(cur.W, r);
+        if (sk->jtype[i] == IM_JOINT_FIXED) {
+            c.Q = cur.Q;
+            c.W = cur.W;
+        } else {
+            c.Q = qmul(cur.Q, slerp_basis(ra, ru, alpha * rw.w));
+            c.W = cur.W + qrot(cur.Q, mk3(rw.x, rw.y, rw.z));
+        }
+        cur = c;
+        visit(i, sk->body[i], cur, A, d);
         if (sk->bslot[i] >= 0) {
             pack_frame(cur, buf);
             st.put(sk->bslot[i], buf);
@@ -242,8 +291,22 @@ __device__ __forceinline__ void write_obs_body(float *obs, int64_t ld, int64_t e
     o[14 * ld] = W.z;
 }
 
-// Reference state initialisation: sim state and observation of env e := the
-// reference at (clip k, phase ph).
+// Observation of env e from its (post-reset) sim state.  The body loop has
+// no dependency between iterations, so several bodies' loads are in flight.
+__device__ __forceinline__ void obs_from_sim(const EnvArgs &a, int64_t e, float phase)
+{
+    const int64_t ld = a.ld;
+    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
+    const int B = a.sk->B;
+#pragma unroll 4
+    for (int b = 0; b < B; ++b)
+        write_obs_body(a.obs, ld, e, b, h, ld3(a.pos, b, ld, e), ld4(a.quat, b, ld, e),
+                       ld3(a.linvel, b, ld, e), ld3(a.angvel, b, ld, e));
+    a.obs[(int64_t)(15 * B) * ld + e] = phase;
+}
+
+// Reference state initialisation: the sim state of env e := the reference
+// at (clip k, phase ph).
 __device__ __forceinline__ void rsi(const EnvArgs &a, int64_t e, int k, float ph)
 {
     const ClipTab ci = a.clips[k];
@@ -252,89 +315,93 @@ __device__ __forceinline__ void rsi(const EnvArgs &a, int64_t e, int k, float ph
     phase_index(ph, ci, &j0, &al);
     const float4 *rec = a.seg + ci.seg_base + (int64_t)j0 * seg_stride(a.sk->B);
     const int64_t ld = a.ld;
-    Heading h{1.0f, 0.0f, 0.0f, 0.0f};
-    walk(a.sk, rec, al, [&](int i, int b, const Frame &f, f3 A) {
-        const f3 P = A + f.P;
-        st3(a.pos, b, ld, e, P);
+    walk_prefetch<NoData>(a.sk, rec, al, [](int) { return NoData{}; },
+                          [&](int, int b, const Frame &f, f3 A, const NoData &) {
+        st3(a.pos, b, ld, e, A + f.P);
         st4(a.quat, b, ld, e, f.Q);
         st3(a.linvel, b, ld, e, f.V);
         st3(a.angvel, b, ld, e, f.W);
-        if (i == 0) h = heading_of(f.Q, P);
-        write_obs_body(a.obs, ld, e, b, h, P, f.Q, f.V, f.W);
     });
-    a.obs[(int64_t)(15 * a.sk->B) * ld + e] = ph;
 }
+
+struct SimPV {
+    f3 P, V;
+};
 
 __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
 {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= a.n) return;
+    const bool active = e < a.n;
     const int64_t ld = a.ld;
     const SkelTab *__restrict__ sk = a.sk;
+    float ph_out = 0.0f;
 
-    // 1. discrete state advance (fp32, exact contract)
-    const int k = safe_clip(a.env_clip[e], a.n_clips);
-    const float phi = a.env_phase[e];
-    const int t1 = a.env_t[e] + 1;
-    const uint32_t n1 = a.env_n[e] + 1u;
-    const ClipTab ci = a.clips[k];
-    float phi1;
-    {
+    if (active) {
+        // 1. discrete state advance (fp32, exact contract)
+        const int k = safe_clip(a.env_clip[e], a.n_clips);
+        const float phi = a.env_phase[e];
+        const int t1 = a.env_t[e] + 1;
+        const uint32_t n1 = a.env_n[e] + 1u;
+        const ClipTab ci = a.clips[k];
+        float phi1;
+        {
 #pragma clang fp contract(off)
-        phi1 = phi + ci.dphi;
+            phi1 = phi + ci.dphi;
+        }
+        const bool trunc = phi1 >= 1.0f;
+        int i0;
+        float alpha;
+        phase_index(phi1 < 1.0f ? phi1 : 1.0f, ci, &i0, &alpha);
+
+        // 2.-3. reference FK and errors against the sim positions/velocities
+        float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
+        f3 dc = mk3(0.0f, 0.0f, 0.0f);
+        const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
+        auto load_pv = [&](int b) {
+            SimPV s;
+            s.P = ld3(a.pos, b, ld, e);
+            s.V = ld3(a.linvel, b, ld, e);
+            return s;
+        };
+        walk_prefetch<SimPV>(sk, rec, alpha, load_pv,
+                             [&](int i, int, const Frame &f, f3 A, const SimPV &sb) {
+            const f3 dp = (sb.P - A) - f.P;
+            const f3 dv = sb.V - f.V;
+            const float x = dot3(dp, dp);
+            e_pos += x;
+            if (sk->leaf[i]) e_ee += x;
+            dc = dc + sk->massw[i] * dp;
+            e_vel += dot3(dv, dv);
+        });
+        const float e_com = dot3(dc, dc);
+        const float r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
+                        a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
+        const float z_root = a.pos[2 * ld + e];
+        const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
+
+        // 4. masked reset
+        int k_out = k, t_out = t1;
+        ph_out = phi1;
+        if (term || trunc) {
+            const uint4 x = philox4x32_10(make_uint4((uint32_t)e, n1, 0u, 1u), (uint32_t)a.seed,
+                                          (uint32_t)(a.seed >> 32));
+            k_out = (int)(((uint64_t)x.x * (uint64_t)(uint32_t)a.n_clips) >> 32);
+            ph_out = (float)(x.y >> 8) * 0x1p-24f;
+            t_out = 0;
+            rsi(a, e, k_out, ph_out);
+        }
+        a.env_clip[e] = k_out;
+        a.env_phase[e] = ph_out;
+        a.env_t[e] = t_out;
+        a.env_n[e] = n1;
+        a.reward[e] = r;
+        a.term[e] = (uint8_t)term;
+        a.trunc[e] = (uint8_t)trunc;
+        if (a.ref_frame) a.ref_frame[e] = i0;
     }
-    const bool trunc = phi1 >= 1.0f;
-    int i0;
-    float alpha;
-    phase_index(phi1 < 1.0f ? phi1 : 1.0f, ci, &i0, &alpha);
-
-    // 2.-3. reference FK, errors against the sim state, speculative obs
-    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
-    float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
-    f3 dc = mk3(0.0f, 0.0f, 0.0f);
-    const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
-    walk(sk, rec, alpha, [&](int i, int b, const Frame &f, f3 A) {
-        const f3 P = ld3(a.pos, b, ld, e);
-        const f3 V = ld3(a.linvel, b, ld, e);
-        const q4 Q = ld4(a.quat, b, ld, e);
-        const f3 W = ld3(a.angvel, b, ld, e);
-        const f3 dp = (P - A) - f.P;
-        const f3 dv = V - f.V;
-        const float x = dot3(dp, dp);
-        e_pos += x;
-        if (sk->leaf[i]) e_ee += x;
-        dc = dc + sk->massw[i] * dp;
-        e_vel += dot3(dv, dv);
-        write_obs_body(a.obs, ld, e, b, h, P, Q, V, W);
-    });
-    const float e_com = dot3(dc, dc);
-    const float r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
-                    a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
-    const float z_root = a.pos[2 * ld + e];
-    const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
-
-    // 4. masked reset
-    int k_out = k, t_out = t1;
-    float ph_out = phi1;
-    if (term || trunc) {
-        const uint4 x = philox4x32_10(make_uint4((uint32_t)e, n1, 0u, 1u), (uint32_t)a.seed,
-                                      (uint32_t)(a.seed >> 32));
-        k_out = (int)(((uint64_t)x.x * (uint64_t)(uint32_t)a.n_clips) >> 32);
-        ph_out = (float)(x.y >> 8) * 0x1p-24f;
-        t_out = 0;
-        rsi(a, e, k_out, ph_out);
-    } else {
-        a.obs[(int64_t)(15 * sk->B) * ld + e] = ph_out;
-    }
-
-    a.env_clip[e] = k_out;
-    a.env_phase[e] = ph_out;
-    a.env_t[e] = t_out;
-    a.env_n[e] = n1;
-    a.reward[e] = r;
-    a.term[e] = (uint8_t)term;
-    a.trunc[e] = (uint8_t)trunc;
-    if (a.ref_frame) a.ref_frame[e] = i0;
+    // 5. observation of the post-reset state (this thread's own env: the
+    //    reference state it may have just written is read back in order)
+    if (active) obs_from_sim(a, e, ph_out);
 }
 
 __global__ __launch_bounds__(256) void reset_kernel(EnvArgs a)
@@ -350,6 +417,7 @@ __global__ __launch_bounds__(256) void reset_kernel(EnvArgs a)
     a.env_clip[e] = k;
     a.env_phase[e] = ph;
     a.env_t[e] = 0;
+    obs_from_sim(a, e, ph);
 }
 
 // ---------------------------------------------------------------------------
