@@ -25,43 +25,107 @@ namespace im {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float HALF_LOG_2PI = 0.91893853320467274f;
 
-template <bool BF16>
-struct Elem;
-template <>
-struct Elem<true> {
-    using T = uint16_t;
-    static constexpr int KSTEP = 16;  // K of one MFMA
-};
-template <>
-struct Elem<false> {
-    using T = float;
-    static constexpr int KSTEP = 2;
-};
-
-// Tile: WGM x WGN waves, each MT x NT MFMA tiles of 32x32; K chunk KC.
-template <bool BF16, bool IN_OBS, bool SAMPLE, int WGM, int WGN, int MT, int NT>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_layer_kernel(GemmArgs g)
+// fp32 layer GEMM.  Tile: WGM x WGN waves, each MT x NT MFMA tiles of 32x32
+// (v_mfma_f32_32x32x2_f32); K chunk 32.  16-byte global loads into
+// registers one chunk ahead, two LDS buffers, one barrier per chunk.  The
+// first layer reads the observation [D][ld] (env fastest) with 16-byte loads
+// along envs and transposes it into LDS.
+template <bool IN_OBS, bool SAMPLE, int WGM, int WGN, int MT, int NT>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
 {
-    using T = typename Elem<BF16>::T;
-    constexpr int KSTEP = Elem<BF16>::KSTEP;
     constexpr int KC = 32;
     constexpr int BM = WGM * MT * 32, BN = WGN * NT * 32;
     constexpr int NTHR = 64 * WGM * WGN;
-    constexpr int PAD = 16 / sizeof(T);  // 16-byte row padding against bank conflicts
-    constexpr int LDA = KC + PAD;
+    constexpr int LDA = KC + 4;                  // floats per LDS row (16-byte pad)
+    constexpr int STAGE = (BM + BN) * LDA;
+    constexpr int A_CH = BM * (KC / 4) / NTHR;   // float4 chunks of the weight tile per thread
+    constexpr int B_CH = BN * (KC / 4) / NTHR;   // hidden input: float4 chunks per thread
+    constexpr int O_CH = KC * (BN / 4) / NTHR;   // observation: float4 (4 envs of one k) per thread
+    static_assert(BM * (KC / 4) % NTHR == 0 && BN * (KC / 4) % NTHR == 0 && KC * (BN / 4) % NTHR == 0, "split");
 
-    __shared__ __attribute__((aligned(16))) T As[BM * LDA];
-    __shared__ __attribute__((aligned(16))) T Bs[BN * LDA];
+    __shared__ __attribute__((aligned(16))) float lds[2 * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     const int64_t m0 = (int64_t)blockIdx.x * BM;
     const int64_t n0 = (int64_t)blockIdx.y * BN;
-    const T *W = (const T *)g.w;
+    const float *W = (const float *)g.w;
+    const float *X = (const float *)g.x;
+    // raw buffer loads: past the extent they return zero (env tail, rows of
+    // the observation beyond D); columns past N inside the extent only feed
+    // accumulator columns that are never stored
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)X, (short)0, (int)g.x_bytes, 0x00020000);
+    const bool vec_obs = IN_OBS && ((g.ld_x & 3) == 0) && ((((uintptr_t)X) & 15) == 0);
+    (void)vec_obs;
+
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)W, (short)0, (int)g.w_bytes, 0x00020000);
+    f32x4_t ra[A_CH], rb[IN_OBS ? O_CH : B_CH];
+    auto load_global = [&](int k0) {
+#pragma unroll
+        for (int c = 0; c < A_CH; ++c) {
+            const int v = tid + c * NTHR;
+            const int r = v / (KC / 4), q = v % (KC / 4);
+            const uint32_t off = (uint32_t)(((m0 + r) * g.K_pad + k0 + q * 4) * 4);
+            ra[c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, off, 0, 0));
+        }
+        if constexpr (!IN_OBS) {
+#pragma unroll
+            for (int c = 0; c < B_CH; ++c) {
+                const int v = tid + c * NTHR;
+                const int r = v / (KC / 4), q = v % (KC / 4);
+                const uint32_t off = (uint32_t)(((n0 + r) * g.ld_x + k0 + q * 4) * 4);
+                rb[c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < O_CH; ++c) {
+                const int v = tid + c * NTHR;
+                const int kk = v / (BN / 4), nq = (v % (BN / 4)) * 4;
+                const uint32_t off = (uint32_t)((((int64_t)(k0 + kk)) * g.ld_x + n0 + nq) * 4);
+                if (vec_obs) {
+                    rb[c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+                } else {
+                    rb[c][0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0));
+                    rb[c][1] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xr, off + 4, 0, 0));
+                    rb[c][2] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xr, off + 8, 0, 0));
+                    rb[c][3] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xr, off + 12, 0, 0));
+                }
+            }
+        }
+    };
+    auto store_lds = [&](int buf) {
+        float *As = lds + buf * STAGE;
+        float *Bs = As + BM * LDA;
+#pragma unroll
+        for (int c = 0; c < A_CH; ++c) {
+            const int v = tid + c * NTHR;
+            *(f32x4_t *)(As + (v / (KC / 4)) * LDA + (v % (KC / 4)) * 4) = ra[c];
+        }
+        if constexpr (!IN_OBS) {
+#pragma unroll
+            for (int c = 0; c < B_CH; ++c) {
+                const int v = tid + c * NTHR;
+                *(f32x4_t *)(Bs + (v / (KC / 4)) * LDA + (v % (KC / 4)) * 4) = rb[c];
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < O_CH; ++c) {
+                const int v = tid + c * NTHR;
+                const int kk = v / (BN / 4), nq = (v % (BN / 4)) * 4;
+                Bs[(nq + 0) * LDA + kk] = rb[c][0];
+                Bs[(nq + 1) * LDA + kk] = rb[c][1];
+                Bs[(nq + 2) * LDA + kk] = rb[c][2];
+                Bs[(nq + 3) * LDA + kk] = rb[c][3];
+            }
+        }
+    };
 
     f32x16_t acc[MT][NT];
 #pragma unroll
@@ -71,94 +135,40 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_layer_kernel(GemmArgs g)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    for (int k0 = 0; k0 < g.K_pad; k0 += KC) {
-        // ---- stage the weight tile (rows contiguous in K) ----
-        {
-            constexpr int VEC = 16 / sizeof(T);          // elements per 16-byte load
-            constexpr int PER_ROW = KC / VEC;
-            for (int v = tid; v < BM * PER_ROW; v += NTHR) {
-                const int r = v / PER_ROW, c = (v % PER_ROW) * VEC;
-                const uint4 q = *(const uint4 *)(W + (m0 + r) * g.K_pad + k0 + c);
-                *(uint4 *)(&As[r * LDA + c]) = q;
-            }
+    auto compute = [&](int buf) {
+        const float *As = lds + buf * STAGE;
+        const float *Bs = As + BM * LDA;
+        const int arow = wm * (MT * 32) + (lane & 31), brow = wn * (NT * 32) + (lane & 31);
+#pragma unroll
+        for (int ks = 0; ks < KC; ks += 2) {
+            const int kof = ks + (lane >> 5);
+            float af[MT], bfr[NT];
+#pragma unroll
+            for (int i = 0; i < MT; ++i) af[i] = As[(arow + i * 32) * LDA + kof];
+#pragma unroll
+            for (int j = 0; j < NT; ++j) bfr[j] = Bs[(brow + j * 32) * LDA + kof];
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
-        // ---- stage the activation tile ----
-        if constexpr (IN_OBS) {
-            const float *X = (const float *)g.x;
-            for (int v = tid; v < BN * KC; v += NTHR) {
-                const int kk = v / BN, nn = v % BN;
-                const int k = k0 + kk;
-                const int64_t n = n0 + nn;
-                float val = 0.0f;
-                if (k < g.K_valid && n < g.N) val = X[(int64_t)k * g.ld_x + n];
-                if constexpr (BF16)
-                    Bs[nn * LDA + kk] = f32_to_bf16_rne(val);
-                else
-                    Bs[nn * LDA + kk] = val;
-            }
-        } else {
-            const T *X = (const T *)g.x;
-            constexpr int VEC = 16 / sizeof(T);
-            constexpr int PER_ROW = KC / VEC;
-            for (int v = tid; v < BN * PER_ROW; v += NTHR) {
-                const int r = v / PER_ROW, c = (v % PER_ROW) * VEC;
-                const int64_t n = n0 + r;
-                uint4 q = make_uint4(0u, 0u, 0u, 0u);
-                if (n < g.N) q = *(const uint4 *)(X + n * g.ld_x + k0 + c);
-                *(uint4 *)(&Bs[r * LDA + c]) = q;
-            }
-        }
-        __syncthreads();
+    };
 
-        // ---- MFMA over the chunk ----
-#pragma unroll
-        for (int ks = 0; ks < KC; ks += KSTEP) {
-            if constexpr (BF16) {
-                bf16x8_t af[MT], bfr[NT];
-                const int kof = ks + 8 * (lane >> 5);
-#pragma unroll
-                for (int i = 0; i < MT; ++i) {
-                    const int row = (wm * MT + i) * 32 + (lane & 31);
-                    af[i] = *(const bf16x8_t *)(&As[row * LDA + kof]);
-                }
-#pragma unroll
-                for (int j = 0; j < NT; ++j) {
-                    const int row = (wn * NT + j) * 32 + (lane & 31);
-                    bfr[j] = *(const bf16x8_t *)(&Bs[row * LDA + kof]);
-                }
-#pragma unroll
-                for (int i = 0; i < MT; ++i)
-#pragma unroll
-                    for (int j = 0; j < NT; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j],
-                                                                            acc[i][j], 0, 0, 0);
-            } else {
-                float af[MT], bfr[NT];
-                const int kof = ks + (lane >> 5);
-#pragma unroll
-                for (int i = 0; i < MT; ++i) {
-                    const int row = (wm * MT + i) * 32 + (lane & 31);
-                    af[i] = As[row * LDA + kof];
-                }
-#pragma unroll
-                for (int j = 0; j < NT; ++j) {
-                    const int row = (wn * NT + j) * 32 + (lane & 31);
-                    bfr[j] = Bs[row * LDA + kof];
-                }
-#pragma unroll
-                for (int i = 0; i < MT; ++i)
-#pragma unroll
-                    for (int j = 0; j < NT; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[j], acc[i][j],
-                                                                         0, 0, 0);
-            }
-        }
+    const int nk = g.K_pad / KC;
+    load_global(0);
+    store_lds(0);
+    __syncthreads();
+    if (nk > 1) load_global(KC);
+    for (int kt = 0; kt < nk; ++kt) {
+        compute(kt & 1);
+        if (kt + 1 < nk) store_lds((kt + 1) & 1);
+        if (kt + 2 < nk) load_global((kt + 2) * KC);
         __syncthreads();
     }
 
-    // ---- epilogues ----
     if constexpr (!SAMPLE) {
-        T *Y = (T *)g.y;
+        float *Y = (float *)g.y;
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -168,21 +178,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_layer_kernel(GemmArgs g)
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp) {
                     const int64_t m = m0 + (wm * MT + i) * 32 + 8 * grp + 4 * (lane >> 5);
-                    float v[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const float y = acc[i][j][4 * grp + q] + g.bias[m + q];
-                        v[q] = y > 0.0f ? y : 0.0f;
-                    }
-                    if constexpr (BF16) {
-                        const uint32_t lo = (uint32_t)f32_to_bf16_rne(v[0]) |
-                                            ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
-                        const uint32_t hi = (uint32_t)f32_to_bf16_rne(v[2]) |
-                                            ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
-                        *(uint2 *)(Y + n * g.ld_y + m) = make_uint2(lo, hi);
-                    } else {
-                        *(float4 *)(Y + n * g.ld_y + m) = make_float4(v[0], v[1], v[2], v[3]);
-                    }
+                    const float4 bb = *(const float4 *)(g.bias + m);
+                    *(float4 *)(Y + n * g.ld_y + m) =
+                        make_float4(fmaxf(acc[i][j][4 * grp + 0] + bb.x, 0.0f),
+                                    fmaxf(acc[i][j][4 * grp + 1] + bb.y, 0.0f),
+                                    fmaxf(acc[i][j][4 * grp + 2] + bb.z, 0.0f),
+                                    fmaxf(acc[i][j][4 * grp + 3] + bb.w, 0.0f));
                 }
             }
     } else {
@@ -481,25 +482,45 @@ static hipError_t launch_bf16_sample(const GemmArgs &g, int M_pad, hipStream_t s
     }
 }
 
+// fp32 layers: 128x128 tiles (2x2 waves of 64x64) for large batches; for
+// small batches 64x64 tiles (one 32x32 MFMA tile per wave) so that a layer
+// still spreads over every SIMD.
+constexpr int64_t SMALL_BATCH = 16384;
+
+template <bool BF16, bool IN_OBS, int MT, int NT>
+static hipError_t launch_hidden_t(const GemmArgs &g, int M_pad, hipStream_t s)
+{
+    constexpr int WGM = 2, WGN = 2;
+    const dim3 grid((unsigned)(M_pad / (WGM * MT * 32)),
+                    (unsigned)((g.N + WGN * NT * 32 - 1) / (WGN * NT * 32)));
+    static_assert(!BF16, "bf16 layers use gemm_bf16_kernel");
+    hipLaunchKernelGGL((gemm_f32_kernel<IN_OBS, false, WGM, WGN, MT, NT>), grid,
+                       dim3(64 * WGM * WGN), 0, s, g);
+    return hipGetLastError();
+}
+
 template <bool BF16, bool IN_OBS>
 static hipError_t launch_hidden(const GemmArgs &g, int M_pad, hipStream_t s)
 {
-    constexpr int WGM = 2, WGN = 2, MT = 2, NT = 2;
-    const dim3 grid((unsigned)(M_pad / (WGM * MT * 32)),
-                    (unsigned)((g.N + WGN * NT * 32 - 1) / (WGN * NT * 32)));
-    hipLaunchKernelGGL((gemm_layer_kernel<BF16, IN_OBS, false, WGM, WGN, MT, NT>), grid,
-                       dim3(64 * WGM * WGN), 0, s, g);
+    if (g.N <= SMALL_BATCH) return launch_hidden_t<BF16, IN_OBS, 1, 1>(g, M_pad, s);
+    return launch_hidden_t<BF16, IN_OBS, 2, 2>(g, M_pad, s);
+}
+
+template <bool BF16, bool IN_OBS, int MT, int WGN>
+static hipError_t launch_sample_t(const GemmArgs &g, hipStream_t s)
+{
+    const dim3 grid(1u, (unsigned)((g.N + WGN * 32 - 1) / (WGN * 32)));
+    static_assert(!BF16, "bf16 layers use gemm_bf16_kernel");
+    hipLaunchKernelGGL((gemm_f32_kernel<IN_OBS, true, 1, WGN, MT, 1>), grid,
+                       dim3(64 * WGN), 0, s, g);
     return hipGetLastError();
 }
 
 template <bool BF16, bool IN_OBS, int MT>
 static hipError_t launch_sample_mt(const GemmArgs &g, hipStream_t s)
 {
-    constexpr int WGN = 4;
-    const dim3 grid(1u, (unsigned)((g.N + WGN * 32 - 1) / (WGN * 32)));
-    hipLaunchKernelGGL((gemm_layer_kernel<BF16, IN_OBS, true, 1, WGN, MT, 1>), grid,
-                       dim3(64 * WGN), 0, s, g);
-    return hipGetLastError();
+    if (g.N <= SMALL_BATCH) return launch_sample_t<BF16, IN_OBS, MT, 1>(g, s);
+    return launch_sample_t<BF16, IN_OBS, MT, 4>(g, s);
 }
 
 template <bool BF16, bool IN_OBS>
