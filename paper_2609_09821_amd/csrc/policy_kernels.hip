@@ -29,6 +29,10 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float HALF_LOG_2PI = 0.91893853320467274f;
 
+// Batches up to this many envs use smaller tiles so that every layer still
+// spreads over all 256 CUs.
+constexpr int64_t SMALL_BATCH = 16384;
+
 // fp32 layer GEMM.  Tile: WGM x WGN waves, each MT x NT MFMA tiles of 32x32
 // (v_mfma_f32_32x32x2_f32); K chunk 32.  16-byte global loads into
 // registers one chunk ahead, two LDS buffers, one barrier per chunk.  The
@@ -267,9 +271,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
 
-    uint4 ra[A_CHUNKS];
-    uint4 rb[IN_OBS ? 1 : B_CHUNKS];
-    float4 ro[IN_OBS ? B_TASKS * 8 : 1];
+    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+    u32x4_t ra[A_CHUNKS];
+    u32x4_t rb[IN_OBS ? 1 : B_CHUNKS];
+    f32x4_t ro[IN_OBS ? B_TASKS * 8 : 1];
     uint32_t a_off[A_CHUNKS], b_off[IN_OBS ? B_TASKS : B_CHUNKS];
 #pragma unroll
     for (int c = 0; c < A_CHUNKS; ++c) {
@@ -294,11 +299,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
         const int k0 = kt * BK;
 #pragma unroll
         for (int c = 0; c < A_CHUNKS; ++c)
-            ra[c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, a_off[c], k0 * 2, 0));
+            ra[c] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, a_off[c], k0 * 2, 0));
         if constexpr (!IN_OBS) {
 #pragma unroll
             for (int c = 0; c < B_CHUNKS; ++c)
-                rb[c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[c], k0 * 2, 0));
+                rb[c] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[c], k0 * 2, 0));
         } else {
             const uint32_t row = (uint32_t)(g.ld_x * 4);
             const uint32_t kofs = (uint32_t)k0 * row;
@@ -307,7 +312,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
                     ro[t * 8 + j] = __builtin_bit_cast(
-                        float4, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[t] + j * row, kofs, 0));
+                        f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, b_off[t] + j * row, kofs, 0));
         }
     };
 
@@ -318,33 +323,31 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
         for (int c = 0; c < A_CHUNKS; ++c) {
             const int v = tid + c * NTHR;
             const int r = v / KQ, q = v % KQ;
-            *(uint4 *)(As + r * LDK + q * 8) = ra[c];
+            *(u32x4_t *)(As + r * LDK + q * 8) = ra[c];
         }
         if constexpr (!IN_OBS) {
 #pragma unroll
             for (int c = 0; c < B_CHUNKS; ++c) {
                 const int v = tid + c * NTHR;
                 const int r = v / KQ, q = v % KQ;
-                *(uint4 *)(Bs + r * LDK + q * 8) = rb[c];
+                *(u32x4_t *)(Bs + r * LDK + q * 8) = rb[c];
             }
         } else {
 #pragma unroll
             for (int t = 0; t < B_TASKS; ++t) {
                 const int v = tid + t * NTHR;
                 const int kg = v % KQ, ng = v / KQ;
-                const float4 *o = ro + t * 8;
+                const f32x4_t *o = ro + t * 8;
                 // env ng*4+e gets the 8 consecutive k values kg*8..kg*8+7 (16 bytes)
-#define IM_PACK(e, comp)                                                                   \
-    {                                                                                      \
-        uint4 w;                                                                           \
-        w.x = (uint32_t)f32_to_bf16_rne(o[0].comp) | ((uint32_t)f32_to_bf16_rne(o[1].comp) << 16); \
-        w.y = (uint32_t)f32_to_bf16_rne(o[2].comp) | ((uint32_t)f32_to_bf16_rne(o[3].comp) << 16); \
-        w.z = (uint32_t)f32_to_bf16_rne(o[4].comp) | ((uint32_t)f32_to_bf16_rne(o[5].comp) << 16); \
-        w.w = (uint32_t)f32_to_bf16_rne(o[6].comp) | ((uint32_t)f32_to_bf16_rne(o[7].comp) << 16); \
-        *(uint4 *)(Bs + (ng * 4 + e) * LDK + kg * 8) = w;                                   \
-    }
-                IM_PACK(0, x) IM_PACK(1, y) IM_PACK(2, z) IM_PACK(3, w)
-#undef IM_PACK
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    u32x4_t w;
+                    w[0] = (uint32_t)f32_to_bf16_rne(o[0][e]) | ((uint32_t)f32_to_bf16_rne(o[1][e]) << 16);
+                    w[1] = (uint32_t)f32_to_bf16_rne(o[2][e]) | ((uint32_t)f32_to_bf16_rne(o[3][e]) << 16);
+                    w[2] = (uint32_t)f32_to_bf16_rne(o[4][e]) | ((uint32_t)f32_to_bf16_rne(o[5][e]) << 16);
+                    w[3] = (uint32_t)f32_to_bf16_rne(o[6][e]) | ((uint32_t)f32_to_bf16_rne(o[7][e]) << 16);
+                    *(u32x4_t *)(Bs + (ng * 4 + e) * LDK + kg * 8) = w;
+                }
             }
         }
     };
@@ -471,21 +474,27 @@ static hipError_t launch_bf16(GemmArgs g, int M_pad, hipStream_t s)
     return hipGetLastError();
 }
 
+template <bool IN_OBS, int BN, int WN>
+static hipError_t launch_bf16_sample_t(const GemmArgs &g, int M_pad, hipStream_t s)
+{
+    switch (M_pad / 32) {
+        case 1: return launch_bf16<32, BN, 64, 1, WN, IN_OBS, true>(g, M_pad, s);
+        case 2: return launch_bf16<64, BN, 64, 1, WN, IN_OBS, true>(g, M_pad, s);
+        case 3: return launch_bf16<96, BN, 64, 1, WN, IN_OBS, true>(g, M_pad, s);
+        default: return launch_bf16<128, BN, 64, 1, WN, IN_OBS, true>(g, M_pad, s);
+    }
+}
+
 template <bool IN_OBS>
 static hipError_t launch_bf16_sample(const GemmArgs &g, int M_pad, hipStream_t s)
 {
-    switch (M_pad / 32) {
-        case 1: return launch_bf16<32, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
-        case 2: return launch_bf16<64, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
-        case 3: return launch_bf16<96, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
-        default: return launch_bf16<128, 256, 64, 1, 4, IN_OBS, true>(g, M_pad, s);
-    }
+    if (g.N <= SMALL_BATCH) return launch_bf16_sample_t<IN_OBS, 64, 2>(g, M_pad, s);
+    return launch_bf16_sample_t<IN_OBS, 256, 4>(g, M_pad, s);
 }
 
 // fp32 layers: 128x128 tiles (2x2 waves of 64x64) for large batches; for
 // small batches 64x64 tiles (one 32x32 MFMA tile per wave) so that a layer
 // still spreads over every SIMD.
-constexpr int64_t SMALL_BATCH = 16384;
 
 template <bool BF16, bool IN_OBS, int MT, int NT>
 static hipError_t launch_hidden_t(const GemmArgs &g, int M_pad, hipStream_t s)
@@ -540,9 +549,13 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
 {
     if (g.N <= 0) return hipSuccess;
     if (bf16) {
-        if (!sample)
+        if (!sample) {
+            if (g.N <= SMALL_BATCH)
+                return in_obs ? launch_bf16<128, 128, 64, 2, 2, true, false>(g, M_pad, s)
+                              : launch_bf16<128, 128, 64, 2, 2, false, false>(g, M_pad, s);
             return in_obs ? launch_bf16<256, 256, 32, 2, 2, true, false>(g, M_pad, s)
                           : launch_bf16<256, 256, 32, 2, 2, false, false>(g, M_pad, s);
+        }
         return in_obs ? launch_bf16_sample<true>(g, M_pad, s) : launch_bf16_sample<false>(g, M_pad, s);
     }
     if (!sample)
