@@ -16,10 +16,13 @@ Prints ONE JSON line.  `value` = n_envs * steps / timed seconds.
 `roofline` covers the policy MLP (the dominant call, MFMA-bound),
 `roofline_env` the fused env-step kernel (HBM-bound); both use algorithmic
 work (FLOPs / bytes) over the mean duration measured with HIP events on the
-launch stream during the timed loop.  `cpu_baseline` times the CPU oracle on
-a bounded sample of the same workload.
+launch stream during the timed loop.  `traffic` is the HBM bytes per launch
+measured with the profiler's byte counters on the same kernels (null when the
+kernel sources changed since).  `cpu_baseline` times the CPU oracle on a
+bounded sample of the same workload.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +36,46 @@ sys.path.insert(0, ROOT)
 METRIC = "env-steps/s (ref FK+reward+obs+reset+MLP policy) at 4096 & 65536 envs"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+# Measured HBM traffic per launch: rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE passes
+# over this bench (KiB per dispatch, mean over the dispatches of each kernel), each scaled
+# by what the same counter reads over a plain 512 MiB device copy (bench.py
+# --calibrate-copy 512): FETCH_SIZE reported 262167 KiB for 524288 KiB read, WRITE_SIZE
+# 524288 KiB for 524288 KiB written, so the factors are 2.0 and 1.0.  Each entry is keyed
+# by a hash of the kernel sources the counters were taken on; once a source changes the
+# figure no longer describes the kernel and the bench reports null.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+CSRC = os.path.join(ROOT, "paper_2609_09821_amd", "csrc")
+SHARED_SOURCES = [os.path.join(CSRC, f) for f in ("api.hip", "device_math.h", "launch.h", "tables.h")] + [
+    os.path.join(ROOT, "include", "instantmimic.h")]
+TRAFFIC_KIB = {
+    # policy: one entry per GEMM launch of im_policy_act, in layer order
+    "policy": {"sources": ["policy_kernels.hip"], "sha": "30cc4525d5e561c4", "workloads": {
+        4: {"fetch": [58722.5, 98518.5, 73894.5, 33704.1],
+            "write": [132735.5, 140023.7, 66342.7, 47292.1]}}},
+    "env": {"sources": ["env_kernels.hip"], "sha": "64bddbfd24ce0b36", "workloads": {
+        4: {"fetch": [61771.5], "write": [169502.4]}}},
+}
+
+
+def source_sha(kind):
+    s = hashlib.sha256()
+    for f in [os.path.join(CSRC, x) for x in TRAFFIC_KIB[kind]["sources"]] + SHARED_SOURCES:
+        with open(f, "rb") as fh:
+            s.update(fh.read())
+    return s.hexdigest()[:16]
+
+
+def measured_traffic(kind, wid):
+    """(total, read, write) HBM bytes per launch, or None when not measured on the
+    current kernel sources."""
+    e = TRAFFIC_KIB[kind]
+    m = e["workloads"].get(wid)
+    if m is None or source_sha(kind) != e["sha"]:
+        return None
+    rd = 1024.0 * FETCH_SCALE * sum(m["fetch"])
+    wr = 1024.0 * WRITE_SCALE * sum(m["write"])
+    return rd + wr, rd, wr
 
 
 def algorithmic_env_bytes(B, D, n_envs, n_reset):
@@ -195,6 +238,8 @@ def main():
     mlp_tflops = r["flops"] / (r["pol_ms"] * 1e-3) / 1e12
     env_gbs = r["env_bytes"] / (r["env_ms"] * 1e-3) / 1e9
     peak = MFMA_PEAK_TFLOPS[r["prec"]]
+    tr_pol = measured_traffic("policy", args.workload)
+    tr_env = measured_traffic("env", args.workload)
     out = {
         "metric": METRIC,
         "value": r["value"],
@@ -221,13 +266,17 @@ def main():
         "roofline": {
             "kernel": "policy MLP (im_policy_act: one MFMA GEMM per layer)",
             "bound": "mfma", "achieved": mlp_tflops, "peak": peak, "unit": "TFLOP/s",
-            "frac": mlp_tflops / peak, "traffic": None,
+            "frac": mlp_tflops / peak, "traffic": tr_pol and tr_pol[0],
+            "traffic_unit": "HBM bytes per launch",
+            "traffic_read_write": tr_pol and tr_pol[1:],
             "per_launch_ms": r["pol_ms"], "work_per_launch": r["flops"],
         },
         "roofline_env": {
             "kernel": "env_step_kernel (im_env_step_fused)",
             "bound": "hbm", "achieved": env_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": env_gbs / HBM_PEAK_GBS, "traffic": None,
+            "frac": env_gbs / HBM_PEAK_GBS, "traffic": tr_env and tr_env[0],
+            "traffic_unit": "HBM bytes per launch",
+            "traffic_read_write": tr_env and tr_env[1:],
             "per_launch_ms": r["env_ms"], "work_per_launch": r["env_bytes"],
         },
     }
