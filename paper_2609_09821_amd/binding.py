@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libinstantmimic.so")
 
 IM_OK, IM_ERR_INVALID_ARG, IM_ERR_UNSUPPORTED, IM_ERR_OOM, IM_ERR_HIP = range(5)
 IM_DTYPE_F32, IM_DTYPE_BF16 = 0, 1
+IM_JOINT_FREE, IM_JOINT_SPHERICAL, IM_JOINT_REVOLUTE, IM_JOINT_FIXED = range(4)
 
 
 class ImConfig(C.Structure):
@@ -208,10 +209,11 @@ class EnvBuffers:
     ENV = ("env_clip", "env_phase", "env_t", "env_n")
 
 
-class Context:
-    """A library context built from a synthetic world description."""
+class Description:
+    """The C structs of a synthetic world description (host memory only; the
+    arrays they point to are kept alive by this object)."""
 
-    def __init__(self, desc, max_envs):
+    def __init__(self, desc):
         sk = desc["skeleton"]
         cfg = desc["config"]
         pol = desc["policy"]
@@ -238,6 +240,7 @@ class Context:
                             _ptr(k(_f32(c["root_quat"])), C.c_float),
                             _ptr(k(_f32(c["local_quat"])), C.c_float))
         self.clips = arr
+        self.n_clips = len(clips)
         L = len(pol["W"])
         dims = k(_i32(pol["dims"]))
         bf16 = bool(pol["bf16"])
@@ -251,9 +254,24 @@ class Context:
                 w = k(w)
             wptrs[l] = w.ctypes.data
             bptrs[l] = _ptr(k(_f32(pol["b"][l])), C.c_float)
+        self.weight_ptrs, self.bias_ptrs = wptrs, bptrs
         self.policy = ImPolicy(L, _ptr(dims, C.c_int32), IM_DTYPE_BF16 if bf16 else IM_DTYPE_F32,
                                wptrs, bptrs, _ptr(k(_f32(pol["log_std"])), C.c_float))
-        self.ptr = im_create(self.cfg, self.skel, self.clips, len(clips), self.policy, max_envs)
+
+    def create_status(self, max_envs):
+        """Raw im_create: (status, context pointer or None)."""
+        out = C.c_void_p()
+        st = lib().im_create(C.byref(self.cfg), C.byref(self.skel), self.clips, self.n_clips,
+                             C.byref(self.policy), int(max_envs), C.byref(out))
+        return st, out
+
+
+class Context:
+    """A library context built from a synthetic world description."""
+
+    def __init__(self, desc, max_envs):
+        d = self.desc = Description(desc)
+        self.ptr = im_create(d.cfg, d.skel, d.clips, d.n_clips, d.policy, max_envs)
         self.info = im_get_info(self.ptr)
 
     def close(self):

@@ -1,0 +1,231 @@
+"""Edge cases of the C ABI on the GPU, each checked against the oracle or
+against the call's documented contract: empty batches, a leading dimension
+above the env count (the tail is never touched), partial reset masks,
+truncation at the phase boundary, non-finite sim state, the grace period and
+the fall height."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_09821_amd import binding, synth
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL_F = -12345.5
+SENTINEL_I = -777
+
+
+def _setup(cfg, N, ld=None, max_envs=None, **over):
+    d = synth.make_world(cfg, n_envs=max(N, 1), **over)
+    w = oracle.World(d)
+    ctx = binding.Context(d, max_envs=max_envs or max(N, 1))
+    bufs = ctx.buffers(N, ld)
+    return d, w, ctx, bufs
+
+
+def _fill_all(bufs):
+    for name in binding.EnvBuffers.SIM + ("env_phase", "reward", "obs"):
+        getattr(bufs, name).fill_(SENTINEL_F)
+    for name in ("env_clip", "env_t", "env_n", "ref_frame"):
+        getattr(bufs, name).fill_(SENTINEL_I)
+    bufs.terminated.fill_(0xA5)
+    bufs.truncated.fill_(0x5A)
+
+
+def _snapshot(bufs):
+    names = binding.EnvBuffers.SIM + binding.EnvBuffers.ENV + (
+        "reward", "terminated", "truncated", "obs", "ref_frame")
+    return {k: getattr(bufs, k).clone() for k in names}
+
+
+def _tail(t, N):
+    return t[..., N:]
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_zero_envs_touch_nothing(cfg):
+    d, w, ctx, bufs = _setup(cfg, 0, ld=64, max_envs=64)
+    _fill_all(bufs)
+    before = _snapshot(bufs)
+    A = d["policy"]["dims"][-1]
+    mean = torch.full((1, A), SENTINEL_F, device="cuda")
+    act = mean.clone()
+    logp = torch.full((1,), SENTINEL_F, device="cuda")
+    ctx.reset_envs(bufs)
+    ctx.standin_physics(bufs, 0.1, 0.5)
+    ctx.env_step_fused(bufs)
+    ctx.policy_act(bufs.obs, bufs.env_n, 0, mean, act, logp)
+    torch.cuda.synchronize()
+    for k, v in _snapshot(bufs).items():
+        assert torch.equal(v, before[k]), k
+    assert (mean == SENTINEL_F).all() and (act == SENTINEL_F).all() and (logp == SENTINEL_F).all()
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_leading_dimension_tail_untouched_and_results_unchanged(cfg):
+    N, T = 1000, 3
+    d, w, ctx, a = _setup(cfg, N)                       # ld = N
+    b = ctx.buffers(N, ld=1000 + 88)                    # ld > N, not a multiple of 64
+    _fill_all(b)
+    b.env_n[:N].zero_()                                  # the same counters as `a`
+    A = d["policy"]["dims"][-1]
+    outs = {}
+    for key, bufs in (("a", a), ("b", b)):
+        ctx.reset_envs(bufs)
+        mean = torch.full((N, A), SENTINEL_F, device="cuda")
+        act = mean.clone()
+        logp = torch.full((N,), SENTINEL_F, device="cuda")
+        for t in range(T):
+            ctx.policy_act(bufs.obs, bufs.env_n, N, mean, act, logp)
+            ctx.standin_physics(bufs, d["sigma_joint"], d["sigma_vel"])
+            ctx.env_step_fused(bufs)
+        torch.cuda.synchronize()
+        outs[key] = (_snapshot(bufs), mean.clone(), act.clone(), logp.clone())
+    sa, sb = outs["a"][0], outs["b"][0]
+    for k in sa:
+        assert torch.equal(sa[k], sb[k][..., :N]), k + " differs with ld > n_envs"
+        tail = _tail(sb[k], N)
+        fill = {"terminated": 0xA5, "truncated": 0x5A}.get(
+            k, SENTINEL_F if tail.dtype == torch.float32 else SENTINEL_I)
+        assert (tail == fill).all(), k + " tail written"
+    for i in (1, 2, 3):
+        assert torch.equal(outs["a"][i], outs["b"][i]), "policy output differs with ld_obs > n_envs"
+
+
+@pytest.mark.parametrize("cfg", [2, 5])
+def test_partial_mask_reset(cfg):
+    N = 1500
+    d, w, ctx, bufs = _setup(cfg, N)
+    rng = np.random.default_rng(cfg)
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    for _ in range(3):                       # a state away from the initial reset
+        w.standin(st, d["sigma_joint"], d["sigma_vel"])
+        w.env_step(st)
+    mask = (rng.random(N) < 0.3).astype(np.uint8)
+    mask[0], mask[-1] = 1, 0
+    H.upload_state(st, bufs)
+    bufs.obs[:, :N].copy_(torch.from_numpy(st.obs))
+    before = H.download(bufs, N)
+    ctx.reset_envs(bufs, mask=torch.from_numpy(mask).cuda())
+    w.reset_envs(st, mask)
+    g = H.download(bufs, N)
+    m = mask.astype(bool)
+    for name in ("clip", "phase", "t", "n"):
+        assert np.array_equal(getattr(g, name), getattr(st, name)), name
+    H.compare_sim_obs(g, st, m, "masked reset")
+    keep = ~m
+    for name in ("pos", "quat", "linvel", "angvel"):
+        assert np.array_equal(getattr(g, name)[:, :, keep], getattr(before, name)[:, :, keep]), name
+    assert np.array_equal(g.obs[:, keep], before.obs[:, keep]), "obs of unmasked envs"
+    assert np.array_equal(g.n, before.n), "reset_envs does not advance the counter"
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_truncation_at_the_phase_boundary(cfg):
+    N = 512
+    d, w, ctx, bufs = _setup(cfg, N)
+    c = d["config"]
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    # phases within a few ulp of 1 - dphi, where phi + dphi crosses 1.0f; dphi as the
+    # clip's per-step phase increment, rounded once to fp32
+    F = d["clips"][0]["n_frames"]
+    fps = np.float32(d["clips"][0]["fps"])
+    dphi = np.float32(np.float64(c["dt"]) * np.float64(fps) / (F - 1))
+    st.clip[:] = 0
+    base = np.float32(1.0) - dphi
+    ks = np.arange(N) % 33 - 16
+    ph = base.copy() * np.ones(N, np.float32)
+    for i, k in enumerate(ks):
+        x = np.float32(base)
+        step = np.float32(np.inf) if k > 0 else np.float32(-np.inf)
+        for _ in range(abs(int(k))):
+            x = np.nextafter(x, step)
+        ph[i] = x
+    st.phase[:] = ph
+    st.t[:] = 3
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    H.upload_state(st, bufs)
+    t_next = st.t + 1
+    z_root = st.pos[0, 2].copy()
+    ctx.env_step_fused(bufs)
+    w.env_step(st)
+    g = H.download(bufs, N)
+    live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, np.ones(N, bool))
+    H.compare_sim_obs(g, st, live, "truncation")
+    expect = (ph + dphi) >= np.float32(1.0)
+    assert np.array_equal(g.truncated.astype(bool), expect)
+    assert 0 < expect.sum() < N
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_non_finite_sim_state_terminates_and_resets(cfg):
+    N = 700
+    d, w, ctx, bufs = _setup(cfg, N)
+    c = d["config"]
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    bad = np.zeros(N, bool)
+    bad[5::37] = True
+    idx = np.flatnonzero(bad)
+    st.pos[3, 1, idx[0::3]] = np.nan
+    st.linvel[2, 0, idx[1::3]] = np.nan
+    st.pos[0, 2, idx[2::3]] = np.nan
+    H.upload_state(st, bufs)
+    t_next = st.t + 1
+    z_root = st.pos[0, 2].copy()
+    ctx.env_step_fused(bufs)
+    w.env_step(st)
+    g = H.download(bufs, N)
+    assert np.all(np.isnan(g.reward[bad])) and np.all(np.isnan(st.reward[bad]))
+    assert np.all(g.terminated[bad] == 1) and np.all(st.terminated[bad] == 1)
+    live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, ~bad)
+    for name in ("clip", "phase", "t", "n"):
+        assert np.array_equal(getattr(g, name)[bad], getattr(st, name)[bad]), name
+    H.compare_sim_obs(g, st, live | bad, "after non-finite state")
+    assert np.all(np.isfinite(g.obs[:, bad]))
+
+
+def test_grace_period_and_fall_height():
+    N, grace = 600, 4
+    d, w, ctx, bufs = _setup(2, N, grace=grace, h_term=5.0)   # every root is "below" 5 m
+    c = d["config"]
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    H.upload_state(st, bufs)
+    live = np.ones(N, bool)
+    for step in range(grace + 3):
+        w.standin(st, d["sigma_joint"], d["sigma_vel"])
+        H.upload_state(st, bufs, env=False)
+        t_next = st.t + 1
+        z_root = st.pos[0, 2].copy()
+        ctx.env_step_fused(bufs)
+        w.env_step(st)
+        g = H.download(bufs, N)
+        live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, live)
+        H.compare_sim_obs(g, st, live, "grace step %d" % step)
+        assert np.array_equal(g.terminated.astype(bool), t_next > grace)
+    assert live.all()
+
+
+def test_terminated_reset_draws_are_uniform():
+    # the in-step reset's clip draw over many envs: every clip of config 5 (16 clips) is hit
+    N = 4096
+    d, w, ctx, bufs = _setup(5, N, h_term=5.0)
+    ctx.reset_envs(bufs)
+    ctx.standin_physics(bufs, d["sigma_joint"], d["sigma_vel"])
+    ctx.env_step_fused(bufs)
+    torch.cuda.synchronize()
+    assert bool(bufs.terminated[:N].all())
+    clips = bufs.env_clip[:N].cpu().numpy()
+    counts = np.bincount(clips, minlength=len(d["clips"]))
+    exp = N / len(d["clips"])
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    assert chi2 < 40.0, counts        # 15 dof: p ~ 5e-4
+    ph = bufs.env_phase[:N].cpu().numpy()
+    assert ph.min() >= 0.0 and ph.max() < 1.0
+    assert np.all(bufs.env_t[:N].cpu().numpy() == 0)

@@ -174,3 +174,22 @@ def test_standin_local_rotation_noise():
             assert np.abs(rv).max() < 1e-3
     root = (R(ref.quat[0]).inv() * R(st.quat[0])).as_rotvec() / sig
     assert np.all(np.abs(root.std(0) - 1) < 0.06)
+
+
+def test_step_non_finite_state_terminates_and_resets():
+    # a NaN anywhere in the read sim state makes the reward NaN, which fails r >= r_min
+    d = synth.make_world(2, n_envs=30)
+    w = oracle.World(d)
+    st = oracle.State(w.B, 30)
+    w.reset_envs(st)
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    st.pos[4, 0, 0:10] = np.nan
+    st.linvel[7, 2, 10:20] = np.nan
+    prev_n = st.n.copy()
+    w.env_step(st)
+    assert np.all(np.isnan(st.reward[:20])) and np.all(np.isfinite(st.reward[20:]))
+    assert st.terminated[:20].all()
+    for e in range(20):
+        k, p = w.reset_draw(e, int(prev_n[e]) + 1, 1)
+        assert st.clip[e] == k and st.phase[e] == p and st.t[e] == 0
+    assert np.all(np.isfinite(st.obs[:, :20])) and np.all(np.isfinite(st.pos[:, :, :20]))
