@@ -33,6 +33,86 @@ constexpr float HALF_LOG_2PI = 0.91893853320467274f;
 // spreads over all 256 CUs.
 constexpr int64_t SMALL_BATCH = 16384;
 
+// Writes n_valid*A consecutive floats from LDS to dst (16-byte stores when dst
+// is 16-byte aligned).
+template <int NTHR>
+__device__ __forceinline__ void copy_rows_out(float *dst, const float *so, int64_t cnt, int tid)
+{
+    if ((((uintptr_t)dst) & 15) == 0) {
+        const int64_t c4 = cnt >> 2;
+        for (int64_t v = tid; v < c4; v += NTHR)
+            *(f32x4_t *)(dst + 4 * v) = *(const f32x4_t *)(so + 4 * v);
+        for (int64_t v = 4 * c4 + tid; v < cnt; v += NTHR) dst[v] = so[v];
+    } else {
+        for (int64_t v = tid; v < cnt; v += NTHR) dst[v] = so[v];
+    }
+}
+
+// Epilogue of the last layer: mean = acc + b, Gaussian noise from Philox, action
+// = mean + exp(log_std) z, logp.  The accumulators follow the 32x32 MFMA layout
+// (lane column = env, rows 8*grp + 4*(lane/32) + q = actions); the block covers
+// every action of its envs (m0 == 0).  The block's envs n0 .. n0+nv-1 own the
+// contiguous ranges mean[n0*A .. (n0+nv)*A) and action[...], so both are staged
+// in LDS (`so`, at least BN*A floats, free once the main loop has ended with a
+// barrier) and written out with wide stores; the accumulators are reused to hold
+// the actions between the two passes.
+template <int NTHR, int TM, int TN>
+__device__ __forceinline__ void sample_epilogue(const GemmArgs &g, float *so, int64_t n0, int64_t nv,
+                                                int col0, int tid, f32x16_t (&acc)[TM][TN])
+{
+    const int lane = tid & 63;
+    const int A = g.A;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int nl = col0 + j * 32 + (lane & 31);
+        const int64_t n = n0 + nl;
+        const bool valid_n = nl < nv;
+        const uint32_t en = valid_n ? g.env_n[n] : 0u;
+        float lp = 0.0f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const int mb = i * 32 + 8 * grp + 4 * (lane >> 5);
+                if (!valid_n || mb >= A) continue;
+                float z[4];
+                normals4(g.seed, (uint32_t)n, en, (uint32_t)(mb >> 2), 0u, z);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int m = mb + q;
+                    if (m < A) {
+                        const float mu = acc[i][j][4 * grp + q] + g.bias[m];
+                        const float ls = g.log_std[m];
+                        so[nl * A + m] = mu;
+                        acc[i][j][4 * grp + q] = mu + expf(ls) * z[q];
+                        lp += 0.5f * z[q] * z[q] + ls + HALF_LOG_2PI;
+                    }
+                }
+            }
+        lp += __shfl_xor(lp, 32);
+        if (valid_n && lane < 32 && g.logp) g.logp[n] = -lp;
+    }
+    __syncthreads();
+    copy_rows_out<NTHR>(g.mean + n0 * A, so, nv * A, tid);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int nl = col0 + j * 32 + (lane & 31);
+        if (nl >= nv) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const int mb = i * 32 + 8 * grp + 4 * (lane >> 5);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (mb + q < A) so[nl * A + mb + q] = acc[i][j][4 * grp + q];
+            }
+    }
+    __syncthreads();
+    copy_rows_out<NTHR>(g.action + n0 * A, so, nv * A, tid);
+}
+
 // fp32 layer GEMM.  Tile: WGM x WGN waves, each MT x NT MFMA tiles of 32x32
 // (v_mfma_f32_32x32x2_f32); K chunk 32.  16-byte global loads into
 // registers one chunk ahead, two LDS buffers, one barrier per chunk.  The
@@ -51,7 +131,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
     constexpr int O_CH = KC * (BN / 4) / NTHR;   // observation: float4 (4 envs of one k) per thread
     static_assert(BM * (KC / 4) % NTHR == 0 && BN * (KC / 4) % NTHR == 0 && KC * (BN / 4) % NTHR == 0, "split");
 
-    __shared__ __attribute__((aligned(16))) float lds[2 * STAGE];
+    // the sampling epilogue reuses the stage buffers for a BN x A output tile
+    constexpr int LDS_FLOATS = (SAMPLE && BN * BM > 2 * STAGE) ? BN * BM : 2 * STAGE;
+    __shared__ __attribute__((aligned(16))) float lds[LDS_FLOATS];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -191,33 +273,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
                 }
             }
     } else {
-        // the block covers every action (m0 == 0); NT == 1
-        const int64_t n = n0 + wn * 32 + (lane & 31);
-        const bool valid_n = n < g.N;
-        float lp = 0.0f;
-        const uint32_t en = valid_n ? g.env_n[n] : 0u;
-#pragma unroll
-        for (int i = 0; i < MT; ++i)
-#pragma unroll
-            for (int grp = 0; grp < 4; ++grp) {
-                const int mb = i * 32 + 8 * grp + 4 * (lane >> 5);
-                if (!valid_n || mb >= g.A) continue;
-                float z[4];
-                normals4(g.seed, (uint32_t)n, en, (uint32_t)(mb >> 2), 0u, z);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int m = mb + q;
-                    if (m < g.A) {
-                        const float mu = acc[i][0][4 * grp + q] + g.bias[m];
-                        const float ls = g.log_std[m];
-                        g.mean[n * g.A + m] = mu;
-                        g.action[n * g.A + m] = mu + expf(ls) * z[q];
-                        lp += 0.5f * z[q] * z[q] + ls + HALF_LOG_2PI;
-                    }
-                }
-            }
-        lp += __shfl_xor(lp, 32);
-        if (valid_n && lane < 32 && g.logp) g.logp[n] = -lp;
+        // the block covers every action (m0 == 0)
+        const int64_t nv = g.N - n0 < BN ? g.N - n0 : BN;
+        sample_epilogue<NTHR, MT, NT>(g, lds, n0, nv, wn * NT * 32, tid, acc);
     }
 }
 
@@ -227,8 +285,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
 // MFMA tiles.  Two LDS stages: while the waves run the MFMAs of stage k from
 // LDS, the 16-byte global loads of stage k+1 (issued one stage earlier) are
 // written into the other LDS buffer and those of stage k+2 are issued.  Rows
-// are padded by 16 bytes so that the 8-lane phases of ds_read_b128 and
-// ds_write_b128 hit distinct banks.  Blocks are renumbered so that the
+// are padded by 16 bytes: at K step 64 (144-byte rows) the fragment reads
+// and tile writes are free of bank conflicts (at K step 32, 80-byte rows, a
+// third of the LDS cycles were conflicts).  Blocks are renumbered so that the
 // feature blocks sharing one env block run on the same XCD (workgroups are
 // dealt to the 8 XCDs round-robin) and share its L2.
 // ---------------------------------------------------------------------------
@@ -247,7 +306,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
     constexpr int B_TASKS = KQ * (BN / 4) / NTHR;  // obs: 8 k x 4 n blocks per thread
     static_assert(IN_OBS ? (KQ * (BN / 4) % NTHR == 0) : (BN * KQ % NTHR == 0), "split");
 
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+    // the sampling epilogue reuses the stage buffers for a BN x A fp32 output tile
+    constexpr int LDS_ELEMS = (SAMPLE && 2 * BN * BM > 2 * STAGE) ? 2 * BN * BM : 2 * STAGE;
+    __shared__ __attribute__((aligned(16))) uint16_t lds[LDS_ELEMS];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -432,35 +493,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
             }
     } else {
         // every action of an env lies in one wave (WM == 1, m0 == 0)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t n = n0 + wn * (TN * 32) + j * 32 + (lane & 31);
-            const bool valid_n = n < g.N;
-            const uint32_t en = valid_n ? g.env_n[n] : 0u;
-            float lp = 0.0f;
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int grp = 0; grp < 4; ++grp) {
-                    const int mb = i * 32 + 8 * grp + 4 * (lane >> 5);
-                    if (!valid_n || mb >= g.A) continue;
-                    float z[4];
-                    normals4(g.seed, (uint32_t)n, en, (uint32_t)(mb >> 2), 0u, z);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int m = mb + q;
-                        if (m < g.A) {
-                            const float mu = acc[i][j][4 * grp + q] + g.bias[m];
-                            const float ls = g.log_std[m];
-                            g.mean[n * g.A + m] = mu;
-                            g.action[n * g.A + m] = mu + expf(ls) * z[q];
-                            lp += 0.5f * z[q] * z[q] + ls + HALF_LOG_2PI;
-                        }
-                    }
-                }
-            lp += __shfl_xor(lp, 32);
-            if (valid_n && lane < 32 && g.logp) g.logp[n] = -lp;
-        }
+        const int64_t nv = g.N - n0 < BN ? g.N - n0 : BN;
+        sample_epilogue<NTHR, TM, TN>(g, (float *)lds, n0, nv, wn * (TN * 32), tid, acc);
     }
 }
 
@@ -489,7 +523,7 @@ template <bool IN_OBS>
 static hipError_t launch_bf16_sample(const GemmArgs &g, int M_pad, hipStream_t s)
 {
     if (g.N <= SMALL_BATCH) return launch_bf16_sample_t<IN_OBS, 64, 2>(g, M_pad, s);
-    return launch_bf16_sample_t<IN_OBS, 256, 4>(g, M_pad, s);
+    return launch_bf16_sample_t<IN_OBS, 128, 4>(g, M_pad, s);
 }
 
 // fp32 layers: 128x128 tiles (2x2 waves of 64x64) for large batches; for
@@ -549,12 +583,15 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
 {
     if (g.N <= 0) return hipSuccess;
     if (bf16) {
+        // large batches: 256x256 tiles of 8 waves (two per SIMD, so that one
+        // wave's LDS reads overlap the other's MFMAs), K step 64; the last layer
+        // 128 envs per block of 4 waves
         if (!sample) {
             if (g.N <= SMALL_BATCH)
                 return in_obs ? launch_bf16<128, 128, 64, 2, 2, true, false>(g, M_pad, s)
                               : launch_bf16<128, 128, 64, 2, 2, false, false>(g, M_pad, s);
-            return in_obs ? launch_bf16<256, 256, 32, 2, 2, true, false>(g, M_pad, s)
-                          : launch_bf16<256, 256, 32, 2, 2, false, false>(g, M_pad, s);
+            return in_obs ? launch_bf16<256, 256, 64, 2, 4, true, false>(g, M_pad, s)
+                          : launch_bf16<256, 256, 64, 2, 4, false, false>(g, M_pad, s);
         }
         return in_obs ? launch_bf16_sample<true>(g, M_pad, s) : launch_bf16_sample<false>(g, M_pad, s);
     }
