@@ -306,8 +306,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
     constexpr int B_TASKS = KQ * (BN / 4) / NTHR;  // obs: 8 k x 4 n blocks per thread
     static_assert(IN_OBS ? (KQ * (BN / 4) % NTHR == 0) : (BN * KQ % NTHR == 0), "split");
 
-    // the sampling epilogue reuses the stage buffers for a BN x A fp32 output tile
-    constexpr int LDS_ELEMS = (SAMPLE && 2 * BN * BM > 2 * STAGE) ? 2 * BN * BM : 2 * STAGE;
+    // the epilogues reuse the stage buffers for the output tile (bf16 BM x BN,
+    // or fp32 BN x A for the sampling layer)
+    constexpr int OUT_ELEMS = SAMPLE ? 2 * BN * BM : BN * BM;
+    constexpr int LDS_ELEMS = OUT_ELEMS > 2 * STAGE ? OUT_ELEMS : 2 * STAGE;
     __shared__ __attribute__((aligned(16))) uint16_t lds[LDS_ELEMS];
 
     const int tid = threadIdx.x;
@@ -471,26 +473,41 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
     }
 
     if constexpr (!SAMPLE) {
-        uint16_t *Y = (uint16_t *)g.y;
+        // bias, ReLU, bf16; the tile is staged env-major in LDS ([env][feature]
+        // rows of BM*2 bytes, 16-byte chunks XOR-swizzled by env) and written
+        // out in whole rows
+        constexpr int CPR = BM / 8;             // 16-byte chunks per staged row
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int64_t n = n0 + wn * (TN * 32) + j * 32 + (lane & 31);
-                if (n >= g.N) continue;
+                const int nl = wn * (TN * 32) + j * 32 + (lane & 31);
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp) {
-                    const int64_t m = m0 + wm * (TM * 32) + i * 32 + 8 * grp + 4 * (lane >> 5);
-                    const float4 bb = *(const float4 *)(g.bias + m);
+                    const int ml = wm * (TM * 32) + i * 32 + 8 * grp + 4 * (lane >> 5);
+                    const float4 bb = *(const float4 *)(g.bias + m0 + ml);
                     const float v0 = fmaxf(acc[i][j][4 * grp + 0] + bb.x, 0.0f);
                     const float v1 = fmaxf(acc[i][j][4 * grp + 1] + bb.y, 0.0f);
                     const float v2 = fmaxf(acc[i][j][4 * grp + 2] + bb.z, 0.0f);
                     const float v3 = fmaxf(acc[i][j][4 * grp + 3] + bb.w, 0.0f);
                     const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
                     const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
-                    *(uint2 *)(Y + n * g.ld_y + m) = make_uint2(lo, hi);
+                    const int chunk = (ml >> 3) ^ (nl & (CPR - 1));
+                    *(uint2 *)(lds + nl * BM + chunk * 8 + 4 * (lane >> 5)) = make_uint2(lo, hi);
                 }
             }
+        __syncthreads();
+        uint16_t *Y = (uint16_t *)g.y;
+        constexpr int RPP = NTHR / CPR;         // rows per pass
+        const int cl = tid % CPR;
+#pragma unroll 4
+        for (int pass = 0; pass < BN / RPP; ++pass) {
+            const int nl = pass * RPP + tid / CPR;
+            const int64_t n = n0 + nl;
+            if (n < g.N)
+                *(uint4 *)(Y + n * g.ld_y + m0 + cl * 8) =
+                    *(const uint4 *)(lds + nl * BM + ((cl ^ (nl & (CPR - 1))) * 8));
+        }
     } else {
         // every action of an env lies in one wave (WM == 1, m0 == 0)
         const int64_t nv = g.N - n0 < BN ? g.N - n0 : BN;
@@ -505,6 +522,193 @@ static hipError_t launch_bf16(GemmArgs g, int M_pad, hipStream_t s)
     const int64_t nb = (g.N + BN - 1) / BN;
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WM, WN, IN_OBS, SAMPLE>),
                        dim3((unsigned)(nb * g.M_blocks)), dim3(64 * WM * WN), 0, s, g);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// bf16 hidden-layer GEMM for large batches, ping-pong schedule.  Tile 256x256
+// (features x envs), K step 64, 8 waves in two groups of four.  Waves are
+// dealt to the 4 SIMDs round-robin, so every SIMD holds one wave of each
+// group.  Group g owns feature rows [128g, 128g+128) of the tile and its wave
+// w owns env columns [64w, 64w+64): 4x2 MFMA tiles of 32x32 each.  The groups
+// alternate between two phases separated by workgroup barriers: while one
+// group runs the 32 MFMAs of a K step from fragments already in its
+// registers, the other reads its fragments of the K step from LDS (group 0
+// also issues the global->LDS loads of the next K step), so each SIMD's
+// MFMA pipe is fed by one wave while the other waits on memory.  Operands
+// move global->LDS without passing through registers (buffer loads with the
+// LDS flag, 16 bytes per lane; past the buffer end they return zero, which
+// pads the env tail).  A 128-byte LDS row holds its eight 16-byte chunks
+// XOR-swizzled by (row/2)%8, so that fragment reads of 16 consecutive rows
+// hit distinct banks.  Two LDS stages of 64 KB; a K step's loads are issued
+// two phases before its first fragment read.
+// ---------------------------------------------------------------------------
+#define IM_LDS_AS __attribute__((address_space(3)))
+
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+__device__ __forceinline__ void wg_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+__global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
+{
+    constexpr int BK = 64;
+    constexpr int ROWB = BK * 2;                // bytes per LDS row
+    constexpr int TILE_B = 256 * ROWB;          // one 256-row operand tile
+    constexpr int STAGE_B = 2 * TILE_B;         // weight tile, then activation tile
+    constexpr int TM = 4, TN = 2, NS = BK / 16;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE_B];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+    const int grp = wave >> 2, wi = wave & 3;
+
+    const int mblocks = g.M_blocks;
+    const int nblk = gridDim.x;
+    int bid = blockIdx.x;
+    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+    const int64_t m0 = (int64_t)(bid % mblocks) * 256;
+    const int64_t n0 = (int64_t)(bid / mblocks) * 256;
+    const int nk = g.K_pad / BK;
+
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.w, (short)0, (int)g.w_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
+
+    // Loads (group 0): thread t fills 16-byte slot 256c + t of a stage, c = 0..15;
+    // slots 0..2047 are the weight tile, 2048.. the activation tile.  Slot s of a
+    // tile: row s/8, physical chunk s%8 = t%8, holding logical chunk
+    // (t%8) ^ ((row/2)%8); the row is 32c' + t/8, so the swizzle depends on t only.
+    const int lrow = (tid & 255) >> 3;
+    const int lq = (tid & 7) ^ ((lrow >> 1) & 7);
+    const uint32_t a_voff = (uint32_t)((lrow * g.K_pad + lq * 8) * 2);
+    const uint32_t b_voff = (uint32_t)((lrow * g.ld_x + lq * 8) * 2);
+    // Activation row offsets stay in the per-lane offset (the part the buffer
+    // range check sees), so rows past the env count read as zero; weight rows
+    // are always in range.
+    auto issue = [&](int kt, int buf) {
+        uint8_t *base = lds + buf * STAGE_B + (tid & ~63) * 16;
+        const uint32_t k2 = (uint32_t)(kt * BK * 2);
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wr, (IM_LDS_AS void *)(base + c * 256 * 16), 16, a_voff,
+                (uint32_t)(((m0 + 32 * c) * g.K_pad) * 2) + k2, 0, 0);
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                xr, (IM_LDS_AS void *)(base + TILE_B + c * 256 * 16), 16,
+                b_voff + (uint32_t)(((n0 + 32 * c) * g.ld_x) * 2), k2, 0, 0);
+    };
+
+    bf16x8_t fa[NS][TM], fb[NS][TN];
+    auto read_frags = [&](int buf) {
+        const uint8_t *As = lds + buf * STAGE_B;
+        const uint8_t *Bs = As + TILE_B;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int q = 2 * s + (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = grp * 128 + i * 32 + (lane & 31);
+                fa[s][i] = *(const bf16x8_t *)(As + r * ROWB + ((q ^ ((r >> 1) & 7)) * 16));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = wi * 64 + j * 32 + (lane & 31);
+                fb[s][j] = *(const bf16x8_t *)(Bs + r * ROWB + ((q ^ ((r >> 1) & 7)) * 16));
+            }
+        }
+        wait_lgkmcnt0();
+    };
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    auto mfma_step = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+    };
+
+    // Both groups run the same loop (read K step kt; barrier; MFMAs of kt;
+    // barrier), group 1 one phase behind group 0: it passes one extra barrier
+    // first, and group 0 one extra barrier at the end so that the counts match.
+    if (grp == 0) {
+        issue(0, 0);
+        wait_vmcnt0();
+    }
+    wg_barrier();
+    if (grp == 1) wg_barrier();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        read_frags(buf);
+        // the other buffer was last read in the two phases before this one
+        if (grp == 0 && kt + 1 < nk) issue(kt + 1, buf ^ 1);
+        wg_barrier();
+        mfma_step();
+        wait_vmcnt0();              // group 0: K step kt+1 has landed in LDS
+        wg_barrier();
+    }
+    if (grp == 0) wg_barrier();
+
+    // Epilogue through LDS (free now): bias, ReLU, bf16; the 256x256 tile is
+    // staged env-major ([env][feature], 512-byte rows, 16-byte chunks
+    // XOR-swizzled by env % 32) and written out in whole rows, 1 KB per wave
+    // instruction, instead of 16-byte pieces of 32 rows.
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int nl = wi * 64 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ml = grp * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
+                const float4 bb = *(const float4 *)(g.bias + m0 + ml);
+                const float v0 = fmaxf(acc[i][j][4 * q + 0] + bb.x, 0.0f);
+                const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
+                const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
+                const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
+                const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+                const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+                const int chunk = (ml >> 3) ^ (nl & 31);
+                *(uint2 *)(lds + nl * 512 + chunk * 16 + 8 * (lane >> 5)) = make_uint2(lo, hi);
+            }
+        }
+    __syncthreads();
+    uint16_t *Y = (uint16_t *)g.y;
+    const int cl = tid & 31;
+#pragma unroll 4
+    for (int pass = 0; pass < 16; ++pass) {
+        const int nl = pass * 16 + (tid >> 5);
+        const int64_t n = n0 + nl;
+        if (n < g.N)
+            *(uint4 *)(Y + n * g.ld_y + m0 + cl * 8) =
+                *(const uint4 *)(lds + nl * 512 + ((cl ^ (nl & 31)) * 16));
+    }
+}
+
+static hipError_t launch_bf16_pp(GemmArgs g, int M_pad, hipStream_t s)
+{
+    g.M_blocks = M_pad / 256;
+    const int64_t nb = (g.N + 255) / 256;
+    hipLaunchKernelGGL(gemm_bf16_pp_kernel, dim3((unsigned)(nb * g.M_blocks)), dim3(512), 0, s, g);
     return hipGetLastError();
 }
 
@@ -584,14 +788,15 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
     if (g.N <= 0) return hipSuccess;
     if (bf16) {
         // large batches: 256x256 tiles of 8 waves (two per SIMD, so that one
-        // wave's LDS reads overlap the other's MFMAs), K step 64; the last layer
-        // 128 envs per block of 4 waves
+        // wave's LDS reads overlap the other's MFMAs), K step 64 -- the ping-pong
+        // kernel where the input is a bf16 hidden layer; the last layer 128 envs
+        // per block of 4 waves
         if (!sample) {
             if (g.N <= SMALL_BATCH)
                 return in_obs ? launch_bf16<128, 128, 64, 2, 2, true, false>(g, M_pad, s)
                               : launch_bf16<128, 128, 64, 2, 2, false, false>(g, M_pad, s);
             return in_obs ? launch_bf16<256, 256, 64, 2, 4, true, false>(g, M_pad, s)
-                          : launch_bf16<256, 256, 64, 2, 4, false, false>(g, M_pad, s);
+                          : launch_bf16_pp(g, M_pad, s);
         }
         return in_obs ? launch_bf16_sample<true>(g, M_pad, s) : launch_bf16_sample<false>(g, M_pad, s);
     }
