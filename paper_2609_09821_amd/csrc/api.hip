@@ -33,6 +33,8 @@ struct im_ctx {
     std::vector<float *> d_b;
     float *d_log_std = nullptr;
     void *d_ws[2] = {nullptr, nullptr};
+    void *d_obs16 = nullptr;   // bf16 [max_envs][K_pad[0]] staging of the observation
+    int n_cu = 0;              // compute units of the context's device
     int64_t device_bytes = 0;
 };
 
@@ -73,6 +75,7 @@ void free_ctx(im_ctx *c)
     hipFree(c->d_log_std);
     hipFree(c->d_ws[0]);
     hipFree(c->d_ws[1]);
+    hipFree(c->d_obs16);
     delete c;
 }
 
@@ -337,6 +340,8 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
         free_ctx(c);
         return hip_fail(e, "hipGetDevice");
     }
+    if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess)
+        c->n_cu = 0;
     c->B = sk->n_bodies;
     c->D = 15 * c->B + 1;
     c->L = pol->n_layers;
@@ -453,6 +458,9 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
         const size_t wsb = (size_t)max_envs * (size_t)ws_width * esz;
         IM_TRY_ALLOC(c->d_ws[0], wsb);
         if (c->L >= 3) IM_TRY_ALLOC(c->d_ws[1], wsb);
+        // large bf16 batches stage the observation as bf16 rows for the first layer
+        if (pol->dtype == IM_DTYPE_BF16 && max_envs > SMALL_BATCH)
+            IM_TRY_ALLOC(c->d_obs16, (size_t)max_envs * (size_t)c->K_pad[0] * 2);
     }
 #undef IM_TRY_ALLOC
 #undef IM_TRY_HIP
@@ -540,6 +548,8 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
             return fail(IM_ERR_UNSUPPORTED, "policy input of layer " + std::to_string(l) +
                                                 " exceeds 4 GiB");
     }
+    if (c->d_obs16 && (uint64_t)n_envs * (uint64_t)c->K_pad[0] * 2 > 0xFFFFFFF0ull)
+        return fail(IM_ERR_UNSUPPORTED, "staged policy input exceeds 4 GiB");
     for (int l = 0; l < c->L; ++l) {
         GemmArgs g{};
         const bool last = l == c->L - 1;
@@ -553,6 +563,8 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
         g.K_pad = c->K_pad[l];
         g.K_valid = l == 0 ? c->D : c->K_pad[l];
         g.N = n_envs;
+        g.x16 = l == 0 ? c->d_obs16 : nullptr;
+        g.n_cu = c->n_cu;
         if (!last) {
             g.y = c->d_ws[l & 1];
             g.ld_y = c->M_pad[l];

@@ -9,6 +9,10 @@
 
 namespace im {
 
+// Batches up to this many envs use smaller GEMM tiles so that every layer
+// still spreads over all 256 CUs.
+constexpr int64_t SMALL_BATCH = 16384;
+
 struct GemmArgs {
     const void *x;       // layer input: obs [K][ld_x] fp32 (first layer) or [N][ld_x] of T
     int64_t ld_x;
@@ -27,6 +31,10 @@ struct GemmArgs {
     int M_blocks;        // feature blocks of the grid (set by the launcher)
     uint32_t w_bytes;    // extent of w in bytes (buffer-load bound)
     uint32_t x_bytes;    // extent of x in bytes: N * ld_x * elem, or D * ld_x * 4 for the observation
+    void *x16;           // first bf16 layer of a large batch: [N][K_pad] bf16 staging of the
+                         // observation (null: the GEMM reads the observation itself)
+    int n_cu;            // compute units of the device (persistent grids)
+    uint32_t y_bytes;    // extent of y in bytes (set by the launcher)
 };
 
 hipError_t launch_env_step(int n_slots, const EnvArgs &a, hipStream_t s);

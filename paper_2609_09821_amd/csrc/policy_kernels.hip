@@ -26,12 +26,10 @@ namespace im {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float HALF_LOG_2PI = 0.91893853320467274f;
 
-// Batches up to this many envs use smaller tiles so that every layer still
-// spreads over all 256 CUs.
-constexpr int64_t SMALL_BATCH = 16384;
 
 // Writes n_valid*A consecutive floats from LDS to dst (16-byte stores when dst
 // is 16-byte aligned).
@@ -334,7 +332,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
 
-    typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
     u32x4_t ra[A_CHUNKS];
     u32x4_t rb[IN_OBS ? 1 : B_CHUNKS];
     f32x4_t ro[IN_OBS ? B_TASKS * 8 : 1];
@@ -526,22 +523,30 @@ static hipError_t launch_bf16(GemmArgs g, int M_pad, hipStream_t s)
 }
 
 // ---------------------------------------------------------------------------
-// bf16 hidden-layer GEMM for large batches, ping-pong schedule.  Tile 256x256
-// (features x envs), K step 64, 8 waves in two groups of four.  Waves are
-// dealt to the 4 SIMDs round-robin, so every SIMD holds one wave of each
-// group.  Group g owns feature rows [128g, 128g+128) of the tile and its wave
-// w owns env columns [64w, 64w+64): 4x2 MFMA tiles of 32x32 each.  The groups
+// bf16 hidden-layer GEMM for large batches: persistent, ping-pong schedule.
+// Tile 256x256 (features x envs), K step 64, 8 waves in two groups of four.
+// Waves are dealt to the 4 SIMDs round-robin, so every SIMD holds one wave of
+// each group.  Group g owns feature rows [128g, 128g+128) of a tile and its
+// wave w env columns [64w, 64w+64): 4x2 MFMA tiles of 32x32 each.  The groups
 // alternate between two phases separated by workgroup barriers: while one
 // group runs the 32 MFMAs of a K step from fragments already in its
 // registers, the other reads its fragments of the K step from LDS (group 0
-// also issues the global->LDS loads of the next K step), so each SIMD's
-// MFMA pipe is fed by one wave while the other waits on memory.  Operands
-// move global->LDS without passing through registers (buffer loads with the
-// LDS flag, 16 bytes per lane; past the buffer end they return zero, which
-// pads the env tail).  A 128-byte LDS row holds its eight 16-byte chunks
+// also issues the global->LDS loads of the next K step), so each SIMD's MFMA
+// pipe is fed by one wave while the other waits on memory.  Operands move
+// global->LDS without passing through registers (buffer loads with the LDS
+// flag, 16 bytes per lane; past the buffer end they return zero, which pads
+// the env tail).  A 128-byte LDS row holds its eight 16-byte chunks
 // XOR-swizzled by (row/2)%8, so that fragment reads of 16 consecutive rows
-// hit distinct banks.  Two LDS stages of 64 KB; a K step's loads are issued
-// two phases before its first fragment read.
+// hit distinct banks.  Two LDS stages of 64 KB.
+//
+// One workgroup per CU walks a list of tiles, and the K steps of consecutive
+// tiles form one pipeline: the next tile's first K step is loaded while the
+// current one finishes, and each wave writes out a finished tile (bias, ReLU,
+// bf16) at the start of its next read phase, through an 8 KB LDS slot of its
+// SIMD (the SIMD's two waves use it in different phases), in 128-byte rows.
+// Tiles are ordered so that the workgroups of one XCD (workgroups are dealt
+// to the 8 XCDs round-robin) share env blocks, whose activations then come
+// from that XCD's L2.
 // ---------------------------------------------------------------------------
 #define IM_LDS_AS __attribute__((address_space(3)))
 
@@ -560,21 +565,32 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     constexpr int ROWB = BK * 2;                // bytes per LDS row
     constexpr int TILE_B = 256 * ROWB;          // one 256-row operand tile
     constexpr int STAGE_B = 2 * TILE_B;         // weight tile, then activation tile
+    constexpr int EPI_B = 64 * 64;              // epilogue slot: 64 envs x 32 features bf16
     constexpr int TM = 4, TN = 2, NS = BK / 16;
+    // separate arrays, so that the compiler sees that the global->LDS loads into
+    // the stages never write the epilogue slots or the biases
     __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE_B];
+    __shared__ __attribute__((aligned(16))) uint8_t epi_lds[4 * EPI_B];
+    __shared__ __attribute__((aligned(16))) float bias_lds[2][256];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
     const int grp = wave >> 2, wi = wave & 3;
 
+    // this workgroup's tiles: XCD x = blockIdx % 8 takes the x-th eighth of the
+    // tile order (feature block fastest), its workgroups interleaved over it
     const int mblocks = g.M_blocks;
-    const int nblk = gridDim.x;
-    int bid = blockIdx.x;
-    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
-    const int64_t m0 = (int64_t)(bid % mblocks) * 256;
-    const int64_t n0 = (int64_t)(bid / mblocks) * 256;
+    const int64_t T = ((g.N + 255) / 256) * mblocks;
+    const int per = (int)(gridDim.x >> 3);
+    const int xcd = (int)(blockIdx.x & 7), slot = (int)(blockIdx.x >> 3);
+    const int64_t r_begin = (xcd * T) / 8 + slot, r_end = ((xcd + 1) * T) / 8;
+    if (slot >= per || r_begin >= r_end) return;
+    const int n_tiles = (int)((r_end - r_begin + per - 1) / per);
     const int nk = g.K_pad / BK;
+    const int S = n_tiles * nk;
+    auto tile_m0 = [&](int ti) { return ((r_begin + (int64_t)ti * per) % mblocks) * 256; };
+    auto tile_n0 = [&](int ti) { return ((r_begin + (int64_t)ti * per) / mblocks) * 256; };
 
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.w, (short)0, (int)g.w_bytes, 0x00020000);
@@ -592,7 +608,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     // Activation row offsets stay in the per-lane offset (the part the buffer
     // range check sees), so rows past the env count read as zero; weight rows
     // are always in range.
-    auto issue = [&](int kt, int buf) {
+    auto issue = [&](int st, int buf) {
+        const int ti = st / nk, kt = st - ti * nk;
+        const int64_t m0 = tile_m0(ti), n0 = tile_n0(ti);
         uint8_t *base = lds + buf * STAGE_B + (tid & ~63) * 16;
         const uint32_t k2 = (uint32_t)(kt * BK * 2);
 #pragma unroll
@@ -605,6 +623,13 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 xr, (IM_LDS_AS void *)(base + TILE_B + c * 256 * 16), 16,
                 b_voff + (uint32_t)(((n0 + 32 * c) * g.ld_x) * 2), k2, 0, 0);
+    };
+
+    // the 256 biases of tile ti into LDS buffer ti % 2, by one wave of group 1
+    // (whose only other global memory operations are its tile stores)
+    auto stage_bias = [&](int ti) {
+        const f32x4_t v = *(const f32x4_t *)(g.bias + tile_m0(ti) + lane * 4);
+        *(f32x4_t *)(&bias_lds[ti & 1][lane * 4]) = v;
     };
 
     bf16x8_t fa[NS][TM], fb[NS][TN];
@@ -629,12 +654,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     };
 
     f32x16_t acc[TM][TN];
+    auto zero_acc = [&]() {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+            for (int j = 0; j < TN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    };
     auto mfma_step = [&]() {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
@@ -647,69 +674,165 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
         __builtin_amdgcn_s_setprio(0);
     };
 
-    // Both groups run the same loop (read K step kt; barrier; MFMAs of kt;
+    // Writes this wave's 128x64 block of tile ti (bias from LDS, ReLU, bf16) in
+    // four passes of 32 features through the 4 KB slot `ep`: [env][feature]
+    // rows of 64 bytes, 16-byte chunks XOR-swizzled by env % 4, copied out 16
+    // rows per wave instruction.  LDS operations of one wave complete in order,
+    // so the slot needs no barrier between its writes and reads.  Issues exactly
+    // 16 buffer stores (rows past the env count fall outside the buffer and are
+    // dropped, so no store is skipped).
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+        g.y, (short)0, (int)g.y_bytes, 0x00020000);
+    auto epilogue = [&](int ti, uint8_t *ep) {
+        const int64_t m0 = tile_m0(ti), n0 = tile_n0(ti);
+        const float *bias = bias_lds[ti & 1];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int nl = j * 32 + (lane & 31);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int fl = 8 * q + 4 * (lane >> 5);
+                    const float4 bb = *(const float4 *)(bias + grp * 128 + i * 32 + fl);
+                    const float v0 = fmaxf(acc[i][j][4 * q + 0] + bb.x, 0.0f);
+                    const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
+                    const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
+                    const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
+                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+                    const int chunk = q ^ (nl & 3);
+                    *(uint2 *)(ep + nl * 64 + chunk * 16 + 8 * (lane >> 5)) = make_uint2(lo, hi);
+                }
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int row = p * 16 + (lane >> 2), c = lane & 3;
+                const int64_t n = n0 + wi * 64 + row;
+                const u32x4_t v = *(const u32x4_t *)(ep + row * 64 + ((c ^ (row & 3)) * 16));
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    v, yr, (uint32_t)((n * g.ld_y + m0 + grp * 128 + i * 32 + c * 8) * 2), 0, 0);
+            }
+        }
+    };
+
+    // Both groups run the same pipeline (read K step st; barrier; MFMAs of st;
     // barrier), group 1 one phase behind group 0: it passes one extra barrier
     // first, and group 0 one extra barrier at the end so that the counts match.
+    zero_acc();
     if (grp == 0) {
         issue(0, 0);
         wait_vmcnt0();
+    } else if (wi == 0) {
+        stage_bias(0);
     }
     wg_barrier();
     if (grp == 1) wg_barrier();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
+    uint8_t *my_ep = epi_lds + (wave & 3) * EPI_B;
+    for (int st = 0; st < S; ++st) {
+        const int buf = st & 1;
+        const int kt = st % nk, ti = st / nk;
+        // group 0: loads of K step st+1 into the other buffer (last read in the two
+        // phases before this one).  Group 1, halfway through a tile: the next
+        // tile's biases (both groups wrote the previous tile in the tile's first
+        // K step, and those stores have long completed).
+        if (grp == 0) {
+            if (st + 1 < S) issue(st + 1, buf ^ 1);
+        } else if (wi == 0 && kt == nk / 2 && ti + 1 < n_tiles) {
+            stage_bias(ti + 1);
+        }
+        // a finished tile is written after those loads, so that waiting for the
+        // loads below can leave its 16 stores in flight
+        const bool flush = st > 0 && kt == 0;
+        if (flush) {
+            epilogue(ti - 1, my_ep);
+            zero_acc();
+        }
         read_frags(buf);
-        // the other buffer was last read in the two phases before this one
-        if (grp == 0 && kt + 1 < nk) issue(kt + 1, buf ^ 1);
         wg_barrier();
         mfma_step();
-        wait_vmcnt0();              // group 0: K step kt+1 has landed in LDS
+        // group 0: K step st+1 has landed in LDS.  Vector memory operations of a
+        // wave complete in issue order, so allowing the 16 later stores to be
+        // outstanding still covers every load.
+        if (grp == 0) {
+            if (flush) __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16)
+            else wait_vmcnt0();
+        }
         wg_barrier();
     }
     if (grp == 0) wg_barrier();
-
-    // Epilogue through LDS (free now): bias, ReLU, bf16; the 256x256 tile is
-    // staged env-major ([env][feature], 512-byte rows, 16-byte chunks
-    // XOR-swizzled by env % 32) and written out in whole rows, 1 KB per wave
-    // instruction, instead of 16-byte pieces of 32 rows.
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int nl = wi * 64 + j * 32 + (lane & 31);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int ml = grp * 128 + i * 32 + 8 * q + 4 * (lane >> 5);
-                const float4 bb = *(const float4 *)(g.bias + m0 + ml);
-                const float v0 = fmaxf(acc[i][j][4 * q + 0] + bb.x, 0.0f);
-                const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
-                const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
-                const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
-                const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
-                const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
-                const int chunk = (ml >> 3) ^ (nl & 31);
-                *(uint2 *)(lds + nl * 512 + chunk * 16 + 8 * (lane >> 5)) = make_uint2(lo, hi);
-            }
-        }
-    __syncthreads();
-    uint16_t *Y = (uint16_t *)g.y;
-    const int cl = tid & 31;
-#pragma unroll 4
-    for (int pass = 0; pass < 16; ++pass) {
-        const int nl = pass * 16 + (tid >> 5);
-        const int64_t n = n0 + nl;
-        if (n < g.N)
-            *(uint4 *)(Y + n * g.ld_y + m0 + cl * 8) =
-                *(const uint4 *)(lds + nl * 512 + ((cl ^ (nl & 31)) * 16));
-    }
+    // the last tile: every LDS stage is free now, one slot per wave
+    epilogue(n_tiles - 1, lds + wave * EPI_B);
 }
 
 static hipError_t launch_bf16_pp(GemmArgs g, int M_pad, hipStream_t s)
 {
     g.M_blocks = M_pad / 256;
-    const int64_t nb = (g.N + 255) / 256;
-    hipLaunchKernelGGL(gemm_bf16_pp_kernel, dim3((unsigned)(nb * g.M_blocks)), dim3(512), 0, s, g);
+    g.y_bytes = (uint32_t)((uint64_t)g.N * (uint64_t)g.ld_y * 2);
+    const int64_t tiles = ((g.N + 255) / 256) * g.M_blocks;
+    int P = g.n_cu > 0 ? (g.n_cu & ~7) : 256;
+    if (P < 8) P = 8;
+    // fewer tiles than CUs: one tile per workgroup
+    if (tiles < P) P = (int)((tiles + 7) & ~7);
+    hipLaunchKernelGGL(gemm_bf16_pp_kernel, dim3((unsigned)P), dim3(512), 0, s, g);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Observation staging for the first bf16 layer of a large batch: obs fp32
+// [D][ld] (env fastest) -> bf16 [N][K_pad] (feature fastest, zero for
+// features >= D), rounded to nearest even exactly as the GEMM's own
+// observation path rounds.  Block: 64 envs; per 64-feature chunk the block
+// reads 64 rows of 64 envs (16-byte loads along envs), transposes through LDS
+// (65-float rows: conflict-free column reads) and writes 128-byte feature
+// runs per env.  The ping-pong GEMM then streams the staged copy like any
+// hidden layer.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void stage_obs_bf16_kernel(const float *__restrict__ obs, int64_t ld,
+                                                             int D, int64_t N, int K_pad,
+                                                             uint32_t obs_bytes, uint16_t *__restrict__ x16)
+{
+    __shared__ float t[64][65];
+    const int tid = threadIdx.x;
+    const int64_t n0 = (int64_t)blockIdx.x * 64;
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)obs, (short)0, (int)obs_bytes, 0x00020000);
+    const bool vec = ((ld & 3) == 0) && ((((uintptr_t)obs) & 15) == 0);
+    for (int k0 = 0; k0 < K_pad; k0 += 64) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int idx = tid + 256 * i;
+            const int row = idx >> 4, q = idx & 15;
+            const int f = k0 + row;
+            // features >= D lie past the buffer extent and read as zero
+            const uint32_t off = (uint32_t)(((int64_t)f * ld + n0 + 4 * q) * 4);
+            f32x4_t v;
+            if (vec) {
+                v = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off + 4 * e, 0, 0));
+            }
+            if (f >= D) v = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) t[row][4 * q + e] = v[e];
+        }
+        __syncthreads();
+        const int nl = tid >> 2, r0 = (tid & 3) * 16;
+        const int64_t n = n0 + nl;
+        if (n < N) {
+            uint32_t w[8];
+#pragma unroll
+            for (int h = 0; h < 8; ++h)
+                w[h] = (uint32_t)f32_to_bf16_rne(t[r0 + 2 * h][nl]) |
+                       ((uint32_t)f32_to_bf16_rne(t[r0 + 2 * h + 1][nl]) << 16);
+            uint4 *dst = (uint4 *)(x16 + n * K_pad + k0 + r0);
+            dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+            dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+        }
+        __syncthreads();
+    }
 }
 
 template <bool IN_OBS, int BN, int WN>
@@ -787,16 +910,29 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
 {
     if (g.N <= 0) return hipSuccess;
     if (bf16) {
-        // large batches: 256x256 tiles of 8 waves (two per SIMD, so that one
-        // wave's LDS reads overlap the other's MFMAs), K step 64 -- the ping-pong
-        // kernel where the input is a bf16 hidden layer; the last layer 128 envs
-        // per block of 4 waves
+        // large batches: the ping-pong kernel (256x256 tiles of 8 waves, K step
+        // 64) on bf16 hidden inputs, and on the observation once staged as bf16
+        // [N][K_pad]; the last layer 128 envs per block of 4 waves
         if (!sample) {
             if (g.N <= SMALL_BATCH)
                 return in_obs ? launch_bf16<128, 128, 64, 2, 2, true, false>(g, M_pad, s)
                               : launch_bf16<128, 128, 64, 2, 2, false, false>(g, M_pad, s);
-            return in_obs ? launch_bf16<256, 256, 64, 2, 4, true, false>(g, M_pad, s)
-                          : launch_bf16_pp(g, M_pad, s);
+            // the ping-pong kernel needs whole 256-feature blocks and >= 2 K steps
+            const bool pp = (M_pad & 255) == 0 && (g.K_pad & 63) == 0 && g.K_pad >= 128;
+            if (!in_obs && pp) return launch_bf16_pp(g, M_pad, s);
+            if (!in_obs) return launch_bf16<256, 256, 64, 2, 4, false, false>(g, M_pad, s);
+            if (!g.x16 || !pp)
+                return launch_bf16<256, 256, 64, 2, 4, true, false>(g, M_pad, s);
+            hipLaunchKernelGGL(stage_obs_bf16_kernel, dim3((unsigned)((g.N + 63) / 64)), dim3(256), 0, s,
+                               (const float *)g.x, g.ld_x, g.K_valid, g.N, g.K_pad, g.x_bytes,
+                               (uint16_t *)g.x16);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            GemmArgs h = g;
+            h.x = g.x16;
+            h.ld_x = g.K_pad;
+            h.x_bytes = (uint32_t)((uint64_t)g.N * (uint64_t)g.K_pad * 2);
+            return launch_bf16_pp(h, M_pad, s);
         }
         return in_obs ? launch_bf16_sample<true>(g, M_pad, s) : launch_bf16_sample<false>(g, M_pad, s);
     }
