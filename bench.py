@@ -1,7 +1,7 @@
 """Throughput of the environment-plus-policy step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
-                    [--no-cpu-baseline] [--no-secondary]
+                    [--no-cpu-baseline] [--no-secondary] [--no-graph]
 
 One step = im_policy_act (MLP forward + Gaussian sampling) followed by
 im_env_step_fused (reference sampling, FK, reward, termination, masked reset,
@@ -13,7 +13,9 @@ replayed from the same initial state: the timed loop holds exactly the two
 calls per step, with every input already in device memory.
 
 Prints ONE JSON line.  `value` = n_envs * steps / timed seconds.
-`roofline` covers the policy MLP (the dominant call, MFMA-bound),
+`graph` times the same steps captured as one HIP graph and replayed (results
+checked equal to the eager run).  `roofline` covers the policy MLP (the
+dominant call, MFMA-bound),
 `roofline_env` the fused env-step kernel (HBM-bound); both use algorithmic
 work (FLOPs / bytes) over the mean duration measured with HIP events on the
 launch stream during the timed loop.  `traffic` is the HBM bytes per launch
@@ -89,7 +91,7 @@ def mlp_flops(dims, n_envs):
     return 2.0 * n_envs * sum(dims[i] * dims[i + 1] for i in range(len(dims) - 1))
 
 
-def run_gpu(wid, steps, warmup, quiet=False):
+def run_gpu(wid, steps, warmup, graph=True):
     import torch
     from paper_2609_09821_amd import binding, synth
 
@@ -114,6 +116,9 @@ def run_gpu(wid, steps, warmup, quiet=False):
         ctx.env_step_fused(bufs, with_ref_frame=False)
         resets.append((bufs.terminated | bufs.truncated).sum())
     n_reset = [int(r) for r in torch.stack(resets).cpu()]
+    # the replays write reference states of reset envs into these buffers: keep
+    # a pristine copy so that the graph replay sees the same inputs
+    pristine = [tuple(x.clone() for x in r) for r in rec] if graph else None
     for k, v in init.items():
         getattr(bufs, k).copy_(v)
     torch.cuda.synchronize()
@@ -142,6 +147,48 @@ def run_gpu(wid, steps, warmup, quiet=False):
         step(warmup + t, events[t])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    final_eager = {k: getattr(bufs, k).clone() for k in binding.EnvBuffers.ENV + ("obs",)}
+
+    # The same timed steps captured as one HIP graph (policy_act and
+    # env_step_fused per step, each step with its own recorded sim input) and
+    # replayed from the post-warmup state: the launch cost the graph removes.
+    graph_wall = None
+    if graph:
+        def restore_rec(first):
+            for t in range(first, total):
+                for dst, src in zip(rec[t], pristine[t]):
+                    dst.copy_(src)
+
+        restore_rec(0)
+        for k, v in init.items():
+            getattr(bufs, k).copy_(v)
+        for t in range(warmup):
+            step(t)
+        torch.cuda.synchronize()
+        post_warm = {k: getattr(bufs, k).clone() for k in binding.EnvBuffers.ENV + ("obs",)}
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                for t in range(steps):
+                    bufs.body_pos, bufs.body_quat, bufs.body_linvel, bufs.body_angvel = rec[warmup + t]
+                    ctx.policy_act(bufs.obs, bufs.env_n, N, mean, action, logp)
+                    ctx.env_step_fused(bufs, with_ref_frame=False)
+        torch.cuda.current_stream().wait_stream(side)
+        for rep in range(2):                  # one warm replay, one timed
+            for k, v in post_warm.items():
+                getattr(bufs, k).copy_(v)
+            restore_rec(warmup)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            g.replay()
+            torch.cuda.synchronize()
+            graph_wall = time.perf_counter() - t0
+        for k, v in final_eager.items():
+            if not torch.equal(getattr(bufs, k), v):
+                raise RuntimeError("graph replay differs from the eager run in " + k)
+        del g, pristine
     pol_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     env_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     rho = float(np.mean(n_reset[warmup:]) / N)
@@ -153,6 +200,8 @@ def run_gpu(wid, steps, warmup, quiet=False):
         desc=desc, N=N, B=B, D=D, wall=wall, pol_ms=float(pol_ms.mean()),
         env_ms=float(env_ms.mean()), rho=rho, env_bytes=float(env_bytes), flops=flops,
         prec=prec, value=N * steps / wall,
+        graph_value=None if graph_wall is None else N * steps / graph_wall,
+        graph_ms=None if graph_wall is None else graph_wall * 1e3 / steps,
     )
 
 
@@ -209,6 +258,8 @@ def main():
     ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay of the timed steps")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB mebibytes (profiler calibration "
                          "of the HBM byte counters) and exit")
@@ -232,7 +283,7 @@ def main():
         print(json.dumps({"calibration_copy_bytes": 4 * n}), flush=True)
         return
 
-    r = run_gpu(args.workload, args.steps, args.warmup)
+    r = run_gpu(args.workload, args.steps, args.warmup, graph=not args.no_graph)
     desc = r["desc"]
     spec = desc["spec"]
     mlp_tflops = r["flops"] / (r["pol_ms"] * 1e-3) / 1e12
@@ -263,6 +314,10 @@ def main():
             "reset_fraction_per_step": r["rho"],
             "parallelism": "single GPU",
         },
+        "graph": None if r["graph_value"] is None else {
+            "value": r["graph_value"], "ms_per_step": r["graph_ms"],
+            "note": "same timed steps captured as one HIP graph and replayed; results "
+                    "checked equal to the eager run"},
         "roofline": {
             "kernel": "policy MLP (im_policy_act: one MFMA GEMM per layer)",
             "bound": "mfma", "achieved": mlp_tflops, "peak": peak, "unit": "TFLOP/s",
@@ -281,11 +336,12 @@ def main():
         },
     }
     if not args.no_secondary and args.workload != 2:
-        s = run_gpu(2, args.steps, args.warmup)
+        s = run_gpu(2, args.steps, args.warmup, graph=not args.no_graph)
         out["also"] = [{
             "workload": s["desc"]["spec"]["name"], "n_envs": s["N"], "value": s["value"],
             "ms_per_step": s["wall"] * 1e3 / args.steps, "policy_ms": s["pol_ms"],
-            "env_step_ms": s["env_ms"]}]
+            "env_step_ms": s["env_ms"], "graph_value": s["graph_value"],
+            "graph_ms_per_step": s["graph_ms"]}]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload)
     print(json.dumps(out), flush=True)
