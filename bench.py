@@ -51,12 +51,13 @@ CSRC = os.path.join(ROOT, "paper_2609_09821_amd", "csrc")
 SHARED_SOURCES = [os.path.join(CSRC, f) for f in ("api.hip", "device_math.h", "launch.h", "tables.h")] + [
     os.path.join(ROOT, "include", "instantmimic.h")]
 TRAFFIC_KIB = {
-    # policy: one entry per GEMM launch of im_policy_act, in layer order
-    "policy": {"sources": ["policy_kernels.hip"], "sha": "30cc4525d5e561c4", "workloads": {
-        4: {"fetch": [58722.5, 98518.5, 73894.5, 33704.1],
-            "write": [132735.5, 140023.7, 66342.7, 47292.1]}}},
-    "env": {"sources": ["env_kernels.hip"], "sha": "64bddbfd24ce0b36", "workloads": {
-        4: {"fetch": [61771.5], "write": [169502.4]}}},
+    # policy: one entry per launch of im_policy_act, in order (observation
+    # staging, the four layers)
+    "policy": {"sources": ["policy_kernels.hip"], "sha": "4fe3c7f06e8b30ab", "workloads": {
+        4: {"fetch": [46220.7, 36498.4, 98970.0, 74236.7, 33543.5],
+            "write": [49152.1, 134546.3, 133763.8, 67931.2, 35584.0]}}},
+    "env": {"sources": ["env_kernels.hip"], "sha": "08b97772c0998dda", "workloads": {
+        4: {"fetch": [61772.2], "write": [169502.4]}}},
 }
 
 
