@@ -23,6 +23,7 @@ using namespace im;
 struct im_ctx {
     int device = -1;
     int B = 0, D = 0, A = 0, n_clips = 0, L = 0, dtype = 0, n_slots = 0, max_depth = 0;
+    int half_slots = 0;   // parked-frame slots of the fused step's half walks
     int64_t max_envs = 0;
     im_config cfg{};
     SkelTab *d_skel = nullptr;
@@ -155,6 +156,95 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
             t->axis[i][c] = sk->axis[3 * b + c];
         }
         t->massw[i] = (float)((double)sk->mass[b] / msum);
+    }
+
+    // Two half walks for the fused step.  Half 1 owns the subtrees of a set S
+    // of children of one branch point v, half 0 everything else (root
+    // included); each walks its bodies plus their ancestors.  Walk lengths:
+    // B - |H1| and |H1| + depth(v) + 1; (v, S) minimises the longer one, then
+    // their sum.
+    std::vector<int> size(B, 1);
+    for (int b = B - 1; b > 0; --b) size[sk->parent[b]] += size[b];
+    int best_v = -1, best_mask = 0, best_max = B + 1, best_sum = 2 * B + 2;
+    for (int v = 0; v < B; ++v) {
+        const int nc = (int)ch[v].size();
+        if (nc < 2 || nc > 16) continue;
+        for (int mask = 1; mask < (1 << nc) - 1; ++mask) {
+            int h1 = 0;
+            for (int c = 0; c < nc; ++c)
+                if (mask >> c & 1) h1 += size[ch[v][c]];
+            const int c0 = B - h1, c1 = h1 + depth[v] + 1;
+            const int mx = std::max(c0, c1), sm = c0 + c1;
+            if (mx < best_max || (mx == best_max && sm < best_sum)) {
+                best_v = v;
+                best_mask = mask;
+                best_max = mx;
+                best_sum = sm;
+            }
+        }
+    }
+    std::vector<int> owner(B, 0);
+    if (best_v >= 0) {
+        std::vector<int> stk;
+        for (int c = 0; c < (int)ch[best_v].size(); ++c)
+            if (best_mask >> c & 1) stk.push_back(ch[best_v][c]);
+        while (!stk.empty()) {
+            const int b = stk.back();
+            stk.pop_back();
+            owner[b] = 1;
+            for (int cc : ch[b]) stk.push_back(cc);
+        }
+    }
+    std::vector<int> pos_of(B, 0);
+    for (int i = 0; i < B; ++i) pos_of[order[i]] = i;
+    t->half_slots = 0;
+    for (int h = 0; h < 2; ++h) {
+        // walk set: owned bodies and their ancestors (closed under parent)
+        std::vector<int> in(B, 0);
+        for (int b = 0; b < B; ++b)
+            if (owner[b] == h)
+                for (int x = b; x >= 0 && !in[x]; x = x > 0 ? sk->parent[x] : -1) in[x] = 1;
+        in[0] = 1;
+        std::vector<std::vector<int>> chw(B);
+        for (int b = 1; b < B; ++b)
+            if (in[b]) chw[sk->parent[b]].push_back(b);
+        std::vector<int> nestw(B, 0), slotw(B, -1), ordw;
+        for (int i = 0; i < B; ++i) {            // full preorder restricted to the walk set
+            const int b = order[i];
+            if (!in[b]) continue;
+            ordw.push_back(b);
+            if (b > 0) {
+                const int p = sk->parent[b];
+                nestw[b] = nestw[p] + (chw[p].size() >= 2 ? 1 : 0);
+            }
+        }
+        int ns = 0;
+        for (int b : ordw)
+            if (chw[b].size() >= 2) {
+                slotw[b] = nestw[b];
+                ns = std::max(ns, nestw[b] + 1);
+            }
+        t->half_slots = std::max(t->half_slots, ns);
+        auto &w = t->half[h];
+        w.n = (int)ordw.size();
+        for (int i = 0; i < w.n; ++i) {
+            const int b = ordw[i];
+            w.body[i] = b;
+            w.rec[i] = pos_of[b];
+            w.own[i] = owner[b] == h ? 1 : 0;
+            w.bslot[i] = slotw[b];
+            w.pslot[i] = -1;
+            if (i > 0 && sk->parent[b] != ordw[i - 1]) {
+                const int p = sk->parent[b];
+                if (slotw[p] < 0) return "internal: half-walk parent is not a branch point";
+                w.pslot[i] = slotw[p];
+            }
+            w.jtype[i] = sk->jtype[b];
+            w.leaf[i] = ch[b].empty() ? 1 : 0;
+            for (int c = 0; c < 3; ++c) w.offset[i][c] = sk->offset[3 * b + c];
+            w.offset[i][3] = 0.0f;
+            w.massw[i] = (float)((double)sk->mass[b] / msum);
+        }
     }
     return "";
 }
@@ -330,7 +420,7 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     int max_depth = 0;
     msg = build_skeleton(sk, &tab, &max_depth);
     if (!msg.empty()) return fail(IM_ERR_INVALID_ARG, msg);
-    if (tab.n_slots > IM_MAX_BRANCH_NESTING)
+    if (tab.n_slots > IM_MAX_BRANCH_NESTING || tab.half_slots > IM_MAX_BRANCH_NESTING)
         return fail(IM_ERR_UNSUPPORTED, "branch points nested deeper than " +
                                             std::to_string(IM_MAX_BRANCH_NESTING));
 
@@ -349,6 +439,7 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     c->n_clips = n_clips;
     c->dtype = pol->dtype;
     c->n_slots = tab.n_slots;
+    c->half_slots = tab.half_slots;
     c->max_depth = max_depth;
     c->max_envs = max_envs;
     c->cfg = *cfg;
@@ -497,7 +588,7 @@ im_status im_env_step_fused(im_ctx *c, const im_env_bufs *b, void *stream)
     if (s != IM_OK) return s;
     if ((s = check_device(c)) != IM_OK) return s;
     const EnvArgs a = env_args(c, b);
-    hipError_t e = launch_env_step(c->n_slots, a, (hipStream_t)stream);
+    hipError_t e = launch_env_step(c->n_slots, c->half_slots, a, (hipStream_t)stream);
     return e == hipSuccess ? IM_OK : hip_fail(e, "env_step launch");
 }
 

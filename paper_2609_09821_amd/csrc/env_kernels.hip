@@ -7,10 +7,11 @@
 // cache-resident table (one contiguous record per segment, read
 // sequentially in preorder).
 //
-// Forward kinematics walks the bodies in depth-first preorder, so the
-// frames that can still have children are exactly those on the current
-// root-to-body path; they live in registers, one slot per depth, selected by
-// a wave-uniform switch.
+// Forward kinematics walks the bodies in depth-first preorder: a body's
+// parent is the previous body, or a branch point whose frame was parked in
+// LDS.  The fused step runs every env on two threads (the same lane of two
+// wavefronts), each walking the bodies of one half of the skeleton plus their
+// ancestors; the two partial error sums are combined through LDS.
 //
 // Reference positions are kept relative to an anchor (the clip root
 // position at frame i0) and the simulator positions are differenced against
@@ -328,6 +329,234 @@ struct SimPV {
     f3 P, V;
 };
 
+using HalfWalk = SkelTab::HalfWalk;
+
+// Forward kinematics over one half walk (root first, preorder), with the same
+// depth-2 prefetch as walk_prefetch; load(body) is called for owned bodies
+// only, and visit(i, body, own, frame, anchor, data) for every position.
+template <class D, class Load, class Visit>
+__device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const float4 *rec,
+                                          float alpha, Load &&load, Visit &&visit)
+{
+    const LdsStack<13> st{im_lds + threadIdx.x, (int)blockDim.x};
+    float buf[13];
+    const int n = w->n;
+    const float4 *jr = rec + 6;
+    D d0 = w->own[0] ? load(0) : D{};
+    D d1{}, d2{};
+    float4 a1{}, u1{}, w1{}, a2{}, u2{}, w2{};
+    if (n > 1) {
+        d1 = w->own[1] ? load(w->body[1]) : D{};
+        const float4 *p = jr + 3 * (w->rec[1] - 1);
+        a1 = p[0];
+        u1 = p[1];
+        w1 = p[2];
+    }
+    if (n > 2) {
+        d2 = w->own[2] ? load(w->body[2]) : D{};
+        const float4 *p = jr + 3 * (w->rec[2] - 1);
+        a2 = p[0];
+        u2 = p[1];
+        w2 = p[2];
+    }
+    f3 A;
+    Frame cur = root_frame(rec, alpha, &A);
+    visit(0, 0, w->own[0], cur, A, d0);
+    if (w->bslot[0] >= 0) {
+        pack_frame(cur, buf);
+        st.put(w->bslot[0], buf);
+    }
+    for (int i = 1; i < n; ++i) {
+        const D d = d1;
+        const float4 ra = a1, ru = u1, rw = w1;
+        d1 = d2;
+        a1 = a2;
+        u1 = u2;
+        w1 = w2;
+        if (i + 2 < n) {
+            d2 = w->own[i + 2] ? load(w->body[i + 2]) : D{};
+            const float4 *p = jr + 3 * (w->rec[i + 2] - 1);
+            a2 = p[0];
+            u2 = p[1];
+            w2 = p[2];
+        }
+        if (w->pslot[i] >= 0) {
+            st.get(w->pslot[i], buf);
+            cur = unpack_frame(buf);
+        }
+        const f3 off = mk3(w->offset[i][0], w->offset[i][1], w->offset[i][2]);
+        Frame c;
+        const f3 r = qrot(cur.Q, off);
+        c.P = cur.P + r;
+        c.V = cur.V + cross3(cur.W, r);
+        if (w->jtype[i] == IM_JOINT_FIXED) {
+            c.Q = cur.Q;
+            c.W = cur.W;
+        } else {
+            c.Q = qmul(cur.Q, slerp_basis(ra, ru, alpha * rw.w));
+            c.W = cur.W + qrot(cur.Q, mk3(rw.x, rw.y, rw.z));
+        }
+        cur = c;
+        visit(i, w->body[i], w->own[i], cur, A, d);
+        if (w->bslot[i] >= 0) {
+            pack_frame(cur, buf);
+            st.put(w->bslot[i], buf);
+        }
+    }
+}
+
+// Observation rows of the bodies a half owns, from the sim state (env not reset).
+__device__ __forceinline__ void obs_half_from_sim(const EnvArgs &a, const HalfWalk *__restrict__ w,
+                                                  int64_t e)
+{
+    const int64_t ld = a.ld;
+    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
+    const int n = w->n;
+#pragma unroll 4
+    for (int i = 0; i < n; ++i) {
+        if (!w->own[i]) continue;
+        const int b = w->body[i];
+        write_obs_body(a.obs, ld, e, b, h, ld3(a.pos, b, ld, e), ld4(a.quat, b, ld, e),
+                       ld3(a.linvel, b, ld, e), ld3(a.angvel, b, ld, e));
+    }
+}
+
+// Reference state initialisation of the bodies a half owns at (clip k, phase
+// ph), and their observation rows from the same fp32 values the sim state
+// receives (the heading from the root, which both halves walk first).
+__device__ __forceinline__ void rsi_obs_half(const EnvArgs &a, const HalfWalk *__restrict__ w,
+                                             int64_t e, int k, float ph)
+{
+    const ClipTab ci = a.clips[k];
+    int j0;
+    float al;
+    phase_index(ph, ci, &j0, &al);
+    const float4 *rec = a.seg + ci.seg_base + (int64_t)j0 * seg_stride(a.sk->B);
+    const int64_t ld = a.ld;
+    Heading h{};
+    walk_half<NoData>(w, rec, al, [](int) { return NoData{}; },
+                      [&](int i, int b, int own, const Frame &f, f3 A, const NoData &) {
+        const f3 P = A + f.P;
+        if (i == 0) h = heading_of(f.Q, P);
+        if (!own) return;
+        st3(a.pos, b, ld, e, P);
+        st4(a.quat, b, ld, e, f.Q);
+        st3(a.linvel, b, ld, e, f.V);
+        st3(a.angvel, b, ld, e, f.W);
+        write_obs_body(a.obs, ld, e, b, h, P, f.Q, f.V, f.W);
+    });
+}
+
+// The fused step for small batches: env e runs on two wavefronts of its
+// block, lane l of wave 2p and of wave 2p+1, the first walking
+// SkelTab::half[0] and the second half[1] (the half is wave-uniform, so its
+// tables are read with scalar loads); 64 envs per wave pair, 128 per block.
+// The partial error sums meet in LDS.  Twice the wavefronts of the one-thread
+// kernel for the same envs: below a few waves per SIMD that hides more of the
+// walks' latency, above it the duplicated root and ancestor work costs more.
+__global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
+{
+    __shared__ float part[6][256];
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int hf = wave & 1;
+    const int64_t e = (int64_t)blockIdx.x * 128 + (wave >> 1) * 64 + (tid & 63);
+    const bool active = e < a.n;      // the same for both threads of an env
+    const int64_t ld = a.ld;
+    const SkelTab *__restrict__ sk = a.sk;
+    const HalfWalk *__restrict__ hw = &sk->half[hf];
+
+    // 1. discrete state advance (fp32, exact contract), in both lanes
+    int k = 0, t1 = 0, i0 = 0;
+    uint32_t n1 = 0;
+    float phi1 = 0.0f, alpha = 0.0f;
+    bool trunc = false;
+    // 2.-3. reference FK and this half's error sums against the sim state
+    float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
+    f3 dc = mk3(0.0f, 0.0f, 0.0f);
+    if (active) {
+        k = safe_clip(a.env_clip[e], a.n_clips);
+        const float phi = a.env_phase[e];
+        t1 = a.env_t[e] + 1;
+        n1 = a.env_n[e] + 1u;
+        const ClipTab ci = a.clips[k];
+        {
+#pragma clang fp contract(off)
+            phi1 = phi + ci.dphi;
+        }
+        trunc = phi1 >= 1.0f;
+        phase_index(phi1 < 1.0f ? phi1 : 1.0f, ci, &i0, &alpha);
+        const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
+        auto load_pv = [&](int b) {
+            SimPV s;
+            s.P = ld3(a.pos, b, ld, e);
+            s.V = ld3(a.linvel, b, ld, e);
+            return s;
+        };
+        walk_half<SimPV>(hw, rec, alpha, load_pv,
+                         [&](int i, int, int own, const Frame &f, f3 A, const SimPV &sb) {
+            if (!own) return;
+            const f3 dp = (sb.P - A) - f.P;
+            const f3 dv = sb.V - f.V;
+            const float x = dot3(dp, dp);
+            e_pos += x;
+            if (hw->leaf[i]) e_ee += x;
+            dc = dc + hw->massw[i] * dp;
+            e_vel += dot3(dv, dv);
+        });
+    }
+    // both halves' sums (a + b in one thread, b + a in the other: the same bits)
+    part[0][tid] = e_pos;
+    part[1][tid] = e_ee;
+    part[2][tid] = e_vel;
+    part[3][tid] = dc.x;
+    part[4][tid] = dc.y;
+    part[5][tid] = dc.z;
+    __syncthreads();
+    const int o = tid ^ 64;
+    e_pos += part[0][o];
+    e_ee += part[1][o];
+    e_vel += part[2][o];
+    dc.x += part[3][o];
+    dc.y += part[4][o];
+    dc.z += part[5][o];
+    if (!active) return;
+
+    const float e_com = dot3(dc, dc);
+    const float r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
+                    a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
+    const float z_root = a.pos[2 * ld + e];
+    const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
+
+    // 4. masked reset (the same draw in both lanes)
+    int k_out = k, t_out = t1;
+    float ph_out = phi1;
+    const bool done = term || trunc;
+    if (done) {
+        const uint4 x = philox4x32_10(make_uint4((uint32_t)e, n1, 0u, 1u), (uint32_t)a.seed,
+                                      (uint32_t)(a.seed >> 32));
+        k_out = (int)(((uint64_t)x.x * (uint64_t)(uint32_t)a.n_clips) >> 32);
+        ph_out = (float)(x.y >> 8) * 0x1p-24f;
+        t_out = 0;
+    }
+    if (hf == 0) {
+        a.env_clip[e] = k_out;
+        a.env_phase[e] = ph_out;
+        a.env_t[e] = t_out;
+        a.env_n[e] = n1;
+        a.reward[e] = r;
+        a.term[e] = (uint8_t)term;
+        a.trunc[e] = (uint8_t)trunc;
+        if (a.ref_frame) a.ref_frame[e] = i0;
+        a.obs[(int64_t)(15 * sk->B) * ld + e] = ph_out;
+    }
+    // 5. observation of the post-reset state: a reset env's rows come from the
+    //    reference state written in the same walk, others from the sim state
+    if (done) rsi_obs_half(a, hw, e, k_out, ph_out);
+    else obs_half_from_sim(a, hw, e);
+}
+
+// The fused step, one thread per env (large batches).
 __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
 {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -676,9 +905,15 @@ static hipError_t launch_env(void (*k)(EnvArgs), int n_slots, int frame_floats,
     return hipGetLastError();
 }
 
-hipError_t launch_env_step(int n_slots, const EnvArgs &a, hipStream_t s)
+hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s)
 {
-    return launch_env(env_step_kernel, n_slots, 13, a, s);
+    if (a.n <= 0) return hipSuccess;
+    if (a.n > SPLIT_ENV_MAX) return launch_env(env_step_kernel, n_slots, 13, a, s);
+    // two threads per env: 128 envs per 256-thread block
+    const int bs = 256;
+    const size_t lds = (size_t)(half_slots > 0 ? half_slots : 1) * 13 * sizeof(float) * bs;
+    hipLaunchKernelGGL(env_step_split_kernel, dim3((unsigned)((a.n + 127) / 128)), dim3(bs), lds, s, a);
+    return hipGetLastError();
 }
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s)
 {

@@ -12,6 +12,8 @@ namespace im {
 // Batches up to this many envs use smaller GEMM tiles so that every layer
 // still spreads over all 256 CUs.
 constexpr int64_t SMALL_BATCH = 16384;
+// Batches up to this many envs run the fused step on two threads per env.
+constexpr int64_t SPLIT_ENV_MAX = 32768;
 
 struct GemmArgs {
     const void *x;       // layer input: obs [K][ld_x] fp32 (first layer) or [N][ld_x] of T
@@ -37,7 +39,7 @@ struct GemmArgs {
     uint32_t y_bytes;    // extent of y in bytes (set by the launcher)
 };
 
-hipError_t launch_env_step(int n_slots, const EnvArgs &a, hipStream_t s);
+hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_standin(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_pack_segments(const SkelTab *sk, int F, double fps, const float *root_pos,

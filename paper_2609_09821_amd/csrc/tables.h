@@ -26,6 +26,22 @@ struct SkelTab {
     float offset[IM_MAX_BODIES][4];
     float axis[IM_MAX_BODIES][4];
     float massw[IM_MAX_BODIES];    // m_b / sum m
+    // The fused step splits every env over two threads: half h walks the
+    // bodies it owns and their ancestors (see HalfWalk).
+    int32_t half_slots;            // parked-frame slots needed by either half walk
+    struct HalfWalk {
+        int32_t n;                     // positions of the walk (root first, preorder)
+        int32_t body[IM_MAX_BODIES];   // body at position i
+        int32_t rec[IM_MAX_BODIES];    // its position in the full preorder (segment record)
+        int32_t own[IM_MAX_BODIES];    // 1: errors, reset and observation of this body
+                                       // belong to this half; 0: an ancestor passed through
+        int32_t bslot[IM_MAX_BODIES];  // as above, for the walk's own branch points
+        int32_t pslot[IM_MAX_BODIES];
+        int32_t jtype[IM_MAX_BODIES];
+        int32_t leaf[IM_MAX_BODIES];   // leaf of the whole skeleton (end effector)
+        float offset[IM_MAX_BODIES][4];
+        float massw[IM_MAX_BODIES];
+    } half[2];
 };
 
 // Per clip.  seg_base: float4 index of segment 0 in the segment table.

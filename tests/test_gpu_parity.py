@@ -119,3 +119,28 @@ def test_policy_parity(cfg):
     zg = (act.cpu().numpy() - mean.cpu().numpy()) / sig
     zo = (oa.astype(np.float64) - om) / sig
     assert np.abs(zg - zo).max() < 1e-3
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_env_step_parity_large_batch_kernel(cfg):
+    # above 32768 envs the fused step runs one thread per env (below, two);
+    # a ragged size so that its last block is partly empty
+    N, T = 40037, 2
+    d, w, ctx, bufs = _setup(cfg, N)
+    c = d["config"]
+    st = oracle.State(w.B, N)
+    w.reset_envs(st)
+    H.upload_state(st, bufs)
+    ctx.reset_envs(bufs)
+    live = np.ones(N, bool)
+    for t in range(T):
+        w.standin(st, d["sigma_joint"], d["sigma_vel"])
+        H.upload_state(st, bufs, env=False)
+        t_next = st.t + 1
+        z_root = st.pos[0, 2].copy()
+        ctx.env_step_fused(bufs)
+        w.env_step(st)
+        g = H.download(bufs, N)
+        live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, live)
+        H.compare_sim_obs(g, st, live, "step %d" % t)
+    assert live.mean() > 0.999
