@@ -74,7 +74,12 @@ def lib():
                                 C.POINTER(C.c_int), C.POINTER(C.c_float)]
     L.or_env_step.argtypes = [
         C.c_void_p, C.c_int64, _i64p_opt, C.c_int64, _i32p, _f32p, _i32p, _u32p,
-        _f32p, _f32p, _f32p, _f32p, C.c_int64, _f32p, _u8p, _u8p, _f32p, C.c_int64, _i32p_opt]
+        _f32p, _f32p, _f32p, _f32p, C.c_int64, _f32p, _u8p, _u8p, _f32p, C.c_int64, _i32p_opt,
+        _f32p_opt]
+    L.or_world_set_training.argtypes = [C.c_void_p, C.c_int, _f32p, C.c_int, C.c_int, C.c_int]
+    L.or_obs_dim.argtypes = [C.c_void_p]
+    L.or_obs_dim.restype = C.c_int
+    L.or_mreward.argtypes = [C.c_void_p, _f64p, _f64p, _f64p, C.c_int, C.c_float, _f64p]
     L.or_reset_envs.argtypes = [
         C.c_void_p, C.c_int64, _u8p_opt, _i32p, _f32p, _i32p, _u32p, _f32p, _f32p, _f32p, _f32p,
         C.c_int64, _f32p, C.c_int64]
@@ -183,6 +188,13 @@ class World:
             float(cfg["r_min"]), int(cfg["grace"]), weights, self.seed)
         if not self.ptr:
             raise ValueError("oracle rejected the world description")
+        self.A = int(desc["policy"]["dims"][-1])
+        mw = k([cfg.get("m_jrot", 0.0), cfg.get("m_jvel", 0.0), cfg.get("m_com", 0.0),
+                cfg.get("m_eepos", 0.0), cfg.get("m_eerot", 0.0)], np.float32)
+        lib().or_world_set_training(self.ptr, int(cfg.get("reward_form", 0)), mw,
+                                    int(cfg.get("obs_future", 0)),
+                                    int(cfg.get("obs_prev_action", 0)), self.A)
+        self.D = int(lib().or_obs_dim(self.ptr))
 
     def __del__(self):
         if getattr(self, "ptr", None):
@@ -213,6 +225,17 @@ class World:
         lib().or_reward(self.ptr, f(P), f(V), f(Pr), f(Vr), out)
         return dict(e_pos=out[0], e_vel=out[1], e_ee=out[2], e_com=out[3], r=out[4])
 
+    def mreward(self, P, Q, W, k, phi_ev):
+        """Multiplicative reward terms of a sim state against clip k at phi_ev."""
+        out = np.zeros(6)
+        f = lambda a: np.ascontiguousarray(a, np.float64).reshape(-1)
+        lib().or_mreward(self.ptr, f(P), f(Q), f(W), int(k), float(np.float32(phi_ev)), out)
+        return dict(e_jrot=out[0], e_jvel=out[1], e_com=out[2], e_eepos=out[3], e_eerot=out[4],
+                    r=out[5])
+
+    def state(self, N):
+        return State(self.B, N, self.D)
+
     def terminated(self, t_next, z_root, r_out):
         return bool(lib().or_terminated(self.ptr, int(t_next), float(np.float32(z_root)),
                                         float(np.float32(r_out))))
@@ -230,14 +253,21 @@ class World:
         return kk.value, np.float32(ph.value)
 
     # -- batch operations on State objects (numpy SoA buffers)
-    def env_step(self, st, idx=None):
+    def env_step(self, st, idx=None, prev_action=None):
+        """prev_action: [N][A] float32, the actions applied in this step (needed when the
+        observation holds the previous action)."""
         idx_a = None if idx is None else np.ascontiguousarray(idx, np.int64)
+        pa = None if prev_action is None else np.ascontiguousarray(prev_action, np.float32)
+        if pa is not None:
+            assert pa.shape == (st.N, self.A)
+        assert st.obs.shape[0] == self.D
         lib().or_env_step(self.ptr, st.N, idx_a, 0 if idx_a is None else len(idx_a),
                           st.clip, st.phase, st.t, st.n, st.pos, st.quat, st.linvel, st.angvel,
                           st.ld, st.reward, st.terminated, st.truncated, st.obs, st.ld,
-                          st.ref_frame)
+                          st.ref_frame, pa)
 
     def reset_envs(self, st, mask=None):
+        assert st.obs.shape[0] == self.D
         m = None if mask is None else np.ascontiguousarray(mask, np.uint8)
         lib().or_reset_envs(self.ptr, st.N, m, st.clip, st.phase, st.t, st.n, st.pos, st.quat,
                             st.linvel, st.angvel, st.ld, st.obs, st.ld)
@@ -252,9 +282,9 @@ class World:
 class State:
     """Host SoA buffers in the library's layout (ld = N)."""
 
-    def __init__(self, B, N):
+    def __init__(self, B, N, D=None):
         self.B, self.N, self.ld = B, N, N
-        D = 15 * B + 1
+        D = 15 * B + 1 if D is None else D
         self.clip = np.zeros(N, np.int32)
         self.phase = np.zeros(N, np.float32)
         self.t = np.zeros(N, np.int32)

@@ -295,6 +295,15 @@ typedef struct {
     int grace;
     double c_pose, w_pos, w_ee, c_vel, w_vel, c_com, w_com;
     uint64_t seed;
+    /* training terms (or_world_set_training) */
+    int reward_form;            /* 0: grouped additive reward, 1: multiplicative */
+    double m_w[5];              /* multiplicative weights: joint rotation, joint
+                                   velocity, COM, EE position, EE orientation */
+    int obs_future;             /* future reference frames in the observation */
+    int obs_prev_action;        /* previous action in the observation */
+    int A;                      /* action width */
+    int n_ee;
+    int ee[OR_MAX_BODIES];      /* end effectors (leaves) in body order */
 } or_world;
 
 /*
@@ -362,7 +371,36 @@ or_world *or_world_create(int B, const int *parent, const int *jtype, const floa
     w->c_com = weights[5];
     w->w_com = weights[6];
     w->seed = seed;
+    w->reward_form = 0;
+    w->n_ee = 0;
+    for (int b = 0; b < B; ++b)
+        if (w->is_leaf[b]) w->ee[w->n_ee++] = b;
     return w;
+}
+
+/*
+ * Training terms [Sec. 6.1, and the reward weights, termination and grace
+ * settings of the backflip search's configuration table]:
+ *   reward_form 1: r = prod_k exp(-m_k e_k) over joint rotation, joint
+ *   velocity, COM, end-effector position and end-effector orientation errors;
+ *   obs_future K: the reference root and end-effector frames of the next K
+ *   control steps; obs_prev_action: the action applied in this step.
+ */
+void or_world_set_training(or_world *w, int reward_form, const float *mw, int obs_future,
+                           int obs_prev_action, int A)
+{
+    w->reward_form = reward_form;
+    for (int i = 0; i < 5; ++i) w->m_w[i] = mw[i];
+    w->obs_future = obs_future;
+    w->obs_prev_action = obs_prev_action;
+    w->A = A;
+}
+
+/* Observation width: 15 per body, the phase, 9 per future frame of the root
+ * and each end effector, and the previous action. */
+int or_obs_dim(const or_world *w)
+{
+    return 15 * w->B + 1 + w->obs_future * (1 + w->n_ee) * 9 + (w->obs_prev_action ? w->A : 0);
 }
 
 void or_world_destroy(or_world *w)
@@ -578,6 +616,93 @@ void or_reward(const or_world *w, const double *P, const double *V, const double
     out[0] = r.e_pos; out[1] = r.e_vel; out[2] = r.e_ee; out[3] = r.e_com; out[4] = r.r;
 }
 
+/* Rotation angle in [0, pi] of a unit quaternion (either sign). */
+static double qangle(quat q)
+{
+    double v = sqrt(q.x * q.x + q.y * q.y + q.z * q.z);
+    return 2.0 * atan2(v, fabs(q.w));
+}
+
+typedef struct { double e_jrot, e_jvel, e_com, e_eepos, e_eerot, r; } or_mreward_t;
+
+/*
+ * Multiplicative imitation reward [Sec. 6.1]: r = prod_k exp(-m_k e_k) with
+ *   e_jrot  = sum_b angle(qr_b^-1 q_b)^2, q_b the joint rotation (parent frame;
+ *             the root's world orientation for b = 0), qr_b the reference's;
+ *   e_jvel  = sum_b |w_b - wr_b|^2, w_b the joint angular velocity in the parent
+ *             frame, R(Q_p)^T (W_b - W_p) (the root's world angular velocity);
+ *   e_com   = |c - cr|^2 (point masses at body origins);
+ *   e_eepos = sum_e |P_e - Pr_e|^2 over end effectors;
+ *   e_eerot = sum_e angle(Qr_e^-1 Q_e)^2 (world orientations).
+ */
+static or_mreward_t mreward_of(const or_world *w, const vec3 *P, const quat *Q, const vec3 *W,
+                               const or_local *L, const or_state *Sr)
+{
+    or_mreward_t out = {0, 0, 0, 0, 0, 0};
+    vec3 c = v3(0, 0, 0), cr = v3(0, 0, 0);
+    for (int b = 0; b < w->B; ++b) {
+        quat ql, qr;
+        vec3 wl, wr;
+        if (b == 0) {
+            ql = Q[0];
+            qr = L->root_q;
+            wl = W[0];
+            wr = L->root_w;
+        } else {
+            int p = w->parent[b];
+            ql = qmul(qconj(Q[p]), Q[b]);
+            qr = L->q[b];
+            wl = qrot(qconj(Q[p]), vsub(W[b], W[p]));
+            wr = L->wrel[b];
+        }
+        double th = qangle(qmul(qconj(qr), ql));
+        out.e_jrot += th * th;
+        vec3 dw = vsub(wl, wr);
+        out.e_jvel += vdot(dw, dw);
+        c = vadd(c, vscale(P[b], w->mass[b]));
+        cr = vadd(cr, vscale(Sr->P[b], w->mass[b]));
+        if (w->is_leaf[b]) {
+            vec3 dp = vsub(P[b], Sr->P[b]);
+            out.e_eepos += vdot(dp, dp);
+            double te = qangle(qmul(qconj(Sr->Q[b]), Q[b]));
+            out.e_eerot += te * te;
+        }
+    }
+    c = vscale(c, 1.0 / w->total_mass);
+    cr = vscale(cr, 1.0 / w->total_mass);
+    vec3 dc = vsub(c, cr);
+    out.e_com = vdot(dc, dc);
+    out.r = exp(-w->m_w[0] * out.e_jrot) * exp(-w->m_w[1] * out.e_jvel) *
+            exp(-w->m_w[2] * out.e_com) * exp(-w->m_w[3] * out.e_eepos) *
+            exp(-w->m_w[4] * out.e_eerot);
+    return out;
+}
+
+/* Exported for pins: the sim state as doubles ([B][3], [B][4], ...) against the
+ * reference of clip k at phase phi_ev; out = e_jrot, e_jvel, e_com, e_eepos,
+ * e_eerot, r. */
+void or_mreward(const or_world *w, const double *P, const double *Q, const double *W, int k,
+                float phi_ev, double *out)
+{
+    vec3 a[OR_MAX_BODIES], c[OR_MAX_BODIES];
+    quat q[OR_MAX_BODIES];
+    for (int b = 0; b < w->B; ++b) {
+        a[b] = v3(P[3 * b], P[3 * b + 1], P[3 * b + 2]);
+        q[b] = qmake(Q[4 * b], Q[4 * b + 1], Q[4 * b + 2], Q[4 * b + 3]);
+        c[b] = v3(W[3 * b], W[3 * b + 1], W[3 * b + 2]);
+    }
+    int i0;
+    float alpha;
+    or_phase_index(w->clips[k].F, phi_ev, &i0, &alpha);
+    or_local L;
+    ref_local(w, k, i0, (double)alpha, &L);
+    or_state Sr;
+    fk(w, &L, &Sr);
+    or_mreward_t r = mreward_of(w, a, q, c, &L, &Sr);
+    out[0] = r.e_jrot; out[1] = r.e_jvel; out[2] = r.e_com; out[3] = r.e_eepos;
+    out[4] = r.e_eerot; out[5] = r.r;
+}
+
 /*
  * Termination [Fig. 5, strict "<"]: after the grace steps, an env
  * terminates when the root is below h_term or the fp32 reward is not at
@@ -647,11 +772,11 @@ static void write_state(const or_world *w, const or_sim *s, int64_t e, const or_
  * H^T R(Q_b) as (M00, M10, M20, M01, M11, M21) [6D representation of Zhou
  * et al. cited in Sec. 6.1]; H^T V_b; H^T W_b.  Last entry: the phase.
  */
-static void obs_of(const or_world *w, const vec3 *P, const quat *Q, const vec3 *V,
-                   const vec3 *W, float phase, double *o_out)
+/* H^T of the heading frame of root orientation Q0 (identity if degenerate). */
+static void heading_T(quat Q0, double HT[9])
 {
     double R0[9];
-    qmat(Q[0], R0);
+    qmat(Q0, R0);
     double fx = R0[0], fy = R0[3];
     double h2 = fx * fx + fy * fy;
     double c = 1.0, s = 0.0;
@@ -660,29 +785,73 @@ static void obs_of(const or_world *w, const vec3 *P, const quat *Q, const vec3 *
         c = fx / hn;
         s = fy / hn;
     }
-    /* H^T as a matrix */
-    double HT[9] = {c, s, 0.0, -s, c, 0.0, 0.0, 0.0, 1.0};
+    double M[9] = {c, s, 0.0, -s, c, 0.0, 0.0, 0.0, 1.0};
+    for (int i = 0; i < 9; ++i) HT[i] = M[i];
+}
+
+/* 9 values of a frame in the heading frame: H^T (P - o), then the first two
+ * columns of H^T R(Q). */
+static void frame9(const double HT[9], vec3 org, vec3 P, quat Q, double *o)
+{
+    vec3 p = matvec(HT, vsub(P, org));
+    double R[9];
+    qmat(Q, R);
+    vec3 col0 = matvec(HT, v3(R[0], R[3], R[6]));
+    vec3 col1 = matvec(HT, v3(R[1], R[4], R[7]));
+    o[0] = p.x; o[1] = p.y; o[2] = p.z;
+    o[3] = col0.x; o[4] = col0.y; o[5] = col0.z;
+    o[6] = col1.x; o[7] = col1.y; o[8] = col1.z;
+}
+
+static void obs_of(const or_world *w, const vec3 *P, const quat *Q, const vec3 *V,
+                   const vec3 *W, float phase, double *o_out)
+{
+    double HT[9];
+    heading_T(Q[0], HT);
     vec3 org = v3(P[0].x, P[0].y, 0.0);
     for (int b = 0; b < w->B; ++b) {
         double *o = o_out + 15 * b;
-        vec3 p = matvec(HT, vsub(P[b], org));
-        double R[9];
-        qmat(Q[b], R);
-        vec3 col0 = matvec(HT, v3(R[0], R[3], R[6]));
-        vec3 col1 = matvec(HT, v3(R[1], R[4], R[7]));
+        frame9(HT, org, P[b], Q[b], o);
         vec3 lv = matvec(HT, V[b]);
         vec3 av = matvec(HT, W[b]);
-        o[0] = p.x; o[1] = p.y; o[2] = p.z;
-        o[3] = col0.x; o[4] = col0.y; o[5] = col0.z;
-        o[6] = col1.x; o[7] = col1.y; o[8] = col1.z;
         o[9] = lv.x; o[10] = lv.y; o[11] = lv.z;
         o[12] = av.x; o[13] = av.y; o[14] = av.z;
     }
     o_out[15 * w->B] = (double)phase;
 }
 
-static void obs_from_sim(const or_world *w, const or_sim *s, int64_t e, float phase, float *obs,
-                         int64_t ld_obs)
+/*
+ * Observation extras after the 15B+1 rows [Sec. 6.1, PHC observation]: for
+ * j = 1..K the reference of clip k at the phase of the j-th next control
+ * step (ph_j = ph_{j-1} + dphi_k in fp32, evaluated at min(ph_j, 1)): the
+ * root, then each end effector in body order, as 9 values in the heading
+ * frame of the current sim root; then the previous action (zeros for NULL).
+ */
+static void obs_extras(const or_world *w, int k, float ph, quat Q0, vec3 P0, const float *prev,
+                       double *o)
+{
+    double HT[9];
+    heading_T(Q0, HT);
+    vec3 org = v3(P0.x, P0.y, 0.0);
+    int idx = 0;
+    float phj = ph;
+    for (int j = 1; j <= w->obs_future; ++j) {
+        phj = phj + w->clips[k].dphi;
+        float phi_ev = phj < 1.0f ? phj : 1.0f;
+        or_state S;
+        ref_state(w, k, phi_ev, &S);
+        for (int m = 0; m <= w->n_ee; ++m) {
+            int b = m == 0 ? 0 : w->ee[m - 1];
+            frame9(HT, org, S.P[b], S.Q[b], o + idx);
+            idx += 9;
+        }
+    }
+    if (w->obs_prev_action)
+        for (int a = 0; a < w->A; ++a) o[idx++] = prev ? (double)prev[a] : 0.0;
+}
+
+static void obs_from_sim(const or_world *w, const or_sim *s, int64_t e, float phase, int k,
+                         const float *prev, float *obs, int64_t ld_obs)
 {
     vec3 P[OR_MAX_BODIES], V[OR_MAX_BODIES], W[OR_MAX_BODIES];
     quat Q[OR_MAX_BODIES];
@@ -692,9 +861,12 @@ static void obs_from_sim(const or_world *w, const or_sim *s, int64_t e, float ph
         V[b] = sim_v3(s->linvel, b, s->ld, e);
         W[b] = sim_v3(s->angvel, b, s->ld, e);
     }
-    double o[15 * OR_MAX_BODIES + 1];
+    double o[15 * OR_MAX_BODIES + 1 + 4 * (OR_MAX_BODIES + 1) * 9 + 256];
     obs_of(w, P, Q, V, W, phase, o);
-    for (int i = 0; i <= 15 * w->B; ++i) obs[(int64_t)i * ld_obs + e] = (float)o[i];
+    int D0 = 15 * w->B + 1;
+    obs_extras(w, k, phase, Q[0], P[0], prev, o + D0);
+    int D = or_obs_dim(w);
+    for (int i = 0; i < D; ++i) obs[(int64_t)i * ld_obs + e] = (float)o[i];
 }
 
 /* Exported for pins: one env's state as doubles ([B][3], [B][4], ...). */
@@ -745,7 +917,7 @@ static void reset_one(const or_world *w, const or_sim *s, int64_t e, uint32_t n,
 static void env_step_one(const or_world *w, int64_t e, int32_t *env_clip, float *env_phase,
                          int32_t *env_t, uint32_t *env_n, const or_sim *s, float *reward,
                          uint8_t *term_out, uint8_t *trunc_out, float *obs, int64_t ld_obs,
-                         int32_t *ref_frame)
+                         int32_t *ref_frame, const float *prev_action)
 {
     int k = env_clip[e];
     const or_clip *c = &w->clips[k];
@@ -765,13 +937,22 @@ static void env_step_one(const or_world *w, int64_t e, int32_t *env_clip, float 
     ref_local(w, k, i0, (double)alpha, &L);
     or_state Sr;
     fk(w, &L, &Sr);
-    vec3 P[OR_MAX_BODIES], V[OR_MAX_BODIES];
+    vec3 P[OR_MAX_BODIES], V[OR_MAX_BODIES], W[OR_MAX_BODIES];
+    quat Q[OR_MAX_BODIES];
     for (int b = 0; b < w->B; ++b) {
         P[b] = sim_v3(s->pos, b, s->ld, e);
         V[b] = sim_v3(s->linvel, b, s->ld, e);
+        Q[b] = sim_q(s->quat, b, s->ld, e);
+        W[b] = sim_v3(s->angvel, b, s->ld, e);
     }
-    or_reward_t r = reward_of(w, P, V, Sr.P, Sr.V);
-    float r_out = (float)r.r;
+    float r_out;
+    if (w->reward_form == 1) {
+        or_mreward_t r = mreward_of(w, P, Q, W, &L, &Sr);
+        r_out = (float)r.r;
+    } else {
+        or_reward_t r = reward_of(w, P, V, Sr.P, Sr.V);
+        r_out = (float)r.r;
+    }
     float z_root = s->pos[2 * s->ld + e];
     int term = terminated_of(w, t1, z_root, r_out);
     reward[e] = r_out;
@@ -780,26 +961,30 @@ static void env_step_one(const or_world *w, int64_t e, int32_t *env_clip, float 
 
     /* masked reset (every env runs this; only done envs change) */
     env_n[e] = n1;
+    const float *prev = NULL;
     if (term || trunc) {
         reset_one(w, s, e, n1, OR_TAG_RESET, env_clip, env_phase, env_t);
     } else {
         env_phase[e] = phi1;
         env_t[e] = t1;
+        if (w->obs_prev_action && prev_action) prev = prev_action + (int64_t)w->A * e;
     }
-    /* observation of the post-reset state */
-    obs_from_sim(w, s, e, env_phase[e], obs, ld_obs);
+    /* observation of the post-reset state (a reset env has no previous action) */
+    obs_from_sim(w, s, e, env_phase[e], env_clip[e], prev, obs, ld_obs);
 }
 
 /*
  * Batch step over envs idx[0..n_idx) (all N envs when idx is NULL).
  * Buffers follow the library's layout: env arrays [ld], sim [B][c][ld],
- * outputs [ld], obs [15B+1][ld_obs].  ref_frame may be NULL.
+ * outputs [ld], obs [D][ld_obs] (D = or_obs_dim).  ref_frame may be NULL;
+ * prev_action ([N][A], the actions applied in this step) may be NULL when the
+ * observation has no previous-action rows.
  */
 void or_env_step(const or_world *w, int64_t N, const int64_t *idx, int64_t n_idx,
                  int32_t *env_clip, float *env_phase, int32_t *env_t, uint32_t *env_n,
                  float *pos, float *quat_, float *linvel, float *angvel, int64_t ld,
                  float *reward, uint8_t *term, uint8_t *trunc, float *obs, int64_t ld_obs,
-                 int32_t *ref_frame)
+                 int32_t *ref_frame, const float *prev_action)
 {
     or_sim s = {pos, quat_, linvel, angvel, ld};
     int64_t m = idx ? n_idx : N;
@@ -807,7 +992,7 @@ void or_env_step(const or_world *w, int64_t N, const int64_t *idx, int64_t n_idx
     for (int64_t j = 0; j < m; ++j) {
         int64_t e = idx ? idx[j] : j;
         env_step_one(w, e, env_clip, env_phase, env_t, env_n, &s, reward, term, trunc, obs,
-                     ld_obs, ref_frame);
+                     ld_obs, ref_frame, prev_action);
     }
 }
 
@@ -826,7 +1011,7 @@ void or_reset_envs(const or_world *w, int64_t N, const uint8_t *mask, int32_t *e
     for (int64_t e = 0; e < N; ++e) {
         if (mask && !mask[e]) continue;
         reset_one(w, &s, e, env_n[e], OR_TAG_EXT_RESET, env_clip, env_phase, env_t);
-        obs_from_sim(w, &s, e, env_phase[e], obs, ld_obs);
+        obs_from_sim(w, &s, e, env_phase[e], env_clip[e], NULL, obs, ld_obs);
     }
 }
 

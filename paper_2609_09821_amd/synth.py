@@ -173,6 +173,8 @@ def make_policy(rng, dims, bf16, sigma=0.05):
 
 
 # The five benchmark workloads.  Seeds: master = workload id.
+R_MIN_6 = 0.587   # the oracle's 20th-percentile reward of this workload (3 s.f.)
+
 CONFIGS = {
     1: dict(name="S15 64 envs single step, fp32 MLP 226-1024-512-28", n_envs=64, skeleton="S15",
             frames=[30], mlp=[226, 1024, 512, 28], bf16=False, steps=1, sigma_joint=0.05),
@@ -189,6 +191,17 @@ CONFIGS = {
                  "bf16 MLP 226-1024-512-28",
             n_envs=262144, skeleton="S15", frames="16x60-300", mlp=[226, 1024, 512, 28],
             bf16=True, steps=16, sigma_joint=0.3),
+    # the training step's terms: multiplicative 5-term reward (joint rotation 10, COM 10 and
+    # end-effector orientation 2 as in the configuration table; joint velocity 0.1 and
+    # end-effector position 40 read from DeepMimic's scales), termination height 0.8 and
+    # 4 grace steps (table baseline), 2 future reference frames and the previous action in
+    # the observation (D = 361 + 2*6*9 + 69 = 538)
+    6: dict(name="S24 16384 envs 32-step rollout, 300-frame clip, multiplicative reward, "
+                 "observation with 2 future frames + previous action, bf16 MLP 538-1024-1024-512-69",
+            n_envs=16384, skeleton="S24", frames=[300], mlp=[538, 1024, 1024, 512, 69],
+            bf16=True, steps=32, sigma_joint=0.01, sigma_vel=0.1,
+            config=dict(reward_form=1, h_term=0.8, grace=4, r_min=R_MIN_6,
+                        obs_future=2, obs_prev_action=1)),
 }
 
 SEED_BASE = 0x0A11_2609_0982_1000
@@ -204,9 +217,23 @@ def step_config(master, **over):
         c_vel=0.25, w_vel=0.25,
         c_com=0.15, w_com=8.0,
         seed=SEED_BASE + int(master),
+        # training terms: reward_form 1 = multiplicative reward with weights
+        # m_jrot, m_jvel, m_com, m_eepos, m_eerot; obs_future reference frames
+        # and the previous action in the observation
+        reward_form=0,
+        m_jrot=10.0, m_jvel=0.1, m_com=10.0, m_eepos=40.0, m_eerot=2.0,
+        obs_future=0, obs_prev_action=0,
     )
+    cfg.update(CONFIGS.get(int(master), {}).get("config", {}))
     cfg.update(over)
     return cfg
+
+
+def obs_dim(n_bodies, n_ee, n_actions, cfg):
+    """Observation width: 15 rows per body, the phase, 9 per future reference
+    frame of the root and each end effector, the previous action."""
+    return (15 * n_bodies + 1 + int(cfg["obs_future"]) * (1 + n_ee) * 9
+            + (n_actions if cfg["obs_prev_action"] else 0))
 
 
 def make_world(cfg_id, n_envs=None, **cfg_over):
@@ -231,5 +258,5 @@ def make_world(cfg_id, n_envs=None, **cfg_over):
         policy=pol,
         config=cfg,
         sigma_joint=float(spec["sigma_joint"]),
-        sigma_vel=0.5,
+        sigma_vel=float(spec.get("sigma_vel", 0.5)),
     )
