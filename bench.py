@@ -81,11 +81,12 @@ def measured_traffic(kind, wid):
     return rd + wr, rd, wr
 
 
-def algorithmic_env_bytes(B, D, n_envs, n_reset):
+def algorithmic_env_bytes(B, D, n_envs, n_reset, A_prev=0):
     """HBM bytes one env step must move: sim state read (52 B per body), env
-    state in and out (16 + 16), reward (4), flags (2), observation (4 D), and
-    the reference sim state written for reset envs (52 B per body)."""
-    return n_envs * (52 * B + 32 + 6 + 4 * D) + n_reset * 52 * B
+    state in and out (16 + 16), reward (4), flags (2), observation (4 D), the
+    previous action read when the observation holds it (4 A_prev), and the
+    reference sim state written for reset envs (52 B per body)."""
+    return n_envs * (52 * B + 32 + 6 + 4 * D + 4 * A_prev) + n_reset * 52 * B
 
 
 def mlp_flops(dims, n_envs):
@@ -108,6 +109,8 @@ def run_gpu(wid, steps, warmup, graph=True):
 
     # ---- record: initial reset, then stand-in sim states of every step ----
     ctx.reset_envs(bufs)
+    if bufs.prev_action is not None:
+        bufs.prev_action.normal_()
     init = {k: getattr(bufs, k).clone() for k in binding.EnvBuffers.ENV + ("obs",)}
     rec = []
     resets = []
@@ -127,6 +130,11 @@ def run_gpu(wid, steps, warmup, graph=True):
     mean = torch.empty((N, A), device="cuda")
     action = torch.empty((N, A), device="cuda")
     logp = torch.empty(N, device="cuda")
+    A_prev = 0
+    if bufs.prev_action is not None:
+        # the observation's previous action is the action the policy just drew
+        bufs.prev_action = action
+        A_prev = A
 
     def step(t, ev=None):
         bufs.body_pos, bufs.body_quat, bufs.body_linvel, bufs.body_angvel = rec[t]
@@ -193,7 +201,8 @@ def run_gpu(wid, steps, warmup, graph=True):
     pol_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     env_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     rho = float(np.mean(n_reset[warmup:]) / N)
-    env_bytes = np.mean([algorithmic_env_bytes(B, D, N, n_reset[warmup + t]) for t in range(steps)])
+    env_bytes = np.mean([algorithmic_env_bytes(B, D, N, n_reset[warmup + t], A_prev)
+                         for t in range(steps)])
     flops = mlp_flops(pol["dims"], N)
     prec = "bf16" if pol["bf16"] else "f32"
     ctx.close()
@@ -216,11 +225,12 @@ def cpu_baseline(wid, target_s=16.0):
     pol = desc["policy"]
 
     def env_part(n):
-        st = oracle.State(w.B, n)
+        st = w.state(n)
         w.reset_envs(st)
         w.standin(st, desc["sigma_joint"], desc["sigma_vel"])
+        prev = np.zeros((n, w.A), np.float32) if desc["config"]["obs_prev_action"] else None
         t0 = time.perf_counter()
-        w.env_step(st)
+        w.env_step(st, prev_action=prev)
         return time.perf_counter() - t0, st
 
     def mlp_part(st, n):
@@ -256,7 +266,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=32)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-graph", action="store_true",

@@ -86,6 +86,20 @@ typedef struct im_ctx im_ctx;
  * Termination (Fig. 5, strict "<"; grace steps from the backflip table):
  *   terminated = (t + 1 > grace) && (root_z < h_term || !(r >= r_min)).
  * Truncation: the clip phase reaches 1.
+ *
+ * Training terms (Sec. 6.1 and the backflip configuration table):
+ *   reward_form = IM_REWARD_MULTIPLICATIVE replaces the reward above by
+ *     r = exp(-m_jrot e_jrot) exp(-m_jvel e_jvel) exp(-m_com e_com)
+ *         exp(-m_eepos e_eepos) exp(-m_eerot e_eerot)
+ *   with e_jrot = sum_b angle(qr_b^-1 q_b)^2 over the joint rotations in the
+ *   parent frame (the root's world orientation for b = 0), e_jvel = sum_b
+ *   |w_b - wr_b|^2 over the joint angular velocities in the parent frame
+ *   (R(Q_p)^T (W_b - W_p); the root's world angular velocity), e_com as above,
+ *   e_eepos = sum over end effectors (leaf bodies) of squared position errors,
+ *   e_eerot = sum over end effectors of squared world-orientation angles.
+ *   obs_future = K (0..4) appends, for the next K control steps, the reference
+ *   frames of the root and the end effectors; obs_prev_action appends the
+ *   action applied in this step (see im_env_bufs).
  */
 typedef struct {
     double dt;        /* control step in seconds (> 0) */
@@ -96,7 +110,13 @@ typedef struct {
     float c_vel, w_vel;
     float c_com, w_com;
     uint64_t seed;    /* Philox4x32-10 key (low word, high word) */
+    int32_t reward_form;      /* IM_REWARD_GROUPED (the form above) or IM_REWARD_MULTIPLICATIVE */
+    float m_jrot, m_jvel, m_com, m_eepos, m_eerot;  /* multiplicative weights (finite) */
+    int32_t obs_future;       /* future reference frames in the observation, 0..4 */
+    int32_t obs_prev_action;  /* 1: the previous action ends the observation */
 } im_config;
+
+enum { IM_REWARD_GROUPED = 0, IM_REWARD_MULTIPLICATIVE = 1 };
 
 /* Host arrays; copied at creation. */
 typedef struct {
@@ -118,7 +138,7 @@ typedef struct {
 } im_clip;
 
 /*
- * Gaussian MLP policy.  dims[0] must be the observation width 15*B+1 and
+ * Gaussian MLP policy.  dims[0] must be the observation width D (im_env_bufs) and
  * dims[L] is the action width A.  Hidden layers: ReLU; last layer linear
  * (the mean).  BF16: observation and hidden activations are rounded to bf16
  * (nearest even), weights are bf16, products accumulate in fp32.  Actions:
@@ -148,11 +168,20 @@ typedef struct {
  *   env_t       [ld] int32  steps since the last reset         (read/write)
  *   env_n       [ld] uint32 step counter of the env's random streams
  *   reward      [ld] float, terminated [ld] uint8, truncated [ld] uint8
- *   obs         [D][ld] float, D = 15*B + 1: per body b at rows 15b..15b+14
- *               heading-frame position (3), first two columns of the
- *               heading-frame rotation matrix (6), heading-frame linear (3)
- *               and angular (3) velocity; row 15B = phase (Sec. 6.1)
+ *   obs         [D][ld] float: per body b at rows 15b..15b+14 heading-frame
+ *               position (3), first two columns of the heading-frame rotation
+ *               matrix (6), heading-frame linear (3) and angular (3) velocity;
+ *               row 15B = phase (Sec. 6.1).  With obs_future = K, for j = 1..K
+ *               the reference of the env's clip at the phase of the j-th next
+ *               control step (phase_j = phase_{j-1} + dphi, fp32, evaluated at
+ *               min(phase_j, 1)): the root, then each end effector in body order,
+ *               9 rows each (heading-frame position and the two columns); then,
+ *               with obs_prev_action, A rows of the previous action (zero for an
+ *               env reset in this call).  D = 15B + 1 + 9 K (1 + n_ee) + A?
  *   ref_frame   [ld] int32 or NULL: reference frame index used this step
+ *   prev_action [n_envs][A] float, read when obs_prev_action (else may be
+ *               NULL): the action applied in this step (the im_policy_act
+ *               output of the step).  Appended after ld.
  */
 typedef struct {
     float *body_pos;
@@ -170,6 +199,7 @@ typedef struct {
     int32_t *ref_frame;
     int64_t n_envs;
     int64_t ld;
+    const float *prev_action;
 } im_env_bufs;
 
 typedef struct {

@@ -27,7 +27,10 @@ class ImConfig(C.Structure):
     _fields_ = [("dt", C.c_double), ("h_term", C.c_float), ("r_min", C.c_float),
                 ("grace", C.c_int32), ("c_pose", C.c_float), ("w_pos", C.c_float),
                 ("w_ee", C.c_float), ("c_vel", C.c_float), ("w_vel", C.c_float),
-                ("c_com", C.c_float), ("w_com", C.c_float), ("seed", C.c_uint64)]
+                ("c_com", C.c_float), ("w_com", C.c_float), ("seed", C.c_uint64),
+                ("reward_form", C.c_int32), ("m_jrot", C.c_float), ("m_jvel", C.c_float),
+                ("m_com", C.c_float), ("m_eepos", C.c_float), ("m_eerot", C.c_float),
+                ("obs_future", C.c_int32), ("obs_prev_action", C.c_int32)]
 
 
 class ImSkeleton(C.Structure):
@@ -52,7 +55,8 @@ class ImEnvBufs(C.Structure):
                 ("body_angvel", C.c_void_p), ("env_clip", C.c_void_p), ("env_phase", C.c_void_p),
                 ("env_t", C.c_void_p), ("env_n", C.c_void_p), ("reward", C.c_void_p),
                 ("terminated", C.c_void_p), ("truncated", C.c_void_p), ("obs", C.c_void_p),
-                ("ref_frame", C.c_void_p), ("n_envs", C.c_int64), ("ld", C.c_int64)]
+                ("ref_frame", C.c_void_p), ("n_envs", C.c_int64), ("ld", C.c_int64),
+                ("prev_action", C.c_void_p)]
 
 
 class ImInfo(C.Structure):
@@ -177,7 +181,7 @@ def _dptr(t):
 class EnvBuffers:
     """Device buffers of a batch of envs (torch tensors) in the library layout."""
 
-    def __init__(self, n_bodies, n_envs, ld=None, device="cuda"):
+    def __init__(self, n_bodies, n_envs, ld=None, device="cuda", obs_dim=None, n_actions=0):
         import torch
         B = n_bodies
         ld = int(ld if ld is not None else n_envs)
@@ -194,8 +198,11 @@ class EnvBuffers:
         self.reward = torch.zeros(ld, **f)
         self.terminated = torch.zeros(ld, device=device, dtype=torch.uint8)
         self.truncated = torch.zeros(ld, device=device, dtype=torch.uint8)
-        self.obs = torch.zeros((15 * B + 1, ld), **f)
+        self.obs = torch.zeros((15 * B + 1 if obs_dim is None else obs_dim, ld), **f)
         self.ref_frame = torch.zeros(ld, device=device, dtype=torch.int32)
+        # the action applied in the step ([n_envs][A]), read when the observation
+        # ends with the previous action
+        self.prev_action = torch.zeros((max(self.n_envs, 1), n_actions), **f) if n_actions else None
 
     def struct(self, with_ref_frame=True):
         return ImEnvBufs(
@@ -203,7 +210,8 @@ class EnvBuffers:
             self.body_angvel.data_ptr(), self.env_clip.data_ptr(), self.env_phase.data_ptr(),
             self.env_t.data_ptr(), self.env_n.data_ptr(), self.reward.data_ptr(),
             self.terminated.data_ptr(), self.truncated.data_ptr(), self.obs.data_ptr(),
-            self.ref_frame.data_ptr() if with_ref_frame else None, self.n_envs, self.ld)
+            self.ref_frame.data_ptr() if with_ref_frame else None, self.n_envs, self.ld,
+            None if self.prev_action is None else self.prev_action.data_ptr())
 
     SIM = ("body_pos", "body_quat", "body_linvel", "body_angvel")
     ENV = ("env_clip", "env_phase", "env_t", "env_n")
@@ -226,7 +234,11 @@ class Description:
         self.cfg = ImConfig(float(cfg["dt"]), float(cfg["h_term"]), float(cfg["r_min"]),
                             int(cfg["grace"]), float(cfg["c_pose"]), float(cfg["w_pos"]),
                             float(cfg["w_ee"]), float(cfg["c_vel"]), float(cfg["w_vel"]),
-                            float(cfg["c_com"]), float(cfg["w_com"]), int(cfg["seed"]))
+                            float(cfg["c_com"]), float(cfg["w_com"]), int(cfg["seed"]),
+                            int(cfg.get("reward_form", 0)), float(cfg.get("m_jrot", 0.0)),
+                            float(cfg.get("m_jvel", 0.0)), float(cfg.get("m_com", 0.0)),
+                            float(cfg.get("m_eepos", 0.0)), float(cfg.get("m_eerot", 0.0)),
+                            int(cfg.get("obs_future", 0)), int(cfg.get("obs_prev_action", 0)))
         self.skel = ImSkeleton(int(sk["n_bodies"]), _ptr(k(_i32(sk["parent"])), C.c_int32),
                                _ptr(k(_i32(sk["jtype"])), C.c_int32),
                                _ptr(k(_f32(sk["axis"])), C.c_float),
@@ -287,7 +299,9 @@ class Context:
 
     # -- calls on tensors
     def buffers(self, n_envs, ld=None):
-        return EnvBuffers(self.info.n_bodies, n_envs, ld)
+        prev = int(self.desc.cfg.obs_prev_action) != 0
+        return EnvBuffers(self.info.n_bodies, n_envs, ld, obs_dim=self.info.obs_dim,
+                          n_actions=self.info.action_dim if prev else 0)
 
     def env_step_fused(self, bufs, stream=None, with_ref_frame=True):
         im_env_step_fused(self.ptr, bufs.struct(with_ref_frame), _stream(stream))

@@ -157,6 +157,14 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
         }
         t->massw[i] = (float)((double)sk->mass[b] / msum);
     }
+    for (int b = 0; b < B; ++b) t->pbody[b] = b > 0 ? sk->parent[b] : -1;
+    // future-frame slots: the root, then the leaves in body order
+    t->n_ee = 0;
+    std::vector<int> slot_of(B, -1);
+    for (int b = 1; b < B; ++b)
+        if (ch[b].empty()) slot_of[b] = 1 + t->n_ee++;
+    slot_of[0] = 0;
+    for (int i = 0; i < B; ++i) t->ee_slot[i] = slot_of[order[i]];
 
     // Two half walks for the fused step.  Half 1 owns the subtrees of a set S
     // of children of one branch point v, half 0 everything else (root
@@ -249,6 +257,14 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
     return "";
 }
 
+// Observation width: 15 rows per body, the phase, 9 per future frame of the
+// root and each end effector, the previous action.
+int64_t obs_width(int B, int n_ee, const im_config *cfg, int A)
+{
+    return 15 * (int64_t)B + 1 + 9 * (int64_t)cfg->obs_future * (1 + n_ee) +
+           (cfg->obs_prev_action ? A : 0);
+}
+
 std::string validate(const im_config *cfg, const im_skeleton *sk, const im_clip *clips,
                      int32_t n_clips, const im_policy *pol, int64_t max_envs, im_status *code)
 {
@@ -313,7 +329,26 @@ std::string validate(const im_config *cfg, const im_skeleton *sk, const im_clip 
     if (L < 1 || !pol->dims || !pol->weight || !pol->bias || !pol->log_std)
         return "policy description incomplete";
     if (pol->dtype != IM_DTYPE_F32 && pol->dtype != IM_DTYPE_BF16) return "invalid policy dtype";
-    if (pol->dims[0] != 15 * B + 1) return "policy input width must be 15*B+1";
+    if (cfg->reward_form != IM_REWARD_GROUPED && cfg->reward_form != IM_REWARD_MULTIPLICATIVE)
+        return "invalid reward_form";
+    const float mw[5] = {cfg->m_jrot, cfg->m_jvel, cfg->m_com, cfg->m_eepos, cfg->m_eerot};
+    for (float w : mw)
+        if (!finite_f(w)) return "multiplicative reward weights must be finite";
+    if (cfg->obs_future < 0 || cfg->obs_future > 4) return "obs_future must be in [0, 4]";
+    if (cfg->obs_prev_action != 0 && cfg->obs_prev_action != 1) return "obs_prev_action must be 0 or 1";
+    if (cfg->obs_future > 0 && B == 1) {
+        *code = IM_ERR_UNSUPPORTED;
+        return "future reference frames need at least two bodies";
+    }
+    {
+        std::vector<int> nch(B, 0);
+        for (int b = 1; b < B; ++b) nch[sk->parent[b]]++;
+        int n_ee = 0;
+        for (int b = 0; b < B; ++b) n_ee += nch[b] == 0 ? 1 : 0;
+        const int64_t D = obs_width(B, n_ee, cfg, pol->dims[L]);
+        if (pol->dims[0] != D)
+            return "policy input width must be the observation width " + std::to_string(D);
+    }
     for (int l = 0; l <= L; ++l)
         if (pol->dims[l] < 1 || pol->dims[l] > 16384) return "layer widths must be in [1, 16384]";
     if (pol->dims[L] > 128) {
@@ -348,7 +383,8 @@ im_status check_env_bufs(const im_ctx *c, const im_env_bufs *b, bool need_output
         return fail(IM_ERR_INVALID_ARG, "NULL env buffer");
     if (need_outputs && (!b->reward || !b->terminated || !b->truncated))
         return fail(IM_ERR_INVALID_ARG, "NULL output buffer");
-    (void)c;
+    if (need_outputs && c->cfg.obs_prev_action && !b->prev_action)
+        return fail(IM_ERR_INVALID_ARG, "the observation needs prev_action");
     return IM_OK;
 }
 
@@ -386,6 +422,17 @@ EnvArgs env_args(const im_ctx *c, const im_env_bufs *b)
     a.w_vel = c->cfg.w_vel;
     a.c_com = c->cfg.c_com;
     a.w_com = c->cfg.w_com;
+    a.reward_form = c->cfg.reward_form;
+    a.obs_prev = c->cfg.obs_prev_action;
+    a.m_jrot = c->cfg.m_jrot;
+    a.m_jvel = c->cfg.m_jvel;
+    a.m_com = c->cfg.m_com;
+    a.m_eepos = c->cfg.m_eepos;
+    a.m_eerot = c->cfg.m_eerot;
+    a.obs_future = c->cfg.obs_future;
+    a.obs_base = 15 * c->B + 1;
+    a.A = c->A;
+    a.prev_action = c->cfg.obs_prev_action ? b->prev_action : nullptr;
     return a;
 }
 
@@ -433,7 +480,7 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess)
         c->n_cu = 0;
     c->B = sk->n_bodies;
-    c->D = 15 * c->B + 1;
+    c->D = (int)obs_width(c->B, tab.n_ee, cfg, pol->dims[pol->n_layers]);
     c->L = pol->n_layers;
     c->A = pol->dims[c->L];
     c->n_clips = n_clips;

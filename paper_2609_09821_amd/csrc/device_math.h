@@ -34,6 +34,12 @@ __device__ __forceinline__ q4 qmul(q4 a, q4 b)
 }
 
 // R(q) v for a unit q: v + w t + u x t with t = 2 u x v.
+__device__ __forceinline__ q4 qconj(q4 a) { return q4{a.w, -a.x, -a.y, -a.z}; }
+// rotation angle in [0, pi] of a unit quaternion (either sign)
+__device__ __forceinline__ float qangle(q4 q)
+{
+    return 2.0f * atan2f(sqrtf(q.x * q.x + q.y * q.y + q.z * q.z), fabsf(q.w));
+}
 __device__ __forceinline__ f3 qrot(q4 q, f3 v)
 {
     f3 u{q.x, q.y, q.z};

@@ -114,7 +114,9 @@ __device__ __forceinline__ Frame child_frame(const Frame &p, const float4 *rec, 
 }
 
 // Forward kinematics of one reference segment record in preorder;
-// visit(i, body, frame, anchor, data) is called for every position i.  A
+// visit(i, body, frame, anchor, data, q_joint, w_joint) is called for every
+// position i (q_joint, w_joint: the reference joint rotation and joint angular
+// velocity in the parent frame; the root's world values).  A
 // depth-2 software prefetch keeps the segment record and the per-body data
 // returned by load(body) for positions i+1 and i+2 in flight while body i is
 // processed, so the memory latency of one body overlaps the arithmetic of
@@ -148,7 +150,9 @@ __device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, co
     }
     f3 A;
     Frame cur = root_frame(rec, alpha, &A);
-    visit(0, 0, cur, A, d0);
+    // visit also gets the body's reference joint rotation and joint angular
+    // velocity in the parent frame (the root's world values)
+    visit(0, 0, cur, A, d0, cur.Q, cur.W);
     if (sk->bslot[0] >= 0) {
         pack_frame(cur, buf);
         st.put(sk->bslot[0], buf);
@@ -177,15 +181,19 @@ __device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, co
         const f3 r = qrot(cur.Q, off);
         c.P = cur.P + r;
         c.V = cur.V + cross3(cur.W, r);
+        q4 ql = q4{1.0f, 0.0f, 0.0f, 0.0f};
+        f3 wl = mk3(0.0f, 0.0f, 0.0f);
         if (sk->jtype[i] == IM_JOINT_FIXED) {
             c.Q = cur.Q;
             c.W = cur.W;
         } else {
-            c.Q = qmul(cur.Q, slerp_basis(ra, ru, alpha * rw.w));
-            c.W = cur.W + qrot(cur.Q, mk3(rw.x, rw.y, rw.z));
+            ql = slerp_basis(ra, ru, alpha * rw.w);
+            wl = mk3(rw.x, rw.y, rw.z);
+            c.Q = qmul(cur.Q, ql);
+            c.W = cur.W + qrot(cur.Q, wl);
         }
         cur = c;
-        visit(i, sk->body[i], cur, A, d);
+        visit(i, sk->body[i], cur, A, d, ql, wl);
         if (sk->bslot[i] >= 0) {
             pack_frame(cur, buf);
             st.put(sk->bslot[i], buf);
@@ -263,6 +271,30 @@ __device__ __forceinline__ void st4(float *a, int b, int64_t ld, int64_t e, q4 q
     p[3 * ld] = q.z;
 }
 
+// 9 observation rows of a frame in the heading frame, starting at row `row`:
+// position, then the first two columns of the rotation matrix.
+__device__ __forceinline__ void write_frame9(float *obs, int64_t ld, int64_t e, int row,
+                                             const Heading &h, f3 P, q4 Q)
+{
+    float *o = obs + (int64_t)row * ld + e;
+    const float px = P.x - h.ox, py = P.y - h.oy;
+    o[0] = h.c * px + h.s * py;
+    o[ld] = h.c * py - h.s * px;
+    o[2 * ld] = P.z;
+    const float c0x = 1.0f - 2.0f * (Q.y * Q.y + Q.z * Q.z);
+    const float c0y = 2.0f * (Q.x * Q.y + Q.w * Q.z);
+    const float c0z = 2.0f * (Q.x * Q.z - Q.w * Q.y);
+    const float c1x = 2.0f * (Q.x * Q.y - Q.w * Q.z);
+    const float c1y = 1.0f - 2.0f * (Q.x * Q.x + Q.z * Q.z);
+    const float c1z = 2.0f * (Q.y * Q.z + Q.w * Q.x);
+    o[3 * ld] = h.c * c0x + h.s * c0y;
+    o[4 * ld] = h.c * c0y - h.s * c0x;
+    o[5 * ld] = c0z;
+    o[6 * ld] = h.c * c1x + h.s * c1y;
+    o[7 * ld] = h.c * c1y - h.s * c1x;
+    o[8 * ld] = c1z;
+}
+
 // 15 observation rows of body b in the heading frame.
 __device__ __forceinline__ void write_obs_body(float *obs, int64_t ld, int64_t e, int b,
                                                const Heading &h, f3 P, q4 Q, f3 V, f3 W)
@@ -306,6 +338,42 @@ __device__ __forceinline__ void obs_from_sim(const EnvArgs &a, int64_t e, float 
     a.obs[(int64_t)(15 * B) * ld + e] = phase;
 }
 
+// Observation rows after the phase: the reference frames of the root and the
+// end effectors at the next obs_future control steps of clip k (phase_j =
+// phase_{j-1} + dphi in fp32, evaluated at min(phase_j, 1)), in the heading
+// frame of the env's current sim root, then the previous action (zero for an
+// env reset in this call).
+__device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, float ph, bool reset)
+{
+    if (a.obs_future == 0 && !a.obs_prev) return;
+    const int64_t ld = a.ld;
+    const SkelTab *__restrict__ sk = a.sk;
+    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
+    int row = a.obs_base;
+    const ClipTab ci = a.clips[k];
+    float phj = ph;
+    for (int j = 0; j < a.obs_future; ++j) {
+        {
+#pragma clang fp contract(off)
+            phj = phj + ci.dphi;
+        }
+        int i0;
+        float al;
+        phase_index(phj < 1.0f ? phj : 1.0f, ci, &i0, &al);
+        const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
+        const int base = row;
+        walk_prefetch<NoData>(sk, rec, al, [](int) { return NoData{}; },
+                              [&](int i, int, const Frame &f, f3 A, const NoData &, q4, f3) {
+            const int slot = sk->ee_slot[i];
+            if (slot >= 0) write_frame9(a.obs, ld, e, base + 9 * slot, h, A + f.P, f.Q);
+        });
+        row += 9 * (1 + sk->n_ee);
+    }
+    if (a.obs_prev)
+        for (int c = 0; c < a.A; ++c)
+            a.obs[(int64_t)(row + c) * ld + e] = reset ? 0.0f : a.prev_action[e * a.A + c];
+}
+
 // Reference state initialisation: the sim state of env e := the reference
 // at (clip k, phase ph).
 __device__ __forceinline__ void rsi(const EnvArgs &a, int64_t e, int k, float ph)
@@ -317,7 +385,7 @@ __device__ __forceinline__ void rsi(const EnvArgs &a, int64_t e, int k, float ph
     const float4 *rec = a.seg + ci.seg_base + (int64_t)j0 * seg_stride(a.sk->B);
     const int64_t ld = a.ld;
     walk_prefetch<NoData>(a.sk, rec, al, [](int) { return NoData{}; },
-                          [&](int, int b, const Frame &f, f3 A, const NoData &) {
+                          [&](int, int b, const Frame &f, f3 A, const NoData &, q4, f3) {
         st3(a.pos, b, ld, e, A + f.P);
         st4(a.quat, b, ld, e, f.Q);
         st3(a.linvel, b, ld, e, f.V);
@@ -556,7 +624,14 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
     else obs_half_from_sim(a, hw, e);
 }
 
-// The fused step, one thread per env (large batches).
+struct SimMul {
+    f3 P, W, Wp;
+    q4 Q, Qp;   // the body's and its parent's orientation
+};
+
+// The fused step, one thread per env (large batches and the training terms).
+// MUL: the multiplicative reward.
+template <bool MUL>
 __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
 {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -564,6 +639,8 @@ __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
     const int64_t ld = a.ld;
     const SkelTab *__restrict__ sk = a.sk;
     float ph_out = 0.0f;
+    int k_fin = 0;
+    bool reset = false;
 
     if (active) {
         // 1. discrete state advance (fp32, exact contract)
@@ -582,29 +659,73 @@ __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
         float alpha;
         phase_index(phi1 < 1.0f ? phi1 : 1.0f, ci, &i0, &alpha);
 
-        // 2.-3. reference FK and errors against the sim positions/velocities
-        float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
-        f3 dc = mk3(0.0f, 0.0f, 0.0f);
+        // 2.-3. reference FK and errors against the sim state
         const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
-        auto load_pv = [&](int b) {
-            SimPV s;
-            s.P = ld3(a.pos, b, ld, e);
-            s.V = ld3(a.linvel, b, ld, e);
-            return s;
-        };
-        walk_prefetch<SimPV>(sk, rec, alpha, load_pv,
-                             [&](int i, int, const Frame &f, f3 A, const SimPV &sb) {
-            const f3 dp = (sb.P - A) - f.P;
-            const f3 dv = sb.V - f.V;
-            const float x = dot3(dp, dp);
-            e_pos += x;
-            if (sk->leaf[i]) e_ee += x;
-            dc = dc + sk->massw[i] * dp;
-            e_vel += dot3(dv, dv);
-        });
-        const float e_com = dot3(dc, dc);
-        const float r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
-                        a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
+        float r;
+        if constexpr (!MUL) {
+            float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
+            f3 dc = mk3(0.0f, 0.0f, 0.0f);
+            auto load_pv = [&](int b) {
+                SimPV s;
+                s.P = ld3(a.pos, b, ld, e);
+                s.V = ld3(a.linvel, b, ld, e);
+                return s;
+            };
+            walk_prefetch<SimPV>(sk, rec, alpha, load_pv,
+                                 [&](int i, int, const Frame &f, f3 A, const SimPV &sb, q4, f3) {
+                const f3 dp = (sb.P - A) - f.P;
+                const f3 dv = sb.V - f.V;
+                const float x = dot3(dp, dp);
+                e_pos += x;
+                if (sk->leaf[i]) e_ee += x;
+                dc = dc + sk->massw[i] * dp;
+                e_vel += dot3(dv, dv);
+            });
+            const float e_com = dot3(dc, dc);
+            r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
+                a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
+        } else {
+            // the sim's joint rotations and joint angular velocities in the
+            // parent frame need the parent's orientation and angular velocity
+            float e_jrot = 0.0f, e_jvel = 0.0f, e_eepos = 0.0f, e_eerot = 0.0f;
+            f3 dc = mk3(0.0f, 0.0f, 0.0f);
+            auto load_m = [&](int b) {
+                SimMul s;
+                s.P = ld3(a.pos, b, ld, e);
+                s.Q = ld4(a.quat, b, ld, e);
+                s.W = ld3(a.angvel, b, ld, e);
+                const int p = b > 0 ? sk->pbody[b] : 0;
+                s.Qp = ld4(a.quat, p, ld, e);
+                s.Wp = ld3(a.angvel, p, ld, e);
+                return s;
+            };
+            walk_prefetch<SimMul>(sk, rec, alpha, load_m,
+                                  [&](int i, int, const Frame &f, f3 A, const SimMul &sb, q4 qr,
+                                      f3 wr) {
+                q4 ql = sb.Q;
+                f3 wl = sb.W;
+                if (i > 0) {
+                    const q4 ip = qconj(sb.Qp);
+                    ql = qmul(ip, sb.Q);
+                    wl = qrot(ip, sb.W - sb.Wp);
+                }
+                const float th = qangle(qmul(qconj(qr), ql));
+                e_jrot += th * th;
+                const f3 dw = wl - wr;
+                e_jvel += dot3(dw, dw);
+                const f3 dp = (sb.P - A) - f.P;
+                dc = dc + sk->massw[i] * dp;
+                if (sk->leaf[i]) {
+                    e_eepos += dot3(dp, dp);
+                    const float te = qangle(qmul(qconj(f.Q), sb.Q));
+                    e_eerot += te * te;
+                }
+            });
+            const float e_com = dot3(dc, dc);
+            // the product of the five exponentials, as one
+            r = expf(-(a.m_jrot * e_jrot + a.m_jvel * e_jvel + a.m_com * e_com +
+                       a.m_eepos * e_eepos + a.m_eerot * e_eerot));
+        }
         const float z_root = a.pos[2 * ld + e];
         const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
 
@@ -627,10 +748,15 @@ __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
         a.term[e] = (uint8_t)term;
         a.trunc[e] = (uint8_t)trunc;
         if (a.ref_frame) a.ref_frame[e] = i0;
+        k_fin = k_out;
+        reset = term || trunc;
     }
     // 5. observation of the post-reset state (this thread's own env: the
     //    reference state it may have just written is read back in order)
-    if (active) obs_from_sim(a, e, ph_out);
+    if (active) {
+        obs_from_sim(a, e, ph_out);
+        obs_extras(a, e, k_fin, ph_out, reset);
+    }
 }
 
 __global__ __launch_bounds__(256) void reset_kernel(EnvArgs a)
@@ -647,6 +773,7 @@ __global__ __launch_bounds__(256) void reset_kernel(EnvArgs a)
     a.env_phase[e] = ph;
     a.env_t[e] = 0;
     obs_from_sim(a, e, ph);
+    obs_extras(a, e, k, ph, true);
 }
 
 // ---------------------------------------------------------------------------
@@ -908,7 +1035,11 @@ static hipError_t launch_env(void (*k)(EnvArgs), int n_slots, int frame_floats,
 hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s)
 {
     if (a.n <= 0) return hipSuccess;
-    if (a.n > SPLIT_ENV_MAX) return launch_env(env_step_kernel, n_slots, 13, a, s);
+    // the two-thread kernel covers the grouped reward and the 15 B + 1 observation
+    if (a.reward_form == IM_REWARD_MULTIPLICATIVE)
+        return launch_env(env_step_kernel<true>, n_slots, 13, a, s);
+    if (a.n > SPLIT_ENV_MAX || a.obs_future > 0 || a.obs_prev)
+        return launch_env(env_step_kernel<false>, n_slots, 13, a, s);
     // two threads per env: 128 envs per 256-thread block
     const int bs = 256;
     const size_t lds = (size_t)(half_slots > 0 ? half_slots : 1) * 13 * sizeof(float) * bs;

@@ -26,6 +26,10 @@ struct SkelTab {
     float offset[IM_MAX_BODIES][4];
     float axis[IM_MAX_BODIES][4];
     float massw[IM_MAX_BODIES];    // m_b / sum m
+    int32_t pbody[IM_MAX_BODIES];  // by body index: its parent (-1 for the root)
+    int32_t ee_slot[IM_MAX_BODIES];  // observation slot of the future frames: 0 the
+                                     // root, 1.. the end effectors in body order, -1 none
+    int32_t n_ee;                  // end effectors (leaves)
     // The fused step splits every env over two threads: half h walks the
     // bodies it owns and their ancestors (see HalfWalk).
     int32_t half_slots;            // parked-frame slots needed by either half walk
@@ -86,6 +90,14 @@ struct EnvArgs {
     float h_term, r_min;
     float c_pose, w_pos, w_ee, c_vel, w_vel, c_com, w_com;
     float sigma_joint, sigma_vel;
+    // training terms
+    int32_t reward_form;       // IM_REWARD_GROUPED or IM_REWARD_MULTIPLICATIVE
+    int32_t obs_prev;          // previous-action rows in the observation
+    float m_jrot, m_jvel, m_com, m_eepos, m_eerot;
+    int32_t obs_future;        // future reference frames in the observation
+    int32_t obs_base;          // first observation row after the phase (15 B + 1)
+    int32_t A;                 // action width (previous-action rows)
+    const float *prev_action;  // [n][A] (read by the step when obs_prev)
 };
 
 }  // namespace im

@@ -93,6 +93,10 @@ def test_create_rejects_null_pointers(lib):
     ("r_min", float("nan"), binding.IM_ERR_INVALID_ARG, "thresholds"),
     ("grace", -1, binding.IM_ERR_INVALID_ARG, "grace"),
     ("w_ee", float("nan"), binding.IM_ERR_INVALID_ARG, "weights"),
+    ("reward_form", 2, binding.IM_ERR_INVALID_ARG, "reward_form"),
+    ("m_jvel", float("inf"), binding.IM_ERR_INVALID_ARG, "multiplicative"),
+    ("obs_future", 5, binding.IM_ERR_INVALID_ARG, "obs_future"),
+    ("obs_prev_action", 3, binding.IM_ERR_INVALID_ARG, "obs_prev_action"),
 ])
 def test_create_rejects_bad_config(lib, field, value, code, words):
     d = binding.Description(_world())
@@ -173,7 +177,7 @@ def test_create_rejects_bad_policies(lib):
     dims = list(pol["dims"])
     bad_in = dict(pol, dims=[dims[0] + 1] + dims[1:])
     _, (st, _) = _status(dict(w, policy=bad_in))
-    _expect(lib, st, binding.IM_ERR_INVALID_ARG, "15*B+1")
+    _expect(lib, st, binding.IM_ERR_INVALID_ARG, "observation width")
     ls = pol["log_std"].copy(); ls[0] = np.nan
     _, (st, _) = _status(dict(w, policy=dict(pol, log_std=ls)))
     _expect(lib, st, binding.IM_ERR_INVALID_ARG, "log_std")
@@ -185,6 +189,20 @@ def test_create_rejects_bad_policies(lib):
     d.weight_ptrs[1] = None
     st, _ = d.create_status(64)
     _expect(lib, st, binding.IM_ERR_INVALID_ARG, "NULL weight")
+
+
+def test_create_checks_the_observation_width_of_the_training_terms(lib):
+    # 2 future frames and the previous action widen the observation: a policy
+    # sized for 15 B + 1 is rejected, one sized for D = 538 passes validation
+    w = synth.make_world(6, n_envs=64)
+    d = binding.Description(w)
+    d.cfg.obs_future = 1
+    st, _ = d.create_status(64)
+    _expect(lib, st, binding.IM_ERR_INVALID_ARG, "observation width 484")
+    d = binding.Description(w)
+    d.cfg.obs_prev_action = 0
+    st, _ = d.create_status(64)
+    _expect(lib, st, binding.IM_ERR_INVALID_ARG, "observation width 469")
 
 
 def test_create_reports_unsupported_sizes(lib):

@@ -19,10 +19,10 @@ from tests import gpu_helpers as H
 
 pytestmark = pytest.mark.gpu
 
-FULL = {4: 2, 5: 2}          # workload -> teacher-forced steps
+FULL = {4: 2, 5: 2, 6: 6}    # workload -> teacher-forced steps (6: past its grace period)
 
 
-@pytest.fixture(scope="module", params=[4, 5])
+@pytest.fixture(scope="module", params=[4, 5, 6])
 def world(request):
     cfg = request.param
     d = synth.make_world(cfg)
@@ -39,7 +39,7 @@ def test_full_size_env_step(world):
     cfg, d, w, ctx, bufs = world
     N = d["n_envs"]
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     ctx.reset_envs(bufs)
     g = H.download(bufs, N)
@@ -48,13 +48,18 @@ def test_full_size_env_step(world):
     H.compare_sim_obs(g, st, np.ones(N, bool), "full-size reset")
     live = np.ones(N, bool)
     n_done = 0
+    rng = np.random.default_rng(cfg)
     for t in range(FULL[cfg]):
         w.standin(st, d["sigma_joint"], d["sigma_vel"])
         H.upload_state(st, bufs, env=False)
         t_next = st.t + 1
         z_root = st.pos[0, 2].copy()
+        prev = None
+        if bufs.prev_action is not None:
+            prev = rng.normal(size=(N, w.A)).astype(np.float32)
+            bufs.prev_action[:N].copy_(torch.from_numpy(prev))
         ctx.env_step_fused(bufs, with_ref_frame=(t == 0))
-        w.env_step(st)
+        w.env_step(st, prev_action=prev)
         g = H.download(bufs, N)
         if t > 0:
             g.ref_frame = st.ref_frame.copy()     # not written without the optional buffer
@@ -77,7 +82,7 @@ def test_full_size_policy(world):
     N = d["n_envs"]
     pol = d["policy"]
     A = pol["dims"][-1]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     st.n[:] = (np.arange(N, dtype=np.uint64) * 2654435761 % (1 << 32)).astype(np.uint32)
     w.reset_envs(st)
     w.standin(st, d["sigma_joint"], d["sigma_vel"])

@@ -15,8 +15,9 @@ from tests import gpu_helpers as H
 
 pytestmark = pytest.mark.gpu
 
-SIZES = {1: 64, 2: 1000, 3: 1300, 4: 700, 5: 1100}
-STEPS = {1: 1, 2: 6, 3: 6, 4: 4, 5: 6}
+SIZES = {1: 64, 2: 1000, 3: 1300, 4: 700, 5: 1100, 6: 900}
+STEPS = {1: 1, 2: 6, 3: 6, 4: 4, 5: 6, 6: 7}
+RNG = np.random.default_rng(2609)
 
 
 def _setup(cfg, N, ld=None, **over):
@@ -27,11 +28,11 @@ def _setup(cfg, N, ld=None, **over):
     return d, w, ctx, bufs
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_reset_envs_parity(cfg):
     N = SIZES[cfg]
     d, w, ctx, bufs = _setup(cfg, N)
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     st.n[:] = (np.arange(N, dtype=np.uint32) * 2654435761) & 0xFFFF
     H.upload_state(st, bufs)
     ctx.reset_envs(bufs)
@@ -42,12 +43,12 @@ def test_reset_envs_parity(cfg):
     H.compare_sim_obs(g, st, np.ones(N, bool), "reset")
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_env_step_parity(cfg):
     N, T = SIZES[cfg], STEPS[cfg]
     d, w, ctx, bufs = _setup(cfg, N)
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     H.upload_state(st, bufs)
     ctx.reset_envs(bufs)
@@ -56,10 +57,14 @@ def test_env_step_parity(cfg):
     for t in range(T):
         w.standin(st, d["sigma_joint"], d["sigma_vel"])
         H.upload_state(st, bufs, env=False)
+        prev = None
+        if bufs.prev_action is not None:       # the action applied in this step
+            prev = RNG.normal(size=(N, w.A)).astype(np.float32)
+            bufs.prev_action[:N].copy_(torch.from_numpy(prev))
         t_next = st.t + 1
         z_root = st.pos[0, 2].copy()
         ctx.env_step_fused(bufs)
-        w.env_step(st)
+        w.env_step(st, prev_action=prev)
         g = H.download(bufs, N)
         live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, live)
         H.compare_sim_obs(g, st, live, "step %d" % t)
@@ -69,11 +74,11 @@ def test_env_step_parity(cfg):
                                                                          int((~live).sum())))
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5, 6])
 def test_standin_parity(cfg):
     N = SIZES[cfg]
     d, w, ctx, bufs = _setup(cfg, N)
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     st.n[:] += 3
     H.upload_state(st, bufs)
@@ -88,12 +93,12 @@ def test_standin_parity(cfg):
     del live
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_policy_parity(cfg):
     N = SIZES[cfg]
     d, w, ctx, bufs = _setup(cfg, N)
     pol = d["policy"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     st.n[:] = np.arange(N, dtype=np.uint32) * 3 + 11
     w.reset_envs(st)
     w.standin(st, d["sigma_joint"], d["sigma_vel"])
@@ -128,7 +133,7 @@ def test_env_step_parity_large_batch_kernel(cfg):
     N, T = 40037, 2
     d, w, ctx, bufs = _setup(cfg, N)
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     H.upload_state(st, bufs)
     ctx.reset_envs(bufs)
