@@ -341,15 +341,15 @@ __device__ __forceinline__ void obs_from_sim(const EnvArgs &a, int64_t e, float 
 // Observation rows after the phase: the reference frames of the root and the
 // end effectors at the next obs_future control steps of clip k (phase_j =
 // phase_{j-1} + dphi in fp32, evaluated at min(phase_j, 1)), in the heading
-// frame of the env's current sim root, then the previous action (zero for an
-// env reset in this call).
-__device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, float ph, bool reset)
+// frame h of the env's current (post-reset) sim root, then the previous action
+// (zero for an env reset in this call).  This call writes future frames
+// j = j0, j0 + js, ... (j counted from 0) and, with prev, the action rows.
+__device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, float ph,
+                                           bool reset, const Heading &h, int j0, int js, bool prev)
 {
-    if (a.obs_future == 0 && !a.obs_prev) return;
     const int64_t ld = a.ld;
     const SkelTab *__restrict__ sk = a.sk;
-    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
-    int row = a.obs_base;
+    const int rows_f = 9 * (1 + sk->n_ee);
     const ClipTab ci = a.clips[k];
     float phj = ph;
     for (int j = 0; j < a.obs_future; ++j) {
@@ -357,21 +357,29 @@ __device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, f
 #pragma clang fp contract(off)
             phj = phj + ci.dphi;
         }
+        if (j < j0 || (j - j0) % js != 0) continue;
         int i0;
         float al;
         phase_index(phj < 1.0f ? phj : 1.0f, ci, &i0, &al);
         const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
-        const int base = row;
+        const int base = a.obs_base + j * rows_f;
         walk_prefetch<NoData>(sk, rec, al, [](int) { return NoData{}; },
                               [&](int i, int, const Frame &f, f3 A, const NoData &, q4, f3) {
             const int slot = sk->ee_slot[i];
             if (slot >= 0) write_frame9(a.obs, ld, e, base + 9 * slot, h, A + f.P, f.Q);
         });
-        row += 9 * (1 + sk->n_ee);
     }
-    if (a.obs_prev)
+    if (prev) {
+        const int row = a.obs_base + a.obs_future * rows_f;
         for (int c = 0; c < a.A; ++c)
             a.obs[(int64_t)(row + c) * ld + e] = reset ? 0.0f : a.prev_action[e * a.A + c];
+    }
+}
+
+// The heading frame of env e's current sim root.
+__device__ __forceinline__ Heading sim_heading(const EnvArgs &a, int64_t e)
+{
+    return heading_of(ld4(a.quat, 0, a.ld, e), ld3(a.pos, 0, a.ld, e));
 }
 
 // Reference state initialisation: the sim state of env e := the reference
@@ -401,7 +409,8 @@ using HalfWalk = SkelTab::HalfWalk;
 
 // Forward kinematics over one half walk (root first, preorder), with the same
 // depth-2 prefetch as walk_prefetch; load(body) is called for owned bodies
-// only, and visit(i, body, own, frame, anchor, data) for every position.
+// only, and visit(i, body, own, frame, anchor, data, joint rotation, joint
+// angular velocity) for every position.
 template <class D, class Load, class Visit>
 __device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const float4 *rec,
                                           float alpha, Load &&load, Visit &&visit)
@@ -429,7 +438,7 @@ __device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const 
     }
     f3 A;
     Frame cur = root_frame(rec, alpha, &A);
-    visit(0, 0, w->own[0], cur, A, d0);
+    visit(0, 0, w->own[0], cur, A, d0, cur.Q, cur.W);
     if (w->bslot[0] >= 0) {
         pack_frame(cur, buf);
         st.put(w->bslot[0], buf);
@@ -457,15 +466,19 @@ __device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const 
         const f3 r = qrot(cur.Q, off);
         c.P = cur.P + r;
         c.V = cur.V + cross3(cur.W, r);
+        q4 ql = q4{1.0f, 0.0f, 0.0f, 0.0f};
+        f3 wl = mk3(0.0f, 0.0f, 0.0f);
         if (w->jtype[i] == IM_JOINT_FIXED) {
             c.Q = cur.Q;
             c.W = cur.W;
         } else {
-            c.Q = qmul(cur.Q, slerp_basis(ra, ru, alpha * rw.w));
-            c.W = cur.W + qrot(cur.Q, mk3(rw.x, rw.y, rw.z));
+            ql = slerp_basis(ra, ru, alpha * rw.w);
+            wl = mk3(rw.x, rw.y, rw.z);
+            c.Q = qmul(cur.Q, ql);
+            c.W = cur.W + qrot(cur.Q, wl);
         }
         cur = c;
-        visit(i, w->body[i], w->own[i], cur, A, d);
+        visit(i, w->body[i], w->own[i], cur, A, d, ql, wl);
         if (w->bslot[i] >= 0) {
             pack_frame(cur, buf);
             st.put(w->bslot[i], buf);
@@ -473,12 +486,12 @@ __device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const 
     }
 }
 
-// Observation rows of the bodies a half owns, from the sim state (env not reset).
+// Observation rows of the bodies a half owns, from the sim state (env not
+// reset); h = the heading of the sim root.
 __device__ __forceinline__ void obs_half_from_sim(const EnvArgs &a, const HalfWalk *__restrict__ w,
-                                                  int64_t e)
+                                                  int64_t e, const Heading &h)
 {
     const int64_t ld = a.ld;
-    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
     const int n = w->n;
 #pragma unroll 4
     for (int i = 0; i < n; ++i) {
@@ -491,9 +504,10 @@ __device__ __forceinline__ void obs_half_from_sim(const EnvArgs &a, const HalfWa
 
 // Reference state initialisation of the bodies a half owns at (clip k, phase
 // ph), and their observation rows from the same fp32 values the sim state
-// receives (the heading from the root, which both halves walk first).
-__device__ __forceinline__ void rsi_obs_half(const EnvArgs &a, const HalfWalk *__restrict__ w,
-                                             int64_t e, int k, float ph)
+// receives (the heading from the root, which both halves walk first; it is
+// returned).
+__device__ __forceinline__ Heading rsi_obs_half(const EnvArgs &a, const HalfWalk *__restrict__ w,
+                                                int64_t e, int k, float ph)
 {
     const ClipTab ci = a.clips[k];
     int j0;
@@ -503,7 +517,7 @@ __device__ __forceinline__ void rsi_obs_half(const EnvArgs &a, const HalfWalk *_
     const int64_t ld = a.ld;
     Heading h{};
     walk_half<NoData>(w, rec, al, [](int) { return NoData{}; },
-                      [&](int i, int b, int own, const Frame &f, f3 A, const NoData &) {
+                      [&](int i, int b, int own, const Frame &f, f3 A, const NoData &, q4, f3) {
         const f3 P = A + f.P;
         if (i == 0) h = heading_of(f.Q, P);
         if (!own) return;
@@ -513,7 +527,65 @@ __device__ __forceinline__ void rsi_obs_half(const EnvArgs &a, const HalfWalk *_
         st3(a.angvel, b, ld, e, f.W);
         write_obs_body(a.obs, ld, e, b, h, P, f.Q, f.V, f.W);
     });
+    return h;
 }
+
+struct SimMul {
+    f3 P, W, Wp;
+    q4 Q, Qp;   // the body's and its parent's orientation
+};
+
+// Sim state of body b for the multiplicative reward: the joint rotations and
+// joint angular velocities in the parent frame need the parent's orientation
+// and angular velocity.
+__device__ __forceinline__ SimMul load_mul(const EnvArgs &a, int b, int64_t e)
+{
+    const int64_t ld = a.ld;
+    SimMul s;
+    s.P = ld3(a.pos, b, ld, e);
+    s.Q = ld4(a.quat, b, ld, e);
+    s.W = ld3(a.angvel, b, ld, e);
+    const int p = b > 0 ? a.sk->pbody[b] : 0;
+    s.Qp = ld4(a.quat, p, ld, e);
+    s.Wp = ld3(a.angvel, p, ld, e);
+    return s;
+}
+
+// Error sums of the multiplicative reward.
+struct MulErr {
+    float jrot = 0.0f, jvel = 0.0f, eepos = 0.0f, eerot = 0.0f;
+    f3 dc = mk3(0.0f, 0.0f, 0.0f);
+    // body at walk position i, index b (b = 0: the root); qr, wr: its reference
+    // joint rotation and joint angular velocity
+    __device__ __forceinline__ void add(int b, bool leaf, float massw, const Frame &f, f3 A,
+                                        const SimMul &sb, q4 qr, f3 wr)
+    {
+        q4 ql = sb.Q;
+        f3 wl = sb.W;
+        if (b > 0) {
+            const q4 ip = qconj(sb.Qp);
+            ql = qmul(ip, sb.Q);
+            wl = qrot(ip, sb.W - sb.Wp);
+        }
+        const float th = qangle(qmul(qconj(qr), ql));
+        jrot += th * th;
+        const f3 dw = wl - wr;
+        jvel += dot3(dw, dw);
+        const f3 dp = (sb.P - A) - f.P;
+        dc = dc + massw * dp;
+        if (leaf) {
+            eepos += dot3(dp, dp);
+            const float te = qangle(qmul(qconj(f.Q), sb.Q));
+            eerot += te * te;
+        }
+    }
+    // the product of the five exponentials, as one
+    __device__ __forceinline__ float reward(const EnvArgs &a) const
+    {
+        return expf(-(a.m_jrot * jrot + a.m_jvel * jvel + a.m_com * dot3(dc, dc) +
+                      a.m_eepos * eepos + a.m_eerot * eerot));
+    }
+};
 
 // The fused step for small batches: env e runs on two wavefronts of its
 // block, lane l of wave 2p and of wave 2p+1, the first walking
@@ -522,9 +594,12 @@ __device__ __forceinline__ void rsi_obs_half(const EnvArgs &a, const HalfWalk *_
 // The partial error sums meet in LDS.  Twice the wavefronts of the one-thread
 // kernel for the same envs: below a few waves per SIMD that hides more of the
 // walks' latency, above it the duplicated root and ancestor work costs more.
+// Future reference frames of the observation alternate between the halves.
+// MUL: the multiplicative reward.
+template <bool MUL>
 __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
 {
-    __shared__ float part[6][256];
+    __shared__ float part[7][256];
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hf = wave & 1;
@@ -542,6 +617,7 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
     // 2.-3. reference FK and this half's error sums against the sim state
     float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
     f3 dc = mk3(0.0f, 0.0f, 0.0f);
+    MulErr me;
     if (active) {
         k = safe_clip(a.env_clip[e], a.n_clips);
         const float phi = a.env_phase[e];
@@ -555,44 +631,72 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
         trunc = phi1 >= 1.0f;
         phase_index(phi1 < 1.0f ? phi1 : 1.0f, ci, &i0, &alpha);
         const float4 *rec = a.seg + ci.seg_base + (int64_t)i0 * seg_stride(sk->B);
-        auto load_pv = [&](int b) {
-            SimPV s;
-            s.P = ld3(a.pos, b, ld, e);
-            s.V = ld3(a.linvel, b, ld, e);
-            return s;
-        };
-        walk_half<SimPV>(hw, rec, alpha, load_pv,
-                         [&](int i, int, int own, const Frame &f, f3 A, const SimPV &sb) {
-            if (!own) return;
-            const f3 dp = (sb.P - A) - f.P;
-            const f3 dv = sb.V - f.V;
-            const float x = dot3(dp, dp);
-            e_pos += x;
-            if (hw->leaf[i]) e_ee += x;
-            dc = dc + hw->massw[i] * dp;
-            e_vel += dot3(dv, dv);
-        });
+        if constexpr (!MUL) {
+            auto load_pv = [&](int b) {
+                SimPV s;
+                s.P = ld3(a.pos, b, ld, e);
+                s.V = ld3(a.linvel, b, ld, e);
+                return s;
+            };
+            walk_half<SimPV>(hw, rec, alpha, load_pv,
+                             [&](int i, int, int own, const Frame &f, f3 A, const SimPV &sb, q4,
+                                 f3) {
+                if (!own) return;
+                const f3 dp = (sb.P - A) - f.P;
+                const f3 dv = sb.V - f.V;
+                const float x = dot3(dp, dp);
+                e_pos += x;
+                if (hw->leaf[i]) e_ee += x;
+                dc = dc + hw->massw[i] * dp;
+                e_vel += dot3(dv, dv);
+            });
+        } else {
+            walk_half<SimMul>(hw, rec, alpha, [&](int b) { return load_mul(a, b, e); },
+                              [&](int i, int b, int own, const Frame &f, f3 A, const SimMul &sb,
+                                  q4 qr, f3 wr) {
+                if (own) me.add(b, hw->leaf[i], hw->massw[i], f, A, sb, qr, wr);
+            });
+        }
     }
     // both halves' sums (a + b in one thread, b + a in the other: the same bits)
-    part[0][tid] = e_pos;
-    part[1][tid] = e_ee;
-    part[2][tid] = e_vel;
-    part[3][tid] = dc.x;
-    part[4][tid] = dc.y;
-    part[5][tid] = dc.z;
-    __syncthreads();
     const int o = tid ^ 64;
-    e_pos += part[0][o];
-    e_ee += part[1][o];
-    e_vel += part[2][o];
-    dc.x += part[3][o];
-    dc.y += part[4][o];
-    dc.z += part[5][o];
+    float r;
+    if constexpr (!MUL) {
+        part[0][tid] = e_pos;
+        part[1][tid] = e_ee;
+        part[2][tid] = e_vel;
+        part[3][tid] = dc.x;
+        part[4][tid] = dc.y;
+        part[5][tid] = dc.z;
+        __syncthreads();
+        e_pos += part[0][o];
+        e_ee += part[1][o];
+        e_vel += part[2][o];
+        dc.x += part[3][o];
+        dc.y += part[4][o];
+        dc.z += part[5][o];
+        const float e_com = dot3(dc, dc);
+        r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
+            a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
+    } else {
+        part[0][tid] = me.jrot;
+        part[1][tid] = me.jvel;
+        part[2][tid] = me.eepos;
+        part[3][tid] = me.eerot;
+        part[4][tid] = me.dc.x;
+        part[5][tid] = me.dc.y;
+        part[6][tid] = me.dc.z;
+        __syncthreads();
+        me.jrot += part[0][o];
+        me.jvel += part[1][o];
+        me.eepos += part[2][o];
+        me.eerot += part[3][o];
+        me.dc.x += part[4][o];
+        me.dc.y += part[5][o];
+        me.dc.z += part[6][o];
+        r = me.reward(a);
+    }
     if (!active) return;
-
-    const float e_com = dot3(dc, dc);
-    const float r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
-                    a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
     const float z_root = a.pos[2 * ld + e];
     const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
 
@@ -620,14 +724,17 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
     }
     // 5. observation of the post-reset state: a reset env's rows come from the
     //    reference state written in the same walk, others from the sim state
-    if (done) rsi_obs_half(a, hw, e, k_out, ph_out);
-    else obs_half_from_sim(a, hw, e);
+    Heading h;
+    if (done) {
+        h = rsi_obs_half(a, hw, e, k_out, ph_out);
+    } else {
+        h = sim_heading(a, e);
+        obs_half_from_sim(a, hw, e, h);
+    }
+    // future frames j = hf, hf + 2, ...; the previous action in the second half
+    if (a.obs_future > 0 || a.obs_prev)
+        obs_extras(a, e, k_out, ph_out, done, h, hf, 2, a.obs_prev && hf == 1);
 }
-
-struct SimMul {
-    f3 P, W, Wp;
-    q4 Q, Qp;   // the body's and its parent's orientation
-};
 
 // The fused step, one thread per env (large batches and the training terms).
 // MUL: the multiplicative reward.
@@ -685,46 +792,13 @@ __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
             r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
                 a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
         } else {
-            // the sim's joint rotations and joint angular velocities in the
-            // parent frame need the parent's orientation and angular velocity
-            float e_jrot = 0.0f, e_jvel = 0.0f, e_eepos = 0.0f, e_eerot = 0.0f;
-            f3 dc = mk3(0.0f, 0.0f, 0.0f);
-            auto load_m = [&](int b) {
-                SimMul s;
-                s.P = ld3(a.pos, b, ld, e);
-                s.Q = ld4(a.quat, b, ld, e);
-                s.W = ld3(a.angvel, b, ld, e);
-                const int p = b > 0 ? sk->pbody[b] : 0;
-                s.Qp = ld4(a.quat, p, ld, e);
-                s.Wp = ld3(a.angvel, p, ld, e);
-                return s;
-            };
-            walk_prefetch<SimMul>(sk, rec, alpha, load_m,
-                                  [&](int i, int, const Frame &f, f3 A, const SimMul &sb, q4 qr,
+            MulErr me;
+            walk_prefetch<SimMul>(sk, rec, alpha, [&](int b) { return load_mul(a, b, e); },
+                                  [&](int i, int b, const Frame &f, f3 A, const SimMul &sb, q4 qr,
                                       f3 wr) {
-                q4 ql = sb.Q;
-                f3 wl = sb.W;
-                if (i > 0) {
-                    const q4 ip = qconj(sb.Qp);
-                    ql = qmul(ip, sb.Q);
-                    wl = qrot(ip, sb.W - sb.Wp);
-                }
-                const float th = qangle(qmul(qconj(qr), ql));
-                e_jrot += th * th;
-                const f3 dw = wl - wr;
-                e_jvel += dot3(dw, dw);
-                const f3 dp = (sb.P - A) - f.P;
-                dc = dc + sk->massw[i] * dp;
-                if (sk->leaf[i]) {
-                    e_eepos += dot3(dp, dp);
-                    const float te = qangle(qmul(qconj(f.Q), sb.Q));
-                    e_eerot += te * te;
-                }
+                me.add(b, sk->leaf[i], sk->massw[i], f, A, sb, qr, wr);
             });
-            const float e_com = dot3(dc, dc);
-            // the product of the five exponentials, as one
-            r = expf(-(a.m_jrot * e_jrot + a.m_jvel * e_jvel + a.m_com * e_com +
-                       a.m_eepos * e_eepos + a.m_eerot * e_eerot));
+            r = me.reward(a);
         }
         const float z_root = a.pos[2 * ld + e];
         const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
@@ -755,7 +829,8 @@ __global__ __launch_bounds__(256) void env_step_kernel(EnvArgs a)
     //    reference state it may have just written is read back in order)
     if (active) {
         obs_from_sim(a, e, ph_out);
-        obs_extras(a, e, k_fin, ph_out, reset);
+        if (a.obs_future > 0 || a.obs_prev)
+            obs_extras(a, e, k_fin, ph_out, reset, sim_heading(a, e), 0, 1, a.obs_prev != 0);
     }
 }
 
@@ -773,7 +848,8 @@ __global__ __launch_bounds__(256) void reset_kernel(EnvArgs a)
     a.env_phase[e] = ph;
     a.env_t[e] = 0;
     obs_from_sim(a, e, ph);
-    obs_extras(a, e, k, ph, true);
+    if (a.obs_future > 0 || a.obs_prev)
+        obs_extras(a, e, k, ph, true, sim_heading(a, e), 0, 1, a.obs_prev != 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -1035,15 +1111,17 @@ static hipError_t launch_env(void (*k)(EnvArgs), int n_slots, int frame_floats,
 hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s)
 {
     if (a.n <= 0) return hipSuccess;
-    // the two-thread kernel covers the grouped reward and the 15 B + 1 observation
-    if (a.reward_form == IM_REWARD_MULTIPLICATIVE)
-        return launch_env(env_step_kernel<true>, n_slots, 13, a, s);
-    if (a.n > SPLIT_ENV_MAX || a.obs_future > 0 || a.obs_prev)
-        return launch_env(env_step_kernel<false>, n_slots, 13, a, s);
-    // two threads per env: 128 envs per 256-thread block
+    const bool mul = a.reward_form == IM_REWARD_MULTIPLICATIVE;
+    if (a.n > SPLIT_ENV_MAX)
+        return launch_env(mul ? env_step_kernel<true> : env_step_kernel<false>, n_slots, 13, a, s);
+    // two threads per env: 128 envs per 256-thread block; the future-frame
+    // walks of the observation go over the whole skeleton (n_slots)
     const int bs = 256;
-    const size_t lds = (size_t)(half_slots > 0 ? half_slots : 1) * 13 * sizeof(float) * bs;
-    hipLaunchKernelGGL(env_step_split_kernel, dim3((unsigned)((a.n + 127) / 128)), dim3(bs), lds, s, a);
+    int slots = half_slots;
+    if (a.obs_future > 0 && n_slots > slots) slots = n_slots;
+    const size_t lds = (size_t)(slots > 0 ? slots : 1) * 13 * sizeof(float) * bs;
+    hipLaunchKernelGGL(mul ? env_step_split_kernel<true> : env_step_split_kernel<false>,
+                       dim3((unsigned)((a.n + 127) / 128)), dim3(bs), lds, s, a);
     return hipGetLastError();
 }
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s)

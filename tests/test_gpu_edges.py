@@ -63,7 +63,7 @@ def test_zero_envs_touch_nothing(cfg):
     assert (mean == SENTINEL_F).all() and (act == SENTINEL_F).all() and (logp == SENTINEL_F).all()
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
+@pytest.mark.parametrize("cfg", [2, 3, 6])
 def test_leading_dimension_tail_untouched_and_results_unchanged(cfg):
     N, T = 1000, 3
     d, w, ctx, a = _setup(cfg, N)                       # ld = N
@@ -77,6 +77,8 @@ def test_leading_dimension_tail_untouched_and_results_unchanged(cfg):
         mean = torch.full((N, A), SENTINEL_F, device="cuda")
         act = mean.clone()
         logp = torch.full((N,), SENTINEL_F, device="cuda")
+        if bufs.prev_action is not None:
+            bufs.prev_action = act           # the observation's previous action
         for t in range(T):
             ctx.policy_act(bufs.obs, bufs.env_n, N, mean, act, logp)
             ctx.standin_physics(bufs, d["sigma_joint"], d["sigma_vel"])
@@ -94,12 +96,12 @@ def test_leading_dimension_tail_untouched_and_results_unchanged(cfg):
         assert torch.equal(outs["a"][i], outs["b"][i]), "policy output differs with ld_obs > n_envs"
 
 
-@pytest.mark.parametrize("cfg", [2, 5])
+@pytest.mark.parametrize("cfg", [2, 5, 6])
 def test_partial_mask_reset(cfg):
     N = 1500
     d, w, ctx, bufs = _setup(cfg, N)
     rng = np.random.default_rng(cfg)
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     for _ in range(3):                       # a state away from the initial reset
         w.standin(st, d["sigma_joint"], d["sigma_vel"])
@@ -128,7 +130,7 @@ def test_truncation_at_the_phase_boundary(cfg):
     N = 512
     d, w, ctx, bufs = _setup(cfg, N)
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     # phases within a few ulp of 1 - dphi, where phi + dphi crosses 1.0f; dphi as the
     # clip's per-step phase increment, rounded once to fp32
@@ -161,19 +163,21 @@ def test_truncation_at_the_phase_boundary(cfg):
     assert 0 < expect.sum() < N
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
+@pytest.mark.parametrize("cfg", [2, 4, 6])
 def test_non_finite_sim_state_terminates_and_resets(cfg):
     N = 700
-    d, w, ctx, bufs = _setup(cfg, N)
+    d, w, ctx, bufs = _setup(cfg, N, grace=0)      # terminations count from the first step
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     w.standin(st, d["sigma_joint"], d["sigma_vel"])
     bad = np.zeros(N, bool)
     bad[5::37] = True
     idx = np.flatnonzero(bad)
     st.pos[3, 1, idx[0::3]] = np.nan
-    st.linvel[2, 0, idx[1::3]] = np.nan
+    # a velocity the reward reads: linear (grouped form) or angular (multiplicative)
+    vel = st.angvel if c["reward_form"] == 1 else st.linvel
+    vel[2, 0, idx[1::3]] = np.nan
     st.pos[0, 2, idx[2::3]] = np.nan
     H.upload_state(st, bufs)
     t_next = st.t + 1
@@ -194,7 +198,7 @@ def test_grace_period_and_fall_height():
     N, grace = 600, 4
     d, w, ctx, bufs = _setup(2, N, grace=grace, h_term=5.0)   # every root is "below" 5 m
     c = d["config"]
-    st = oracle.State(w.B, N)
+    st = w.state(N)
     w.reset_envs(st)
     H.upload_state(st, bufs)
     live = np.ones(N, bool)

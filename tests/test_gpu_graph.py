@@ -34,7 +34,7 @@ def _equal(a, b):
     return all(torch.equal(a[k], b[k]) for k in a)
 
 
-@pytest.mark.parametrize("cfg,N", [(1, 64), (2, 1000), (3, 5000), (4, 20000)])
+@pytest.mark.parametrize("cfg,N", [(1, 64), (2, 1000), (3, 5000), (4, 20000), (6, 3000)])
 def test_graph_replay_matches_eager(cfg, N):
     d = synth.make_world(cfg, n_envs=N)
     ctx = binding.Context(d, max_envs=N)
@@ -44,6 +44,8 @@ def test_graph_replay_matches_eager(cfg, N):
     act = torch.zeros((N, A), device="cuda")
     logp = torch.zeros(N, device="cuda")
     extra = (mean, act, logp)
+    if bufs.prev_action is not None:
+        bufs.prev_action = act               # the observation's previous action
     T = 3
 
     def rollout():

@@ -126,7 +126,7 @@ def test_policy_parity(cfg):
     assert np.abs(zg - zo).max() < 1e-3
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
+@pytest.mark.parametrize("cfg", [2, 4, 6])
 def test_env_step_parity_large_batch_kernel(cfg):
     # above 32768 envs the fused step runs one thread per env (below, two);
     # a ragged size so that its last block is partly empty
@@ -141,10 +141,14 @@ def test_env_step_parity_large_batch_kernel(cfg):
     for t in range(T):
         w.standin(st, d["sigma_joint"], d["sigma_vel"])
         H.upload_state(st, bufs, env=False)
+        prev = None
+        if bufs.prev_action is not None:
+            prev = RNG.normal(size=(N, w.A)).astype(np.float32)
+            bufs.prev_action[:N].copy_(torch.from_numpy(prev))
         t_next = st.t + 1
         z_root = st.pos[0, 2].copy()
         ctx.env_step_fused(bufs)
-        w.env_step(st)
+        w.env_step(st, prev_action=prev)
         g = H.download(bufs, N)
         live = H.compare_step(g, st, c["r_min"], c["h_term"], c["grace"], t_next, z_root, live)
         H.compare_sim_obs(g, st, live, "step %d" % t)
