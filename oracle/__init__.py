@@ -329,3 +329,22 @@ def policy(pol, seed, obs, env_n, idx=None):
                     np.ascontiguousarray(env_n, np.uint32), idx_a,
                     0 if idx_a is None else len(idx_a), mean, action, logp)
     return mean, action, logp
+
+
+def value(critic, obs, idx=None):
+    """Oracle value head: the critic MLP (same layer rules as the policy: ReLU
+    hidden layers, bf16 rounding of the input and hidden activations for bf16
+    critics, linear last layer of width 1) evaluated by the policy forward
+    above with a zero log-std; the sampled part is discarded.
+
+    critic: dict like synth.make_policy with dims[-1] == 1; obs: [D][N] float32.
+    Returns value [N] float32 (entries outside idx are zero)."""
+    assert critic["dims"][-1] == 1
+    c = dict(critic)
+    c["log_std"] = np.zeros(1, np.float32)
+    N = np.asarray(obs).shape[1]
+    mean, _, _ = policy(c, 0, obs, np.zeros(N, np.uint32), idx=idx)
+    return mean[:, 0].copy()
+
+
+from .rollout import gae, rollout_summary, SUMMARY_FIELDS  # noqa: E402

@@ -240,7 +240,7 @@ def make_world(cfg_id, n_envs=None, **cfg_over):
     """Everything both implementations need for workload `cfg_id`."""
     spec = dict(CONFIGS[cfg_id])
     ss = np.random.SeedSequence(cfg_id).spawn(4)
-    r_skel, r_clip, r_pol = (np.random.default_rng(s) for s in ss[:3])
+    r_skel, r_clip, r_pol, r_crit = (np.random.default_rng(s) for s in ss)
     skel = skeleton_s15(r_skel) if spec["skeleton"] == "S15" else skeleton_s24(r_skel)
     if spec["frames"] == "16x60-300":
         frames = [int(f) for f in r_clip.integers(60, 301, size=16)]
@@ -248,6 +248,8 @@ def make_world(cfg_id, n_envs=None, **cfg_over):
         frames = list(spec["frames"])
     clips = [make_clip(r_clip, skel, F) for F in frames]
     pol = make_policy(r_pol, spec["mlp"], spec["bf16"])
+    # value head: the policy's hidden widths, one output
+    critic = make_policy(r_crit, list(spec["mlp"][:-1]) + [1], spec["bf16"])
     cfg = step_config(cfg_id, **cfg_over)
     return dict(
         id=cfg_id,
@@ -256,7 +258,29 @@ def make_world(cfg_id, n_envs=None, **cfg_over):
         skeleton=skel,
         clips=clips,
         policy=pol,
+        critic=critic,
         config=cfg,
         sigma_joint=float(spec["sigma_joint"]),
         sigma_vel=float(spec.get("sigma_vel", 0.5)),
     )
+
+
+# PPO rollout-end parameters: discount and GAE lambda (baseline column of the
+# backflip configuration table)
+GAMMA, LAMBDA = 0.99, 0.95
+
+
+def rollout_inputs(seed, T, N, p_term=0.04, p_trunc=0.02):
+    """Seeded stand-ins for a rollout's stored rewards, flags and values:
+    reward U(0, 1), terminated / truncated Bernoulli(p_term / p_trunc) (both
+    may be set), values N(0, 2^2) for the T + 1 observations, running-episode
+    return U(0, 5) and length 0..49 from earlier rollouts."""
+    rng = np.random.default_rng(np.random.SeedSequence([2609, seed]))
+    reward = rng.uniform(0.0, 1.0, size=(T, N)).astype(np.float32)
+    term = (rng.random((T, N)) < p_term).astype(np.uint8)
+    trunc = (rng.random((T, N)) < p_trunc).astype(np.uint8)
+    value = (2.0 * rng.standard_normal((T + 1, N))).astype(np.float32)
+    ep_return = rng.uniform(0.0, 5.0, size=N).astype(np.float32)
+    ep_length = rng.integers(0, 50, size=N).astype(np.int32)
+    return dict(reward=reward, term=term, trunc=trunc, value=value, ep_return=ep_return,
+                ep_length=ep_length)
