@@ -1,7 +1,7 @@
 """Throughput of the environment-plus-policy step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
-                    [--no-cpu-baseline] [--no-secondary] [--no-graph]
+                    [--no-cpu-baseline] [--no-secondary] [--no-graph] [--no-rollout]
 
 One step = im_policy_act (MLP forward + Gaussian sampling) followed by
 im_env_step_fused (reference sampling, FK, reward, termination, masked reset,
@@ -20,8 +20,10 @@ dominant call, MFMA-bound),
 work (FLOPs / bytes) over the mean duration measured with HIP events on the
 launch stream during the timed loop.  `traffic` is the HBM bytes per launch
 measured with the profiler's byte counters on the same kernels (null when the
-kernel sources changed since).  `cpu_baseline` times the CPU oracle on a
-bounded sample of the same workload.
+kernel sources changed since).  `rollout` times a whole PPO rollout of the
+workload (policy, value head and env step per step written in place into the
+rollout storage, then GAE and the rollout summaries).  `cpu_baseline` times
+the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
 import hashlib
@@ -215,6 +217,101 @@ def run_gpu(wid, steps, warmup, graph=True):
     )
 
 
+def run_rollout(wid, reps=2):
+    """A whole PPO rollout of the workload (T = its step count) written in
+    place into the rollout storage: per step policy_act, value and
+    env_step_fused, then the value of the last observation, GAE with the
+    rollout summaries and the copy of the last observation into slot 0 for the
+    next rollout.  The stand-in physics is recorded beforehand and excluded,
+    as in the step benchmark; each timed rollout starts from the same state."""
+    import torch
+    from paper_2609_09821_amd import binding, synth
+
+    desc = synth.make_world(wid)
+    N = desc["n_envs"]
+    T = int(desc["spec"]["steps"])
+    ctx = binding.Context(desc, max_envs=N)
+    bufs = ctx.buffers(N)
+    ro = binding.RolloutStorage(ctx, N, T)
+    stream = torch.cuda.current_stream()
+    bufs.obs = ro.obs[0]
+    ctx.reset_envs(bufs)
+    init = {k: getattr(bufs, k).clone() for k in binding.EnvBuffers.ENV}
+    init_obs = ro.obs[0].clone()
+    rec = []
+    for t in range(T):
+        ctx.standin_physics(bufs, desc["sigma_joint"], desc["sigma_vel"])
+        rec.append(tuple(getattr(bufs, k).clone() for k in binding.EnvBuffers.SIM))
+        ro.env_bufs(bufs, t)
+        ctx.env_step_fused(bufs, with_ref_frame=False)
+    pristine = [tuple(x.clone() for x in r) for r in rec]
+
+    def restore():
+        for k, v in init.items():
+            getattr(bufs, k).copy_(v)
+        ro.obs[0].copy_(init_obs)
+        ro.ep_return.zero_()
+        ro.ep_length.zero_()
+        for r, p in zip(rec, pristine):
+            for dst, src in zip(r, p):
+                dst.copy_(src)
+        torch.cuda.synchronize()
+
+    def one(ev=None):
+        for t in range(T):
+            bufs.body_pos, bufs.body_quat, bufs.body_linvel, bufs.body_angvel = rec[t]
+            if ev is not None:
+                ev[t][0].record(stream)
+            ctx.policy_act(ro.obs[t], bufs.env_n, N, ro.mean[t], ro.action[t], ro.logp[t],
+                           stream=stream)
+            if ev is not None:
+                ev[t][1].record(stream)
+            ctx.value(ro.obs[t], N, ro.value[t], stream=stream)
+            if ev is not None:
+                ev[t][2].record(stream)
+            ro.env_bufs(bufs, t)
+            ctx.env_step_fused(bufs, stream=stream, with_ref_frame=False)
+            if ev is not None:
+                ev[t][3].record(stream)
+        ctx.value(ro.obs[T], N, ro.value[T], stream=stream)
+        if ev is not None:
+            ev[T][0].record(stream)
+        ctx.gae(ro, synth.GAMMA, synth.LAMBDA, stream=stream)
+        if ev is not None:
+            ev[T][1].record(stream)
+        ro.obs[0].copy_(ro.obs[T])
+
+    restore()
+    one()                                   # warm-up
+    walls, pol, val, env, gae = [], [], [], [], []
+    for _ in range(reps):
+        restore()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(T + 1)]
+        t0 = time.perf_counter()
+        one(ev)
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        pol.append(np.mean([ev[t][0].elapsed_time(ev[t][1]) for t in range(T)]))
+        val.append(np.mean([ev[t][1].elapsed_time(ev[t][2]) for t in range(T)]))
+        env.append(np.mean([ev[t][2].elapsed_time(ev[t][3]) for t in range(T)]))
+        gae.append(ev[T][0].elapsed_time(ev[T][1]))
+    summ = ro.summary.cpu().numpy()
+    ctx.close()
+    wall = float(np.min(walls))
+    return {
+        "workload": desc["spec"]["name"], "n_envs": N, "T": T,
+        "value": N * T / wall, "unit": "env-steps/s", "ms_per_rollout": wall * 1e3,
+        "policy_us_per_step": float(np.mean(pol)) * 1e3,
+        "value_us_per_step": float(np.mean(val)) * 1e3,
+        "env_step_us_per_step": float(np.mean(env)) * 1e3,
+        "gae_summary_us": float(np.mean(gae)) * 1e3,
+        "episodes_ended": int(summ[3]), "mean_reward": float(summ[0] / (N * T)),
+        "note": "policy_act + value + env_step_fused per step into the rollout storage, value of "
+                "the last observation, GAE + summaries, last observation to slot 0; stand-in "
+                "physics excluded; best of %d rollouts" % reps,
+    }
+
+
 def cpu_baseline(wid, target_s=16.0):
     """The oracle, as it stands, on a bounded sample of workload `wid`."""
     import oracle
@@ -269,6 +366,7 @@ def main():
     ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-rollout", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay of the timed steps")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
@@ -353,6 +451,8 @@ def main():
             "ms_per_step": s["wall"] * 1e3 / args.steps, "policy_ms": s["pol_ms"],
             "env_step_ms": s["env_ms"], "graph_value": s["graph_value"],
             "graph_ms_per_step": s["graph_ms"]}]
+    if not args.no_rollout:
+        out["rollout"] = run_rollout(args.workload)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload)
     print(json.dumps(out), flush=True)

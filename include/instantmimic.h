@@ -274,6 +274,87 @@ im_status im_reset_envs(im_ctx *ctx, const im_env_bufs *bufs, const uint8_t *mas
 im_status im_standin_physics(im_ctx *ctx, const im_env_bufs *bufs, float sigma_joint,
                              float sigma_vel, void *stream);
 
+/*
+ * Value head for the PPO rollout (Fig. 3: the rollout storage feeds the
+ * policy update): a critic MLP laid out like im_policy with dims[0] = D,
+ * dims[L] = 1, ReLU hidden layers, linear output and the policy's dtype (the
+ * same bf16 rounding points); log_std is not used and may be NULL.  Copied
+ * to the device; a second call replaces the critic.  Not hot: allocates, and
+ * synchronises the device; no call on the context may be in flight.
+ */
+im_status im_set_critic(im_ctx *ctx, const im_policy *critic);
+
+/*
+ * value[e] = V(obs[:, e]) for e < n_envs: obs [D][ld_obs] float (device),
+ * value [n_envs] float (device).  Needs im_set_critic.  Shares the policy's
+ * workspace: calls on one context must be ordered (same stream or
+ * synchronised).
+ */
+im_status im_value(im_ctx *ctx, const float *obs, int64_t ld_obs, int64_t n_envs, float *value,
+                   void *stream);
+
+/* Fields of the rollout summary (float64, device). */
+enum {
+    IM_SUM_REWARD = 0,          /* sum of rewards over steps and envs */
+    IM_SUM_TERMINATED,          /* terminated steps */
+    IM_SUM_TRUNCATED,           /* truncated steps */
+    IM_SUM_EPISODES,            /* episodes ended (terminated or truncated) */
+    IM_SUM_EPISODE_RETURN,      /* sum of the returns of the ended episodes */
+    IM_SUM_EPISODE_LENGTH,      /* sum of their lengths in steps */
+    IM_SUM_ADVANTAGE,           /* sum of the stored advantages */
+    IM_SUM_ADVANTAGE_SQ,        /* sum of their squares */
+    IM_SUM_VALUE,               /* sum of V_t, t < T */
+    IM_SUM_RETURN,              /* sum of the stored returns */
+    IM_SUMMARY_FIELDS
+};
+
+/*
+ * Rollout storage (device, caller-owned).  The step writes into it in place:
+ * step t reads obs slot t and writes action/logp/value slot t, and the fused
+ * env step writes reward/terminated/truncated slot t and obs slot t+1, so
+ * storing a step copies nothing (Fig. 3 storage write).  [T][ld] arrays have
+ * the env fastest.
+ *   reward [T][ld] float, terminated / truncated [T][ld] uint8
+ *   value [T+1][ld] float: V of the observation of each step, slot T the
+ *         observation after the last step
+ *   advantage, ret [T][ld] float: written
+ *   ep_return [ld] float, ep_length [ld] int32: return and length of the
+ *         episode each env is in, carried across rollouts (read/write; used
+ *         with summary only)
+ *   summary [IM_SUMMARY_FIELDS] double or NULL: written
+ */
+typedef struct {
+    int32_t T;
+    int64_t n_envs, ld;
+    float gamma, lambda;
+    const float *reward;
+    const uint8_t *terminated;
+    const uint8_t *truncated;
+    const float *value;
+    float *advantage;
+    float *ret;
+    float *ep_return;
+    int32_t *ep_length;
+    double *summary;
+} im_rollout;
+
+/*
+ * Generalized advantage estimation over the rollout storage (Schulman et al.
+ * 2016; gamma and lambda from the configuration table of the Appendix):
+ *   delta_t = r_t + gamma * next_t - V_t, next_t = 0 if terminated, V_t if
+ *             truncated only (cut off, not failed: the next observation is
+ *             already the reset one, so the step's own value stands in),
+ *             V_{t+1} otherwise;
+ *   A_t = delta_t + gamma * lambda * A_{t+1}, the sum stopping at an episode
+ *         end (terminated or truncated) and after step T-1; R_t = A_t + V_t.
+ * Computed in float64, stored as float32.  With summary: the rollout
+ * summaries (IM_SUM_*); at every step the reward is added to ep_return
+ * (float32) and ep_length grows by one, an ended episode enters the sums and
+ * restarts at 0.  Sums are in float64 in a fixed order (results do not depend
+ * on timing).  1 <= T, 0 <= n_envs <= max_envs, ld >= n_envs.
+ */
+im_status im_gae(im_ctx *ctx, const im_rollout *r, void *stream);
+
 const char *im_status_str(im_status s);
 const char *im_last_error(void);
 

@@ -59,6 +59,20 @@ class ImEnvBufs(C.Structure):
                 ("prev_action", C.c_void_p)]
 
 
+class ImRollout(C.Structure):
+    _fields_ = [("T", C.c_int32), ("n_envs", C.c_int64), ("ld", C.c_int64), ("gamma", C.c_float),
+                ("lam", C.c_float), ("reward", C.c_void_p), ("terminated", C.c_void_p),
+                ("truncated", C.c_void_p), ("value", C.c_void_p), ("advantage", C.c_void_p),
+                ("ret", C.c_void_p), ("ep_return", C.c_void_p), ("ep_length", C.c_void_p),
+                ("summary", C.c_void_p)]
+
+
+# fields of the rollout summary (IM_SUM_* order)
+SUMMARY_FIELDS = ("reward_sum", "n_terminated", "n_truncated", "n_episodes",
+                  "episode_return_sum", "episode_length_sum", "advantage_sum",
+                  "advantage_sq_sum", "value_sum", "return_sum")
+
+
 class ImInfo(C.Structure):
     _fields_ = [("n_bodies", C.c_int32), ("obs_dim", C.c_int32), ("action_dim", C.c_int32),
                 ("n_clips", C.c_int32), ("n_layers", C.c_int32), ("policy_dtype", C.c_int32),
@@ -66,7 +80,8 @@ class ImInfo(C.Structure):
 
 
 EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_policy_act",
-            "im_reset_envs", "im_standin_physics", "im_status_str", "im_last_error"]
+            "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value", "im_gae",
+            "im_status_str", "im_last_error"]
 
 _lib = None
 
@@ -98,6 +113,12 @@ def lib():
     L.im_standin_physics.argtypes = [C.c_void_p, C.POINTER(ImEnvBufs), C.c_float, C.c_float,
                                      C.c_void_p]
     L.im_standin_physics.restype = st
+    L.im_set_critic.argtypes = [C.c_void_p, C.POINTER(ImPolicy)]
+    L.im_set_critic.restype = st
+    L.im_value.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p]
+    L.im_value.restype = st
+    L.im_gae.argtypes = [C.c_void_p, C.POINTER(ImRollout), C.c_void_p]
+    L.im_gae.restype = st
     L.im_status_str.argtypes = [C.c_int]
     L.im_status_str.restype = C.c_char_p
     L.im_last_error.argtypes = []
@@ -152,6 +173,18 @@ def im_reset_envs(ctx, bufs, mask_ptr=None, stream=None):
 def im_standin_physics(ctx, bufs, sigma_joint, sigma_vel, stream=None):
     _check(lib().im_standin_physics(ctx, C.byref(bufs), float(sigma_joint), float(sigma_vel),
                                     stream))
+
+
+def im_set_critic(ctx, critic):
+    _check(lib().im_set_critic(ctx, C.byref(critic)))
+
+
+def im_value(ctx, obs_ptr, ld_obs, n_envs, value_ptr, stream=None):
+    _check(lib().im_value(ctx, obs_ptr, int(ld_obs), int(n_envs), value_ptr, stream))
+
+
+def im_gae(ctx, rollout, stream=None):
+    _check(lib().im_gae(ctx, C.byref(rollout), stream))
 
 
 # ------------------------------------------------------------- conveniences
@@ -253,22 +286,35 @@ class Description:
                             _ptr(k(_f32(c["local_quat"])), C.c_float))
         self.clips = arr
         self.n_clips = len(clips)
-        L = len(pol["W"])
-        dims = k(_i32(pol["dims"]))
-        bf16 = bool(pol["bf16"])
+        self.policy = self._mlp(pol)
+        self.critic = self._mlp(desc["critic"]) if desc.get("critic") is not None else None
+
+    def _mlp(self, net):
+        """ImPolicy of an MLP description (weights and biases kept alive here)."""
+        keep = self._keep
+        L = len(net["W"])
+        dims = _i32(net["dims"])
+        keep.append(dims)
+        bf16 = bool(net["bf16"])
         wptrs = (C.c_void_p * L)()
         bptrs = (C.POINTER(C.c_float) * L)()
         for l in range(L):
-            w = _f32(pol["W"][l])
+            w = _f32(net["W"][l])
             if bf16:
-                w = k(np.ascontiguousarray((w.view(np.uint32) >> 16).astype(np.uint16)))
-            else:
-                w = k(w)
+                w = np.ascontiguousarray((w.view(np.uint32) >> 16).astype(np.uint16))
+            keep.append(w)
             wptrs[l] = w.ctypes.data
-            bptrs[l] = _ptr(k(_f32(pol["b"][l])), C.c_float)
-        self.weight_ptrs, self.bias_ptrs = wptrs, bptrs
-        self.policy = ImPolicy(L, _ptr(dims, C.c_int32), IM_DTYPE_BF16 if bf16 else IM_DTYPE_F32,
-                               wptrs, bptrs, _ptr(k(_f32(pol["log_std"])), C.c_float))
+            b = _f32(net["b"][l])
+            keep.append(b)
+            bptrs[l] = _ptr(b, C.c_float)
+        keep += [wptrs, bptrs]
+        log_std = net.get("log_std")
+        ls = None
+        if log_std is not None:
+            ls = _f32(log_std)
+            keep.append(ls)
+        return ImPolicy(L, _ptr(dims, C.c_int32), IM_DTYPE_BF16 if bf16 else IM_DTYPE_F32,
+                        wptrs, bptrs, None if ls is None else _ptr(ls, C.c_float))
 
     def create_status(self, max_envs):
         """Raw im_create: (status, context pointer or None)."""
@@ -281,9 +327,11 @@ class Description:
 class Context:
     """A library context built from a synthetic world description."""
 
-    def __init__(self, desc, max_envs):
+    def __init__(self, desc, max_envs, critic=True):
         d = self.desc = Description(desc)
         self.ptr = im_create(d.cfg, d.skel, d.clips, d.n_clips, d.policy, max_envs)
+        if critic and d.critic is not None:
+            im_set_critic(self.ptr, d.critic)
         self.info = im_get_info(self.ptr)
 
     def close(self):
@@ -315,3 +363,57 @@ class Context:
     def policy_act(self, obs, env_n, n_envs, mean, action, logp=None, stream=None):
         im_policy_act(self.ptr, _dptr(obs), obs.shape[1], _dptr(env_n), n_envs, _dptr(mean),
                       _dptr(action), _dptr(logp), _stream(stream))
+
+    def value(self, obs, n_envs, value, stream=None):
+        im_value(self.ptr, _dptr(obs), obs.shape[1], n_envs, _dptr(value), _stream(stream))
+
+    def gae(self, ro, gamma, lam, summary=True, stream=None):
+        """GAE (and, with summary, the rollout summaries) over a RolloutStorage."""
+        im_gae(self.ptr, ro.struct(gamma, lam, summary), _stream(stream))
+
+
+class RolloutStorage:
+    """Device storage of a T-step rollout, written in place by the step calls:
+    step t's policy and value read obs[t] and write action/mean/logp/value
+    slot t; the fused env step writes reward/terminated/truncated slot t and
+    obs[t + 1].  `env_bufs(t)` points an EnvBuffers at those slots."""
+
+    def __init__(self, ctx, n_envs, T, ld=None, device="cuda"):
+        import torch
+        ld = int(ld if ld is not None else n_envs)
+        D, A = ctx.info.obs_dim, ctx.info.action_dim
+        self.T, self.n_envs, self.ld = int(T), int(n_envs), ld
+        f = dict(device=device, dtype=torch.float32)
+        u8 = dict(device=device, dtype=torch.uint8)
+        self.obs = torch.zeros((T + 1, D, ld), **f)
+        self.mean = torch.zeros((T, max(n_envs, 1), A), **f)
+        self.action = torch.zeros((T, max(n_envs, 1), A), **f)
+        self.logp = torch.zeros((T, ld), **f)
+        self.value = torch.zeros((T + 1, ld), **f)
+        self.reward = torch.zeros((T, ld), **f)
+        self.terminated = torch.zeros((T, ld), **u8)
+        self.truncated = torch.zeros((T, ld), **u8)
+        self.advantage = torch.zeros((T, ld), **f)
+        self.ret = torch.zeros((T, ld), **f)
+        self.ep_return = torch.zeros(ld, **f)
+        self.ep_length = torch.zeros(ld, device=device, dtype=torch.int32)
+        self.summary = torch.zeros(len(SUMMARY_FIELDS), device=device, dtype=torch.float64)
+
+    def env_bufs(self, bufs, t):
+        """`bufs` (sim and env state) with its step outputs pointed at slot t."""
+        assert bufs.ld == self.ld and bufs.n_envs == self.n_envs
+        bufs.reward = self.reward[t]
+        bufs.terminated = self.terminated[t]
+        bufs.truncated = self.truncated[t]
+        bufs.obs = self.obs[t + 1]
+        if bufs.prev_action is not None:
+            bufs.prev_action = self.action[t]
+        return bufs
+
+    def struct(self, gamma, lam, summary=True):
+        return ImRollout(self.T, self.n_envs, self.ld, float(gamma), float(lam),
+                         self.reward.data_ptr(), self.terminated.data_ptr(),
+                         self.truncated.data_ptr(), self.value.data_ptr(),
+                         self.advantage.data_ptr(), self.ret.data_ptr(),
+                         self.ep_return.data_ptr(), self.ep_length.data_ptr(),
+                         self.summary.data_ptr() if summary else None)

@@ -35,8 +35,22 @@ struct im_ctx {
     float *d_log_std = nullptr;
     void *d_ws[2] = {nullptr, nullptr};
     void *d_obs16 = nullptr;   // bf16 [max_envs][K_pad[0]] staging of the observation
+    size_t ws_bytes[2] = {0, 0};
     int n_cu = 0;              // compute units of the context's device
     int64_t device_bytes = 0;
+    // value head (im_set_critic): hidden layers packed like the policy's,
+    // the last layer as an fp32 vector
+    struct {
+        int L = 0;   // 0: no critic
+        std::vector<int> dims, M_pad, K_pad;
+        std::vector<void *> d_w;
+        std::vector<float *> d_b;
+        float *d_head = nullptr;   // [K_head] last-layer weights, zero-padded
+        float head_bias = 0.0f;
+        int K_head = 0;            // D for a one-layer critic, else M_pad[L-2]
+        int64_t bytes = 0;         // device memory of the above
+    } critic;
+    double *d_partial = nullptr;   // per-block summary sums, [ceil(max_envs/256)][fields]
 };
 
 namespace {
@@ -65,9 +79,25 @@ bool unit_quat(const float *q, double tol)
     return std::isfinite(n) && std::fabs(n - 1.0) <= tol;
 }
 
+void free_critic(im_ctx *c)
+{
+    auto &k = c->critic;
+    for (void *p : k.d_w) hipFree(p);
+    for (float *p : k.d_b) hipFree(p);
+    hipFree(k.d_head);
+    k.d_w.clear();
+    k.d_b.clear();
+    k.d_head = nullptr;
+    k.L = 0;
+    c->device_bytes -= k.bytes;
+    k.bytes = 0;
+}
+
 void free_ctx(im_ctx *c)
 {
     if (!c) return;
+    free_critic(c);
+    hipFree(c->d_partial);
     hipFree(c->d_skel);
     hipFree(c->d_clips);
     hipFree(c->d_seg);
@@ -592,10 +622,16 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     IM_TRY_ALLOC(c->d_log_std, sizeof(float) * c->A);
     IM_TRY_HIP(hipMemcpy(c->d_log_std, pol->log_std, sizeof(float) * c->A, hipMemcpyHostToDevice),
                "upload log_std");
+    IM_TRY_ALLOC(c->d_partial,
+                  sizeof(double) * IM_SUMMARY_FIELDS * (size_t)((max_envs + 255) / 256));
     if (c->L >= 2) {
         const size_t wsb = (size_t)max_envs * (size_t)ws_width * esz;
         IM_TRY_ALLOC(c->d_ws[0], wsb);
-        if (c->L >= 3) IM_TRY_ALLOC(c->d_ws[1], wsb);
+        c->ws_bytes[0] = wsb;
+        if (c->L >= 3) {
+            IM_TRY_ALLOC(c->d_ws[1], wsb);
+            c->ws_bytes[1] = wsb;
+        }
         // large bf16 batches stage the observation as bf16 rows for the first layer
         if (pol->dtype == IM_DTYPE_BF16 && max_envs > SMALL_BATCH)
             IM_TRY_ALLOC(c->d_obs16, (size_t)max_envs * (size_t)c->K_pad[0] * 2);
@@ -719,6 +755,228 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
         if (e != hipSuccess) return hip_fail(e, "policy layer launch");
     }
     return IM_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Hidden layers 0..n_hidden-1 of a packed MLP (bias, ReLU, the dtype's
+// rounding) on the observation; the last activations end in d_ws[(n_hidden-1) & 1].
+im_status mlp_hidden(im_ctx *c, int n_hidden, const std::vector<int> &M_pad,
+                     const std::vector<int> &K_pad, const std::vector<void *> &d_w,
+                     const std::vector<float *> &d_b, const float *obs, int64_t ld_obs,
+                     int64_t n_envs, hipStream_t stream)
+{
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    const uint64_t esz = bf16 ? 2 : 4;
+    for (int l = 0; l < n_hidden; ++l) {
+        GemmArgs g{};
+        g.x = l == 0 ? (const void *)obs : c->d_ws[(l - 1) & 1];
+        g.ld_x = l == 0 ? ld_obs : M_pad[l - 1];
+        g.x_bytes = (uint32_t)(l == 0 ? (uint64_t)c->D * (uint64_t)ld_obs * 4
+                                      : (uint64_t)n_envs * (uint64_t)M_pad[l - 1] * esz);
+        g.w_bytes = (uint32_t)((uint64_t)M_pad[l] * (uint64_t)K_pad[l] * esz);
+        g.w = d_w[l];
+        g.bias = d_b[l];
+        g.K_pad = K_pad[l];
+        g.K_valid = l == 0 ? c->D : K_pad[l];
+        g.N = n_envs;
+        g.x16 = l == 0 ? c->d_obs16 : nullptr;
+        g.n_cu = c->n_cu;
+        g.y = c->d_ws[l & 1];
+        g.ld_y = M_pad[l];
+        hipError_t e = launch_policy_layer(bf16, l == 0, false, g, M_pad[l], stream);
+        if (e != hipSuccess) return hip_fail(e, "hidden layer launch");
+    }
+    return IM_OK;
+}
+
+// Grow workspace buffer i to at least `bytes`.
+im_status ensure_ws(im_ctx *c, int i, size_t bytes)
+{
+    if (c->ws_bytes[i] >= bytes) return IM_OK;
+    hipFree(c->d_ws[i]);
+    c->device_bytes -= (int64_t)c->ws_bytes[i];
+    c->d_ws[i] = nullptr;
+    c->ws_bytes[i] = 0;
+    if (dev_alloc(c, &c->d_ws[i], bytes) != hipSuccess)
+        return fail(IM_ERR_OOM, "device allocation failed (workspace)");
+    c->ws_bytes[i] = bytes;
+    return IM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_set_critic(im_ctx *c, const im_policy *k)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (!k) return fail(IM_ERR_INVALID_ARG, "NULL critic");
+    const int L = k->n_layers;
+    if (L < 1 || !k->dims || !k->weight || !k->bias) return fail(IM_ERR_INVALID_ARG, "critic description incomplete");
+    if (k->dtype != c->dtype) return fail(IM_ERR_INVALID_ARG, "critic dtype must be the policy's");
+    if (k->dims[0] != c->D)
+        return fail(IM_ERR_INVALID_ARG, "critic input width must be the observation width " +
+                                            std::to_string(c->D));
+    if (k->dims[L] != 1) return fail(IM_ERR_INVALID_ARG, "critic output width must be 1");
+    for (int l = 0; l <= L; ++l)
+        if (k->dims[l] < 1 || k->dims[l] > 16384)
+            return fail(IM_ERR_INVALID_ARG, "layer widths must be in [1, 16384]");
+    for (int l = 0; l < L; ++l)
+        if (!k->weight[l] || !k->bias[l]) return fail(IM_ERR_INVALID_ARG, "NULL weight or bias");
+    im_status s = check_device(c);
+    if (s != IM_OK) return s;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "synchronise before replacing the critic");
+    free_critic(c);
+    auto &cr = c->critic;
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    const size_t esz = bf16 ? 2 : 4;
+    cr.dims.assign(k->dims, k->dims + L + 1);
+    cr.M_pad.assign(L - 1, 0);
+    cr.K_pad.assign(L - 1, 0);
+    int64_t ws_width = 0;
+    auto alloc = [&](auto **p, size_t bytes) {
+        if (dev_alloc(c, p, bytes) != hipSuccess) return false;
+        cr.bytes += (int64_t)bytes;
+        return true;
+    };
+    auto oom = [&](const char *what) {
+        free_critic(c);
+        return fail(IM_ERR_OOM, std::string("device allocation failed (") + what + ")");
+    };
+    auto upload_fail = [&](hipError_t err, const char *what) {
+        free_critic(c);
+        return hip_fail(err, what);
+    };
+    for (int l = 0; l < L - 1; ++l) {
+        cr.M_pad[l] = (int)round_up(cr.dims[l + 1], 256);
+        cr.K_pad[l] = l == 0 ? (int)round_up(cr.dims[0], 64) : cr.M_pad[l - 1];
+        ws_width = std::max<int64_t>(ws_width, cr.M_pad[l]);
+        const int M = cr.dims[l + 1], K = cr.dims[l];
+        std::vector<uint8_t> wbuf((size_t)cr.M_pad[l] * cr.K_pad[l] * esz, 0);
+        for (int m = 0; m < M; ++m)
+            std::memcpy(wbuf.data() + ((size_t)m * cr.K_pad[l]) * esz,
+                        (const uint8_t *)k->weight[l] + (size_t)m * K * esz, (size_t)K * esz);
+        std::vector<float> bbuf(cr.M_pad[l], 0.0f);
+        std::memcpy(bbuf.data(), k->bias[l], sizeof(float) * M);
+        void *dw = nullptr;
+        float *db = nullptr;
+        if (!alloc(&dw, wbuf.size())) return oom("critic weights");
+        cr.d_w.push_back(dw);
+        if (!alloc(&db, sizeof(float) * bbuf.size())) return oom("critic biases");
+        cr.d_b.push_back(db);
+        if ((e = hipMemcpy(dw, wbuf.data(), wbuf.size(), hipMemcpyHostToDevice)) != hipSuccess)
+            return upload_fail(e, "upload critic weights");
+        if ((e = hipMemcpy(db, bbuf.data(), sizeof(float) * bbuf.size(), hipMemcpyHostToDevice)) !=
+            hipSuccess)
+            return upload_fail(e, "upload critic biases");
+    }
+    // last layer as an fp32 vector (bf16 weights convert exactly)
+    cr.K_head = L == 1 ? c->D : cr.M_pad[L - 2];
+    std::vector<float> head(cr.K_head, 0.0f);
+    const int K = cr.dims[L - 1];
+    for (int i = 0; i < K; ++i) {
+        if (bf16) {
+            uint16_t h;
+            std::memcpy(&h, (const uint8_t *)k->weight[L - 1] + 2 * (size_t)i, 2);
+            const uint32_t u = (uint32_t)h << 16;
+            std::memcpy(&head[i], &u, 4);
+        } else {
+            std::memcpy(&head[i], (const uint8_t *)k->weight[L - 1] + 4 * (size_t)i, 4);
+        }
+    }
+    cr.head_bias = k->bias[L - 1][0];
+    if (!alloc(&cr.d_head, sizeof(float) * head.size())) return oom("critic head");
+    if ((e = hipMemcpy(cr.d_head, head.data(), sizeof(float) * head.size(), hipMemcpyHostToDevice)) !=
+        hipSuccess)
+        return upload_fail(e, "upload critic head");
+    // workspace for the hidden activations and the bf16 observation staging
+    if (L >= 2) {
+        const size_t wsb = (size_t)c->max_envs * (size_t)ws_width * esz;
+        if ((s = ensure_ws(c, 0, wsb)) != IM_OK || (L >= 3 && (s = ensure_ws(c, 1, wsb)) != IM_OK)) {
+            free_critic(c);
+            return s;
+        }
+        if (bf16 && c->max_envs > SMALL_BATCH && !c->d_obs16 &&
+            dev_alloc(c, &c->d_obs16, (size_t)c->max_envs * (size_t)round_up(c->D, 64) * 2) !=
+                hipSuccess)
+            return oom("observation staging");
+    }
+    cr.L = L;
+    return IM_OK;
+}
+
+im_status im_value(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, float *value,
+                   void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    const auto &cr = c->critic;
+    if (cr.L == 0) return fail(IM_ERR_INVALID_ARG, "no critic (im_set_critic)");
+    if (!obs || !value) return fail(IM_ERR_INVALID_ARG, "NULL buffer");
+    if (n_envs < 0 || n_envs > c->max_envs) return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
+    if (ld_obs < n_envs || ld_obs < 1) return fail(IM_ERR_INVALID_ARG, "ld_obs must be >= n_envs");
+    im_status s = check_device(c);
+    if (s != IM_OK) return s;
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    const uint64_t esz = bf16 ? 2 : 4;
+    if ((uint64_t)c->D * (uint64_t)ld_obs * 4 > 0xFFFFFFF0ull)
+        return fail(IM_ERR_UNSUPPORTED, "critic input exceeds 4 GiB");
+    for (int l = 1; l < cr.L - 1; ++l)
+        if ((uint64_t)n_envs * (uint64_t)cr.M_pad[l - 1] * esz > 0xFFFFFFF0ull)
+            return fail(IM_ERR_UNSUPPORTED, "critic layer input exceeds 4 GiB");
+    if (c->d_obs16 && (uint64_t)n_envs * (uint64_t)round_up(c->D, 64) * 2 > 0xFFFFFFF0ull)
+        return fail(IM_ERR_UNSUPPORTED, "staged critic input exceeds 4 GiB");
+    const hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if (cr.L == 1) {
+        e = launch_value_head_obs(obs, ld_obs, c->D, cr.d_head, cr.head_bias, bf16, n_envs, value, st);
+    } else {
+        if ((s = mlp_hidden(c, cr.L - 1, cr.M_pad, cr.K_pad, cr.d_w, cr.d_b, obs, ld_obs, n_envs,
+                            st)) != IM_OK)
+            return s;
+        e = launch_value_head_rows(bf16, c->d_ws[(cr.L - 2) & 1], cr.K_head, cr.K_head, cr.d_head,
+                                   cr.head_bias, n_envs, value, st);
+    }
+    return e == hipSuccess ? IM_OK : hip_fail(e, "value head launch");
+}
+
+im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (!r) return fail(IM_ERR_INVALID_ARG, "NULL rollout");
+    if (r->T < 1) return fail(IM_ERR_INVALID_ARG, "T must be >= 1");
+    if (r->n_envs < 0 || r->n_envs > c->max_envs)
+        return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
+    if (r->ld < r->n_envs || r->ld < 1) return fail(IM_ERR_INVALID_ARG, "ld must be >= n_envs and >= 1");
+    if (!r->reward || !r->terminated || !r->truncated || !r->value || !r->advantage || !r->ret)
+        return fail(IM_ERR_INVALID_ARG, "NULL rollout buffer");
+    if (r->summary && (!r->ep_return || !r->ep_length))
+        return fail(IM_ERR_INVALID_ARG, "summaries need ep_return and ep_length");
+    if (!(r->gamma >= 0.0f && r->gamma <= 1.0f) || !(r->lambda >= 0.0f && r->lambda <= 1.0f))
+        return fail(IM_ERR_INVALID_ARG, "gamma and lambda must be in [0, 1]");
+    im_status s = check_device(c);
+    if (s != IM_OK) return s;
+    GaeArgs g{};
+    g.T = r->T;
+    g.n = r->n_envs;
+    g.ld = r->ld;
+    g.gamma = (double)r->gamma;
+    g.lambda = (double)r->lambda;
+    g.reward = r->reward;
+    g.term = r->terminated;
+    g.trunc = r->truncated;
+    g.value = r->value;
+    g.adv = r->advantage;
+    g.ret = r->ret;
+    g.ep_return = r->ep_return;
+    g.ep_length = r->ep_length;
+    g.summary = r->summary;
+    g.partial = c->d_partial;
+    hipError_t e = launch_gae(g, (hipStream_t)stream);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "gae launch");
 }
 
 }  // extern "C"

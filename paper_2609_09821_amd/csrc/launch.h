@@ -39,6 +39,27 @@ struct GemmArgs {
     uint32_t y_bytes;    // extent of y in bytes (set by the launcher)
 };
 
+// Rollout end (rollout_kernels.hip).
+struct GaeArgs {
+    int T;
+    int64_t n, ld;
+    double gamma, lambda;
+    const float *reward;
+    const uint8_t *term, *trunc;
+    const float *value;
+    float *adv, *ret;
+    float *ep_return;
+    int32_t *ep_length;
+    double *summary;      // null: no summaries
+    double *partial;      // [blocks][IM_SUMMARY_FIELDS] per-block sums
+};
+
+hipError_t launch_value_head_rows(bool bf16, const void *x, int64_t ld_x, int K, const float *w,
+                                  float bias, int64_t N, float *value, hipStream_t s);
+hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w, float bias,
+                                 bool bf16, int64_t N, float *value, hipStream_t s);
+hipError_t launch_gae(const GaeArgs &g, hipStream_t s);
+
 hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_standin(int n_slots, const EnvArgs &a, hipStream_t s);

@@ -186,7 +186,7 @@ def test_create_rejects_bad_policies(lib):
     st, _ = d.create_status(64)
     _expect(lib, st, binding.IM_ERR_INVALID_ARG, "dtype")
     d = binding.Description(w)
-    d.weight_ptrs[1] = None
+    d.policy.weight[1] = None
     st, _ = d.create_status(64)
     _expect(lib, st, binding.IM_ERR_INVALID_ARG, "NULL weight")
 
@@ -234,6 +234,13 @@ def test_calls_reject_null_context(lib):
     _expect(lib, lib.im_policy_act(None, None, 1, None, 1, None, None, None, None),
             binding.IM_ERR_INVALID_ARG, "NULL context")
     _expect(lib, lib.im_destroy(None), binding.IM_ERR_INVALID_ARG, "NULL context")
+    d = binding.Description(_world())
+    _expect(lib, lib.im_set_critic(None, C.byref(d.critic)), binding.IM_ERR_INVALID_ARG,
+            "NULL context")
+    _expect(lib, lib.im_value(None, None, 1, 1, None, None), binding.IM_ERR_INVALID_ARG,
+            "NULL context")
+    ro = binding.ImRollout()
+    _expect(lib, lib.im_gae(None, C.byref(ro), None), binding.IM_ERR_INVALID_ARG, "NULL context")
     info = binding.ImInfo()
     _expect(lib, lib.im_get_info(None, C.byref(info)), binding.IM_ERR_INVALID_ARG, "NULL")
 

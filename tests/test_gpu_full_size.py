@@ -118,3 +118,27 @@ def test_full_size_policy(world):
     n = zf.size
     assert abs(zf.mean()) < 5.0 / np.sqrt(n)
     assert abs(zf.var() - 1.0) < 5.0 * np.sqrt(2.0 / n)
+
+
+def test_full_size_value(world):
+    """The critic at full size (large-batch GEMM tiles and the value head)
+    against the oracle on the sampled envs, finite everywhere."""
+    cfg, d, w, ctx, bufs = world
+    N = d["n_envs"]
+    st = w.state(N)
+    w.reset_envs(st)
+    w.standin(st, d["sigma_joint"], d["sigma_vel"])
+    w.env_step(st)
+    bufs.obs.copy_(torch.from_numpy(st.obs))
+    v = torch.empty(N, device="cuda")
+    ctx.value(bufs.obs, N, v)
+    torch.cuda.synchronize()
+    gv = v.cpu().numpy()
+    idx = _sample(N, np.random.default_rng(cfg + 100))
+    ov = oracle.value(d["critic"], st.obs, idx=idx)[idx]
+    s = np.sqrt(np.mean(ov.astype(np.float64) ** 2))
+    tol = 2e-2 if d["critic"]["bf16"] else 1e-4
+    err = np.abs(gv[idx] - ov) / np.maximum(np.abs(ov), s)
+    assert err.max() <= tol, "value: worst %.3e" % err.max()
+    print("cfg %d value (%d sampled envs): max rel err %.2e" % (cfg, len(idx), err.max()))
+    assert np.all(np.isfinite(gv))
