@@ -296,6 +296,9 @@ def run_rollout(wid, reps=2):
         env.append(np.mean([ev[t][2].elapsed_time(ev[t][3]) for t in range(T)]))
         gae.append(ev[T][0].elapsed_time(ev[T][1]))
     summ = ro.summary.cpu().numpy()
+    ppo = None
+    if desc["policy"]["bf16"]:
+        ppo = run_ppo_update(ctx, desc, ro)
     ctx.close()
     wall = float(np.min(walls))
     return {
@@ -306,9 +309,62 @@ def run_rollout(wid, reps=2):
         "env_step_us_per_step": float(np.mean(env)) * 1e3,
         "gae_summary_us": float(np.mean(gae)) * 1e3,
         "episodes_ended": int(summ[3]), "mean_reward": float(summ[0] / (N * T)),
+        "ppo_update": ppo,
         "note": "policy_act + value + env_step_fused per step into the rollout storage, value of "
                 "the last observation, GAE + summaries, last observation to slot 0; stand-in "
                 "physics excluded; best of %d rollouts" % reps,
+    }
+
+
+def ppo_flops_per_sample(dims):
+    """Forward, input-gradient and weight-gradient products of one MLP:
+    2 in out each, no input gradient for the first layer."""
+    macs = [dims[i] * dims[i + 1] for i in range(len(dims) - 1)]
+    return 2.0 * (3 * sum(macs) - macs[0])
+
+
+def run_ppo_update(ctx, desc, ro, reps=2):
+    """One PPO update (the configuration table's baseline: 5 learning epochs,
+    here 4 minibatches) over the rollout storage just filled, timed with HIP
+    events on the launch stream after one warm-up update."""
+    import torch
+    from paper_2609_09821_amd import binding
+
+    N, T = ro.n_envs, ro.T
+    p = dict(binding.PPO_DEFAULTS)
+    n_chunks = T * N // 64
+    mb = (n_chunks + p["minibatches"] - 1) // p["minibatches"] * 64
+    ctx.ppo_setup(mb)
+    rng = np.random.default_rng(0)
+    perm = torch.from_numpy(np.stack([rng.permutation(n_chunks) for _ in range(p["epochs"])])
+                            .astype(np.int32)).cuda()
+    lr = torch.full((1,), 5e-4, device="cuda")
+    stats = torch.zeros(len(binding.PPO_STATS), dtype=torch.float64, device="cuda")
+    batch = binding.ppo_batch(ro, perm, lr, stats)
+    params = binding.ppo_params(**p)
+    stream = torch.cuda.current_stream()
+    ctx.ppo_update(batch, params, stream=stream)       # warm-up
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ctx.ppo_update(batch, params, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e-3)
+    t = float(np.min(times))
+    samples = p["epochs"] * T * N
+    flops = samples * (ppo_flops_per_sample(desc["policy"]["dims"]) +
+                       ppo_flops_per_sample(desc["critic"]["dims"]))
+    st = stats.cpu().numpy()
+    return {
+        "ms": t * 1e3, "samples_per_s": samples / t, "epochs": p["epochs"],
+        "minibatches": p["minibatches"], "minibatch_samples": mb,
+        "tflops": flops / t / 1e12, "frac_of_bf16_peak": flops / t / 1e12 / MFMA_PEAK_TFLOPS["bf16"],
+        "mean_kl": float(st[2] / st[5]), "mean_clip_frac": float(st[3] / st[5]),
+        "note": "forward, backward and Adam of actor and critic on MFMA; flops = 2 in out per "
+                "layer for the forward, input and weight gradients (no input gradient for the "
+                "first layer), per sample and epoch",
     }
 
 

@@ -355,6 +355,96 @@ typedef struct {
  */
 im_status im_gae(im_ctx *ctx, const im_rollout *r, void *stream);
 
+/*
+ * PPO update (Fig. 3 update_policy; objective of Schulman et al. 2017, the
+ * paper's configuration table gives its coefficients).  bf16 policies only.
+ * Per minibatch: advantages normalised with the rollout's mean and unbiased
+ * std (from the im_gae summary), ratio = exp(logp - logp_old),
+ *   L_pi = mean max(-A ratio, -A clip(ratio, 1 - clip, 1 + clip)),
+ *   L_V  = mean max((V - R)^2, (V_old + clip(V - V_old, -clip, clip) - R)^2)
+ *          (clipped_value_loss; else mean (V - R)^2),
+ *   H    = sum_a (log_std_a + (1 + ln 2 pi) / 2),
+ *   loss = L_pi + value_coef L_V - entropy_coef H;
+ * KL to the rollout policy (mean_old, log_std at the start of the update),
+ * averaged over the minibatch, adapts the learning rate when desired_kl > 0
+ * (/1.5 above 2 desired_kl, not below lr_min; x1.5 below desired_kl / 2,
+ * not above lr_max); the gradient of all parameters is clipped to the
+ * global norm max_grad_norm (> 0), then one Adam step updates the float32
+ * master weights, and the policy and critic copies the rollout calls use are
+ * refreshed from them.  The forward rounds input, weights and hidden
+ * activations to bf16 like im_policy_act; the backward stores the gradient
+ * of every layer's pre-activation as bf16 and accumulates in float32.
+ */
+typedef struct {
+    float clip;                /* ratio clip, also the value clip */
+    float value_coef, entropy_coef;
+    int32_t clipped_value_loss;
+    float max_grad_norm;       /* <= 0: no clipping */
+    float beta1, beta2, eps;   /* Adam */
+    float desired_kl;          /* <= 0: fixed learning rate */
+    float lr_min, lr_max;
+    int32_t epochs, minibatches;
+} im_ppo_params;
+
+/*
+ * The rollout to learn from (device, the im_rollout storage after im_gae):
+ *   obs [T+1][D][ld] (slots 0..T-1), action and mean [T][n_envs][A] (the
+ *   actions and means im_policy_act returned), logp [T][ld], value [T+1][ld],
+ *   advantage and ret [T][ld], summary: the im_gae summary of this rollout.
+ *   perm [epochs][T * n_envs / 64] int32: the order of the rollout's 64-env
+ *   chunks in each epoch (chunk q = envs 64 (q % (n_envs/64)) .. +63 of step
+ *   q / (n_envs/64)); the chunks of an epoch are split into `minibatches`
+ *   consecutive groups, the first (count % minibatches) one chunk longer
+ *   (entries outside [0, count) are clamped into it).
+ *   lr: device float, the learning rate (adapted in place).
+ *   stats: device double [IM_PPO_STATS] (sums over minibatches, added to) or
+ *   NULL.  n_envs must be a multiple of 64.
+ */
+typedef struct {
+    int32_t T;
+    int64_t n_envs, ld;
+    const float *obs, *action, *mean, *logp, *value, *advantage, *ret;
+    const double *summary;
+    const int32_t *perm;
+    float *lr;
+    double *stats;
+} im_ppo_batch;
+
+enum {
+    IM_PPO_LOSS_PI = 0,   /* surrogate loss (sum of minibatch means) */
+    IM_PPO_LOSS_V,        /* value loss */
+    IM_PPO_KL,            /* KL to the rollout policy */
+    IM_PPO_CLIP_FRAC,     /* fraction of clipped ratios */
+    IM_PPO_GRAD_NORM,     /* gradient norm before clipping */
+    IM_PPO_MINIBATCHES,   /* minibatches counted */
+    IM_PPO_LR,            /* learning rate after the last step (not a sum) */
+    IM_PPO_STATS
+};
+
+/*
+ * Allocate the training state for minibatches of up to max_minibatch
+ * samples: float32 master weights (from the current policy and critic),
+ * Adam moments, activation and gradient buffers.  Not hot: allocates and
+ * synchronises.  Needs a critic; a second call resets the optimizer.
+ * Parameter vector order: actor W_0 [out][in], b_0, ..., log_std, critic
+ * W_0, b_0, ..., the critic's output layer W [1][in], b [1].
+ */
+im_status im_ppo_setup(im_ctx *ctx, int64_t max_minibatch);
+
+/* The whole update (epochs x minibatches); enqueued on the stream, no host
+ * synchronisation, allocates nothing. */
+im_status im_ppo_update(im_ctx *ctx, const im_ppo_batch *b, const im_ppo_params *p, void *stream);
+
+/* The float32 gradient (parameter vector order, before clipping) of one
+ * minibatch of one epoch at the current weights, no step; stats (device
+ * double [IM_PPO_STATS] or NULL) receives that minibatch's loss terms. */
+im_status im_ppo_grad(im_ctx *ctx, const im_ppo_batch *b, const im_ppo_params *p, int32_t epoch,
+                      int32_t minibatch, float *grad, double *stats, void *stream);
+
+/* Number of parameters and, when params != NULL, a copy of the master
+ * weights (device float [n]). */
+im_status im_ppo_params_get(im_ctx *ctx, float *params, int64_t *n, void *stream);
+
 const char *im_status_str(im_status s);
 const char *im_last_error(void);
 

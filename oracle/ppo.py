@@ -182,6 +182,27 @@ def adapt_lr(lr, kl, p):
     return lr
 
 
+def gather(data, chunks, log_std_old, chunk=64):
+    """The minibatch of the given 64-env chunk ids (chunk q = step
+    q // (N / chunk), envs chunk * (q % (N / chunk)) onwards), in chunk order."""
+    N = np.asarray(data["obs"]).shape[2]
+    cpt = N // chunk
+    grp = np.asarray(chunks)
+    ts = np.repeat(grp // cpt, chunk)
+    es = np.repeat((grp % cpt) * chunk, chunk) + np.tile(np.arange(chunk), len(grp))
+    return dict(obs=np.asarray(data["obs"])[ts, :, es].astype(np.float32),
+                action=data["action"][ts, es], mean_old=data["mean"][ts, es],
+                logp_old=data["logp"][ts, es], adv=data["adv"][ts, es], ret=data["ret"][ts, es],
+                value_old=data["value"][ts, es], log_std_old=log_std_old)
+
+
+def adv_stats(adv):
+    """Mean and unbiased standard deviation of the rollout's advantages."""
+    a = np.asarray(adv, np.float64)
+    m = a.mean()
+    return m, np.sqrt(((a - m) ** 2).sum() / (a.size - 1))
+
+
 def update(actor, critic, data, perm, p, lr, chunk=64):
     """The whole update: for every epoch the chunks of perm[epoch] (chunk q =
     step q // (N / chunk), envs chunk * (q % (N / chunk)) onwards) are split
@@ -190,14 +211,7 @@ def update(actor, critic, data, perm, p, lr, chunk=64):
 
     data: obs [T][D][N], action / mean [T][N][A], logp / adv / ret [T][N],
     value [T(+1)][N].  Returns (actor, critic, lr, per-minibatch records)."""
-    obs = np.asarray(data["obs"])
-    T, D, N = obs.shape[0], obs.shape[1], obs.shape[2]
-    T = data["adv"].shape[0]
-    cpt = N // chunk
-    adv = np.asarray(data["adv"], np.float64)
-    n = adv.size
-    adv_mean = adv.mean()
-    adv_std = np.sqrt(((adv - adv_mean) ** 2).sum() / (n - 1))
+    adv_mean, adv_std = adv_stats(data["adv"])
     log_std_old = np.asarray(actor["log_std"], np.float32).copy()
     x = flat_params(actor, critic).astype(np.float64)
     m = np.zeros_like(x)
@@ -208,12 +222,7 @@ def update(actor, critic, data, perm, p, lr, chunk=64):
         q = np.asarray(perm[ep])
         groups = np.array_split(q, p["minibatches"])
         for grp in groups:
-            ts = np.repeat(grp // cpt, chunk)
-            es = (np.repeat((grp % cpt) * chunk, chunk) + np.tile(np.arange(chunk), len(grp)))
-            mb = dict(obs=obs[ts, :, es].astype(np.float32), action=data["action"][ts, es],
-                      mean_old=data["mean"][ts, es], logp_old=data["logp"][ts, es],
-                      adv=data["adv"][ts, es], ret=data["ret"][ts, es],
-                      value_old=data["value"][ts, es], log_std_old=log_std_old)
+            mb = gather(data, grp, log_std_old, chunk)
             a, c = unflat(x.astype(np.float32), actor, critic)
             r = minibatch(a, c, mb, p, adv_mean, adv_std)
             lr = adapt_lr(lr, r["kl"], p)

@@ -73,6 +73,26 @@ SUMMARY_FIELDS = ("reward_sum", "n_terminated", "n_truncated", "n_episodes",
                   "advantage_sq_sum", "value_sum", "return_sum")
 
 
+class ImPpoParams(C.Structure):
+    _fields_ = [("clip", C.c_float), ("value_coef", C.c_float), ("entropy_coef", C.c_float),
+                ("clipped_value_loss", C.c_int32), ("max_grad_norm", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("desired_kl", C.c_float), ("lr_min", C.c_float), ("lr_max", C.c_float),
+                ("epochs", C.c_int32), ("minibatches", C.c_int32)]
+
+
+class ImPpoBatch(C.Structure):
+    _fields_ = [("T", C.c_int32), ("n_envs", C.c_int64), ("ld", C.c_int64), ("obs", C.c_void_p),
+                ("action", C.c_void_p), ("mean", C.c_void_p), ("logp", C.c_void_p),
+                ("value", C.c_void_p), ("advantage", C.c_void_p), ("ret", C.c_void_p),
+                ("summary", C.c_void_p), ("perm", C.c_void_p), ("lr", C.c_void_p),
+                ("stats", C.c_void_p)]
+
+
+# PPO update statistics (IM_PPO_* order)
+PPO_STATS = ("loss_pi", "loss_v", "kl", "clip_frac", "grad_norm", "minibatches", "lr")
+
+
 class ImInfo(C.Structure):
     _fields_ = [("n_bodies", C.c_int32), ("obs_dim", C.c_int32), ("action_dim", C.c_int32),
                 ("n_clips", C.c_int32), ("n_layers", C.c_int32), ("policy_dtype", C.c_int32),
@@ -81,6 +101,7 @@ class ImInfo(C.Structure):
 
 EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_policy_act",
             "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value", "im_gae",
+            "im_ppo_setup", "im_ppo_update", "im_ppo_grad", "im_ppo_params_get",
             "im_status_str", "im_last_error"]
 
 _lib = None
@@ -119,6 +140,15 @@ def lib():
     L.im_value.restype = st
     L.im_gae.argtypes = [C.c_void_p, C.POINTER(ImRollout), C.c_void_p]
     L.im_gae.restype = st
+    L.im_ppo_setup.argtypes = [C.c_void_p, C.c_int64]
+    L.im_ppo_setup.restype = st
+    L.im_ppo_update.argtypes = [C.c_void_p, C.POINTER(ImPpoBatch), C.POINTER(ImPpoParams), C.c_void_p]
+    L.im_ppo_update.restype = st
+    L.im_ppo_grad.argtypes = [C.c_void_p, C.POINTER(ImPpoBatch), C.POINTER(ImPpoParams), C.c_int32,
+                              C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.im_ppo_grad.restype = st
+    L.im_ppo_params_get.argtypes = [C.c_void_p, C.c_void_p, C.POINTER(C.c_int64), C.c_void_p]
+    L.im_ppo_params_get.restype = st
     L.im_status_str.argtypes = [C.c_int]
     L.im_status_str.restype = C.c_char_p
     L.im_last_error.argtypes = []
@@ -185,6 +215,25 @@ def im_value(ctx, obs_ptr, ld_obs, n_envs, value_ptr, stream=None):
 
 def im_gae(ctx, rollout, stream=None):
     _check(lib().im_gae(ctx, C.byref(rollout), stream))
+
+
+def im_ppo_setup(ctx, max_minibatch):
+    _check(lib().im_ppo_setup(ctx, int(max_minibatch)))
+
+
+def im_ppo_update(ctx, batch, params, stream=None):
+    _check(lib().im_ppo_update(ctx, C.byref(batch), C.byref(params), stream))
+
+
+def im_ppo_grad(ctx, batch, params, epoch, minibatch, grad_ptr, stats_ptr, stream=None):
+    _check(lib().im_ppo_grad(ctx, C.byref(batch), C.byref(params), int(epoch), int(minibatch),
+                             grad_ptr, stats_ptr, stream))
+
+
+def im_ppo_params_get(ctx, params_ptr=None, stream=None):
+    n = C.c_int64()
+    _check(lib().im_ppo_params_get(ctx, params_ptr, C.byref(n), stream))
+    return n.value
 
 
 # ------------------------------------------------------------- conveniences
@@ -367,6 +416,22 @@ class Context:
     def value(self, obs, n_envs, value, stream=None):
         im_value(self.ptr, _dptr(obs), obs.shape[1], n_envs, _dptr(value), _stream(stream))
 
+    def ppo_setup(self, max_minibatch):
+        im_ppo_setup(self.ptr, max_minibatch)
+
+    def ppo_update(self, batch, params, stream=None):
+        im_ppo_update(self.ptr, batch, params, _stream(stream))
+
+    def ppo_grad(self, batch, params, epoch, minibatch, grad, stats=None, stream=None):
+        im_ppo_grad(self.ptr, batch, params, epoch, minibatch, _dptr(grad), _dptr(stats),
+                    _stream(stream))
+
+    def ppo_params(self, out=None, stream=None):
+        """Number of parameters, or the master weights copied into `out`."""
+        if out is None:
+            return im_ppo_params_get(self.ptr)
+        return im_ppo_params_get(self.ptr, _dptr(out), _stream(stream))
+
     def gae(self, ro, gamma, lam, summary=True, stream=None):
         """GAE (and, with summary, the rollout summaries) over a RolloutStorage."""
         im_gae(self.ptr, ro.struct(gamma, lam, summary), _stream(stream))
@@ -417,3 +482,26 @@ class RolloutStorage:
                          self.advantage.data_ptr(), self.ret.data_ptr(),
                          self.ep_return.data_ptr(), self.ep_length.data_ptr(),
                          self.summary.data_ptr() if summary else None)
+
+
+# PPO defaults: the baseline column of the backflip configuration table (ratio
+# clip, value and entropy coefficients, KL threshold, learning epochs) and the
+# usual Adam / norm-clip settings
+PPO_DEFAULTS = dict(clip=0.2, value_coef=2.0, entropy_coef=0.0, clipped_value_loss=1,
+                    max_grad_norm=1.0, beta1=0.9, beta2=0.999, eps=1e-8, desired_kl=0.008,
+                    lr_min=1e-5, lr_max=1e-2, epochs=5, minibatches=4)
+
+
+def ppo_params(**over):
+    p = dict(PPO_DEFAULTS, **over)
+    return ImPpoParams(*(p[k] for k, _ in ImPpoParams._fields_))
+
+
+def ppo_batch(ro, perm, lr, stats=None):
+    """ImPpoBatch over a RolloutStorage after im_gae; perm: device int32
+    [epochs][T * n_envs / 64]; lr: device float [1]; stats: device float64
+    [len(PPO_STATS)] or None."""
+    return ImPpoBatch(ro.T, ro.n_envs, ro.ld, ro.obs.data_ptr(), ro.action.data_ptr(),
+                      ro.mean.data_ptr(), ro.logp.data_ptr(), ro.value.data_ptr(),
+                      ro.advantage.data_ptr(), ro.ret.data_ptr(), ro.summary.data_ptr(),
+                      perm.data_ptr(), lr.data_ptr(), None if stats is None else stats.data_ptr())

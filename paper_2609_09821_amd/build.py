@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libinstantmimic.so")
-SOURCES = ["api.hip", "env_kernels.hip", "policy_kernels.hip", "rollout_kernels.hip"]
+SOURCES = ["api.hip", "env_kernels.hip", "policy_kernels.hip", "rollout_kernels.hip",
+           "train_kernels.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

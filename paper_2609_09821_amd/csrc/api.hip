@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/instantmimic.h"
@@ -19,6 +20,11 @@ using namespace im;
 // thread in the stand-in, 256 threads per block): 3 slots keep a block within
 // 64 KB.  Humanoid trees need 2.
 #define IM_MAX_BRANCH_NESTING 3
+
+namespace im {
+struct TrainState;
+void free_train(TrainState *t);
+}  // namespace im
 
 struct im_ctx {
     int device = -1;
@@ -45,12 +51,12 @@ struct im_ctx {
         std::vector<int> dims, M_pad, K_pad;
         std::vector<void *> d_w;
         std::vector<float *> d_b;
-        float *d_head = nullptr;   // [K_head] last-layer weights, zero-padded
-        float head_bias = 0.0f;
+        float *d_head = nullptr;   // [K_head + 1]: last-layer weights (zero-padded), then its bias
         int K_head = 0;            // D for a one-layer critic, else M_pad[L-2]
         int64_t bytes = 0;         // device memory of the above
     } critic;
     double *d_partial = nullptr;   // per-block summary sums, [ceil(max_envs/256)][fields]
+    im::TrainState *train = nullptr;   // PPO update state (im_ppo_setup)
 };
 
 namespace {
@@ -96,6 +102,7 @@ void free_critic(im_ctx *c)
 void free_ctx(im_ctx *c)
 {
     if (!c) return;
+    im::free_train(c->train);
     free_critic(c);
     hipFree(c->d_partial);
     hipFree(c->d_skel);
@@ -876,7 +883,7 @@ im_status im_set_critic(im_ctx *c, const im_policy *k)
     }
     // last layer as an fp32 vector (bf16 weights convert exactly)
     cr.K_head = L == 1 ? c->D : cr.M_pad[L - 2];
-    std::vector<float> head(cr.K_head, 0.0f);
+    std::vector<float> head(cr.K_head + 1, 0.0f);
     const int K = cr.dims[L - 1];
     for (int i = 0; i < K; ++i) {
         if (bf16) {
@@ -888,7 +895,7 @@ im_status im_set_critic(im_ctx *c, const im_policy *k)
             std::memcpy(&head[i], (const uint8_t *)k->weight[L - 1] + 4 * (size_t)i, 4);
         }
     }
-    cr.head_bias = k->bias[L - 1][0];
+    head[cr.K_head] = k->bias[L - 1][0];
     if (!alloc(&cr.d_head, sizeof(float) * head.size())) return oom("critic head");
     if ((e = hipMemcpy(cr.d_head, head.data(), sizeof(float) * head.size(), hipMemcpyHostToDevice)) !=
         hipSuccess)
@@ -932,13 +939,14 @@ im_status im_value(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, 
     const hipStream_t st = (hipStream_t)stream;
     hipError_t e;
     if (cr.L == 1) {
-        e = launch_value_head_obs(obs, ld_obs, c->D, cr.d_head, cr.head_bias, bf16, n_envs, value, st);
+        e = launch_value_head_obs(obs, ld_obs, c->D, cr.d_head, cr.d_head + cr.K_head, bf16, n_envs,
+                                  value, st);
     } else {
         if ((s = mlp_hidden(c, cr.L - 1, cr.M_pad, cr.K_pad, cr.d_w, cr.d_b, obs, ld_obs, n_envs,
                             st)) != IM_OK)
             return s;
         e = launch_value_head_rows(bf16, c->d_ws[(cr.L - 2) & 1], cr.K_head, cr.K_head, cr.d_head,
-                                   cr.head_bias, n_envs, value, st);
+                                   cr.d_head + cr.K_head, n_envs, value, st);
     }
     return e == hipSuccess ? IM_OK : hip_fail(e, "value head launch");
 }
@@ -980,3 +988,554 @@ im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// PPO update: training state and entry points.
+// ---------------------------------------------------------------------------
+namespace im {
+
+struct TrainLayer {
+    int out = 0, in = 0, Mp = 0, Kp = 0;   // Mp, Kp: multiples of the 128 GEMM tile
+    int64_t w_off = 0, b_off = 0;          // in the parameter vector
+    uint16_t *wt = nullptr;                // [Mp][Kp] bf16
+    uint16_t *wtt = nullptr;               // [Kp][Mp] bf16
+    float *bias = nullptr;                 // [Mp]
+    uint16_t *act = nullptr;               // hidden output [Mp][Mb] bf16 (null: output layer)
+    void *roll = nullptr;                  // the rollout's packed copy [.][roll_K]
+    int roll_K = 0;
+    float *roll_bias = nullptr;
+};
+
+struct TrainState {
+    int64_t Mb_max = 0;                    // samples per minibatch, padded to 256
+    int64_t P = 0;                         // parameters
+    float *x = nullptr, *m = nullptr, *v = nullptr, *grad = nullptr;
+    int *step = nullptr;
+    OptScalars *opt = nullptr;
+    std::vector<TrainLayer> actor, critic;  // critic: its hidden layers
+    int64_t log_std_off = 0, head_w_off = 0, head_b_off = 0;
+    int head_K = 0;                        // input width of the critic's output layer
+    int Kp0 = 0;
+    uint16_t *x0 = nullptr;                // [Kp0][Mb] gathered observation (bf16)
+    float *act = nullptr, *mean_old = nullptr;   // [A][Mb]
+    float *logp_old = nullptr, *adv = nullptr, *ret = nullptr, *vold = nullptr;
+    float *mean_new = nullptr, *value_new = nullptr, *dv = nullptr;
+    uint16_t *dmu = nullptr;               // [Mp of the actor's output layer][Mb], rows >= A zero
+    uint16_t *dz[2] = {nullptr, nullptr};  // [max width][Mb]
+    float *splitk = nullptr;
+    size_t splitk_floats = 0;
+    double *loss_partial = nullptr, *mb_stats = nullptr, *norm_partial = nullptr;
+    int norm_blocks = 0;
+    float *log_std_old = nullptr;
+    std::vector<void *> allocs;
+    int64_t bytes = 0;
+};
+
+void free_train(TrainState *t)
+{
+    if (!t) return;
+    for (void *p : t->allocs) hipFree(p);
+    delete t;
+}
+
+}  // namespace im
+
+namespace {
+
+using im::TrainLayer;
+using im::TrainState;
+
+// split-K for a weight gradient of tiles x (K = Mb): about 1024 blocks, at
+// least 4 K steps each
+void splitk_plan(int tiles, int64_t Mb, int *splits, int *k_split)
+{
+    int64_t S = (1024 + tiles - 1) / tiles;
+    const int64_t smax = Mb / 256 > 0 ? Mb / 256 : 1;
+    if (S > smax) S = smax;
+    if (S < 1) S = 1;
+    int64_t ks = round_up((Mb + S - 1) / S, 64);
+    *k_split = (int)ks;
+    *splits = (int)((Mb + ks - 1) / ks);
+}
+
+im_status tg(bool bt, int epi, const im::TGemm &g, int splits, hipStream_t st)
+{
+    hipError_t e = im::launch_tgemm(bt, epi, g, splits, st);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "training GEMM launch");
+}
+
+#define IM_CHK(call)                                          \
+    do {                                                      \
+        hipError_t e_ = (call);                               \
+        if (e_ != hipSuccess) return hip_fail(e_, #call);     \
+    } while (0)
+#define IM_CHS(call)                   \
+    do {                               \
+        im_status s_ = (call);         \
+        if (s_ != IM_OK) return s_;    \
+    } while (0)
+
+// forward of one network's GEMM layers; returns the output of the last one
+im_status net_forward(const std::vector<TrainLayer> &net, const uint16_t *x0, int Kp0, int64_t Mb,
+                      bool linear_last, float *out_last, int M_valid, hipStream_t st)
+{
+    const uint16_t *x = x0;
+    int Kx = Kp0;
+    for (size_t l = 0; l < net.size(); ++l) {
+        const TrainLayer &L = net[l];
+        const bool last = linear_last && l + 1 == net.size();
+        im::TGemm g{};
+        g.A = L.wt;
+        g.lda = L.Kp;
+        g.a_bytes = (uint32_t)((uint64_t)L.Mp * L.Kp * 2);
+        g.B = x;
+        g.ldb = Mb;
+        g.b_bytes = (uint32_t)((uint64_t)Kx * Mb * 2);
+        g.M = L.Mp;
+        g.N = (int)Mb;
+        g.K = L.Kp;
+        g.k_split = L.Kp;
+        g.bias = L.bias;
+        g.ldc = Mb;
+        if (last) {
+            g.C = out_last;
+            g.M_valid = M_valid;
+            IM_CHS(tg(true, im::T_LINEAR, g, 1, st));
+        } else {
+            g.C = L.act;
+            IM_CHS(tg(true, im::T_HIDDEN, g, 1, st));
+        }
+        x = L.act;
+        Kx = L.Mp;
+    }
+    return IM_OK;
+}
+
+// backward of one network's GEMM layers from dz (gradient of the last GEMM
+// layer's pre-activation, [Mp][Mb] bf16): weight and bias gradients into
+// t->grad; dz buffers alternate in t->dz starting after `dz`
+im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const uint16_t *x0,
+                       const uint16_t *dz, int64_t Mb, hipStream_t st)
+{
+    int pp = dz == t->dz[0] ? 1 : 0;
+    for (int l = (int)net.size() - 1; l >= 0; --l) {
+        const TrainLayer &L = net[l];
+        const uint16_t *X = l == 0 ? x0 : net[l - 1].act;
+        // dW = dZ^T X over the minibatch (split over it)
+        const int tiles = (L.Mp / 128) * (L.Kp / 128);
+        int S, ks;
+        splitk_plan(tiles, Mb, &S, &ks);
+        im::TGemm g{};
+        g.A = dz;
+        g.lda = Mb;
+        g.a_bytes = (uint32_t)((uint64_t)L.Mp * Mb * 2);
+        g.B = X;
+        g.ldb = Mb;
+        g.b_bytes = (uint32_t)((uint64_t)L.Kp * Mb * 2);
+        g.M = L.Mp;
+        g.N = L.Kp;
+        g.K = (int)Mb;
+        g.k_split = ks;
+        g.C = t->splitk;
+        g.ldc = L.Kp;
+        IM_CHS(tg(false, im::T_PARTIAL, g, S, st));
+        IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, L.Kp, L.out, L.in, t->grad + L.w_off, st));
+        IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->grad + L.b_off, st));
+        if (l == 0) break;
+        // dX^T = W^T dZ^T, masked where the layer input (a ReLU output) is 0
+        im::TGemm h{};
+        h.A = L.wtt;
+        h.lda = L.Mp;
+        h.a_bytes = (uint32_t)((uint64_t)L.Kp * L.Mp * 2);
+        h.B = dz;
+        h.ldb = Mb;
+        h.b_bytes = (uint32_t)((uint64_t)L.Mp * Mb * 2);
+        h.M = L.Kp;
+        h.N = (int)Mb;
+        h.K = L.Mp;
+        h.k_split = L.Mp;
+        h.C = t->dz[pp];
+        h.ldc = Mb;
+        h.mask = X;
+        h.ldm = Mb;
+        IM_CHS(tg(true, im::T_MASK, h, 1, st));
+        dz = t->dz[pp];
+        pp ^= 1;
+    }
+    return IM_OK;
+}
+
+// minibatch chunk range of (epoch, mb): numpy array_split of the epoch's chunks
+void mb_range(int64_t n_chunks, int mbs, int mb, int64_t *first, int64_t *count)
+{
+    const int64_t q = n_chunks / mbs, r = n_chunks % mbs;
+    *first = mb * q + (mb < r ? mb : r);
+    *count = q + (mb < r ? 1 : 0);
+}
+
+// forward, loss and backward of one minibatch: t->grad and t->mb_stats
+im_status run_minibatch(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p, int epoch, int mb,
+                        hipStream_t st)
+{
+    TrainState *t = c->train;
+    const int64_t n_chunks = (int64_t)b->T * (b->n_envs / 64);
+    int64_t first, count;
+    mb_range(n_chunks, p->minibatches, mb, &first, &count);
+    const int64_t Mb = count * 64;
+    const int64_t Mbp = round_up(Mb, 256);
+    im::GatherArgs ga{};
+    ga.obs = b->obs;
+    ga.action = b->action;
+    ga.mean = b->mean;
+    ga.logp = b->logp;
+    ga.adv_src = b->advantage;
+    ga.ret_src = b->ret;
+    ga.value = b->value;
+    ga.perm = b->perm + (int64_t)epoch * n_chunks + first;
+    ga.chunks = (int)count;
+    ga.chunks_pad = (int)(Mbp / 64);
+    ga.n_chunks = (int)n_chunks;
+    ga.cpt = b->n_envs / 64;
+    ga.N = b->n_envs;
+    ga.ld = b->ld;
+    ga.Mb_pad = Mbp;
+    ga.D = c->D;
+    ga.K0 = t->Kp0;
+    ga.A = c->A;
+    ga.x0 = t->x0;
+    ga.act = t->act;
+    ga.mean_old = t->mean_old;
+    ga.logp_old = t->logp_old;
+    ga.adv = t->adv;
+    ga.ret = t->ret;
+    ga.vold = t->vold;
+    IM_CHK(im::launch_gather(ga, st));
+    // forward
+    IM_CHS(net_forward(t->actor, t->x0, t->Kp0, Mbp, true, t->mean_new, c->A, st));
+    IM_CHS(net_forward(t->critic, t->x0, t->Kp0, Mbp, false, nullptr, 0, st));
+    const TrainLayer &hl = t->critic.back();
+    const float *head = c->critic.d_head;
+    IM_CHK(im::launch_head_forward(hl.act, t->head_K, Mbp, head, head + c->critic.K_head, t->value_new,
+                                   st));
+    // loss
+    im::LossArgs la{};
+    la.Mb = Mb;
+    la.Mb_pad = Mbp;
+    la.A = c->A;
+    la.n_samples = (int64_t)b->T * b->n_envs;
+    la.summary = b->summary;
+    la.mean = t->mean_new;
+    la.act = t->act;
+    la.mean_old = t->mean_old;
+    la.log_std = t->x + t->log_std_off;
+    la.log_std_old = t->log_std_old;
+    la.logp_old = t->logp_old;
+    la.adv = t->adv;
+    la.ret = t->ret;
+    la.vold = t->vold;
+    la.value = t->value_new;
+    la.clip = p->clip;
+    la.value_coef = p->value_coef;
+    la.clipped_value_loss = p->clipped_value_loss;
+    la.dmu = t->dmu;
+    la.dv = t->dv;
+    la.partial = t->loss_partial;
+    IM_CHK(im::launch_loss(la, st));
+    im::LossReduceArgs lr{};
+    lr.partial = t->loss_partial;
+    lr.blocks = (int)(Mbp / 256);
+    lr.A = c->A;
+    lr.Mb = Mb;
+    lr.entropy_coef = p->entropy_coef;
+    lr.grad_log_std = t->grad + t->log_std_off;
+    lr.mb_stats = t->mb_stats;
+    IM_CHK(im::launch_loss_reduce(lr, st));
+    // backward: actor from the output-layer gradient, critic from dV
+    IM_CHS(net_backward(t, t->actor, t->x0, t->dmu, Mbp, st));
+    IM_CHK(im::launch_rowsum(true, hl.act, t->head_K, Mbp, t->dv, t->grad + t->head_w_off, st));
+    IM_CHK(im::launch_rowsum(false, t->dv, 1, Mbp, nullptr, t->grad + t->head_b_off, st));
+    IM_CHK(im::launch_head_backward(hl.act, t->head_K, hl.Mp, Mbp, head, t->dv, t->dz[0], st));
+    IM_CHS(net_backward(t, t->critic, t->x0, t->dz[0], Mbp, st));
+    return IM_OK;
+}
+
+// training and rollout copies of every layer from the masters
+im_status repack_all(im_ctx *c, hipStream_t st)
+{
+    TrainState *t = c->train;
+    for (auto *net : {&t->actor, &t->critic})
+        for (const TrainLayer &L : *net) {
+            im::RepackArgs r{};
+            r.W = t->x + L.w_off;
+            r.b = t->x + L.b_off;
+            r.out = L.out;
+            r.in = L.in;
+            r.wt = L.wt;
+            r.wtt = L.wtt;
+            r.Mp = L.Mp;
+            r.Kp = L.Kp;
+            r.roll = L.roll;
+            r.roll_K = L.roll_K;
+            r.roll_bf16 = 1;
+            r.bias_train = L.bias;
+            r.bias_roll = L.roll_bias;
+            IM_CHK(im::launch_repack(r, st));
+        }
+    // the critic's output layer (bf16-rounded weights, as the forward uses them)
+    im::RepackArgs h{};
+    h.W = t->x + t->head_w_off;
+    h.b = t->x + t->head_b_off;
+    h.out = 1;
+    h.in = t->head_K;
+    h.roll = c->critic.d_head;
+    h.roll_K = 0;
+    h.roll_bf16 = 2;
+    h.bias_roll = c->critic.d_head + c->critic.K_head;
+    IM_CHK(im::launch_repack(h, st));
+    IM_CHK(hipMemcpyAsync(c->d_log_std, t->x + t->log_std_off, sizeof(float) * c->A,
+                          hipMemcpyDeviceToDevice, st));
+    return IM_OK;
+}
+
+im_status check_ppo(const im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (!b || !p) return fail(IM_ERR_INVALID_ARG, "NULL argument");
+    if (!c->train) return fail(IM_ERR_INVALID_ARG, "no training state (im_ppo_setup)");
+    if (b->T < 1) return fail(IM_ERR_INVALID_ARG, "T must be >= 1");
+    if (b->n_envs < 64 || b->n_envs % 64) return fail(IM_ERR_INVALID_ARG, "n_envs must be a positive multiple of 64");
+    if (b->ld < b->n_envs) return fail(IM_ERR_INVALID_ARG, "ld must be >= n_envs");
+    if (!b->obs || !b->action || !b->mean || !b->logp || !b->value || !b->advantage || !b->ret ||
+        !b->summary || !b->perm || !b->lr)
+        return fail(IM_ERR_INVALID_ARG, "NULL batch buffer");
+    if (p->epochs < 1 || p->minibatches < 1) return fail(IM_ERR_INVALID_ARG, "epochs and minibatches must be >= 1");
+    const int64_t n_chunks = (int64_t)b->T * (b->n_envs / 64);
+    if (p->minibatches > n_chunks) return fail(IM_ERR_INVALID_ARG, "more minibatches than 64-env chunks");
+    const int64_t largest = (n_chunks + p->minibatches - 1) / p->minibatches * 64;
+    if (round_up(largest, 256) > c->train->Mb_max)
+        return fail(IM_ERR_UNSUPPORTED, "minibatch of " + std::to_string(largest) +
+                                            " samples exceeds the im_ppo_setup size");
+    const float vals[] = {p->clip, p->value_coef, p->entropy_coef, p->max_grad_norm, p->beta1, p->beta2,
+                          p->eps, p->desired_kl, p->lr_min, p->lr_max};
+    for (float v : vals)
+        if (!finite_f(v)) return fail(IM_ERR_INVALID_ARG, "PPO parameters must be finite");
+    if (!(p->clip > 0.0f) || p->value_coef < 0.0f || p->entropy_coef < 0.0f)
+        return fail(IM_ERR_INVALID_ARG, "clip must be > 0 and the coefficients >= 0");
+    if (!(p->beta1 >= 0.0f && p->beta1 < 1.0f) || !(p->beta2 >= 0.0f && p->beta2 < 1.0f) || !(p->eps > 0.0f))
+        return fail(IM_ERR_INVALID_ARG, "Adam betas must be in [0, 1) and eps > 0");
+    if (!(p->lr_min > 0.0f) || p->lr_min > p->lr_max) return fail(IM_ERR_INVALID_ARG, "need 0 < lr_min <= lr_max");
+    return check_device(c);
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (c->dtype != IM_DTYPE_BF16) return fail(IM_ERR_UNSUPPORTED, "the PPO update needs a bf16 policy");
+    if (c->critic.L < 2) return fail(IM_ERR_INVALID_ARG, "the PPO update needs a critic with a hidden layer");
+    if (max_minibatch < 64 || max_minibatch > ((int64_t)1 << 24))
+        return fail(IM_ERR_INVALID_ARG, "max_minibatch must be in [64, 2^24]");
+    im_status s = check_device(c);
+    if (s != IM_OK) return s;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "synchronise before the training setup");
+    im::free_train(c->train);
+    c->train = nullptr;
+    auto *t = new TrainState();
+    const int64_t Mb = round_up(max_minibatch, 256);
+    t->Mb_max = Mb;
+    auto alloc = [&](auto **p, size_t bytes) {
+        void *q = nullptr;
+        if (hipMalloc(&q, bytes) != hipSuccess) return false;
+        t->allocs.push_back(q);
+        t->bytes += (int64_t)bytes;
+        *p = (std::remove_reference_t<decltype(*p)>)q;
+        return hipMemset(q, 0, bytes) == hipSuccess;
+    };
+    auto oom = [&]() {
+        im::free_train(t);
+        return fail(IM_ERR_OOM, "device allocation failed (training state)");
+    };
+    // layer tables and parameter offsets
+    int64_t off = 0;
+    auto layer = [&](int out, int in) {
+        TrainLayer L;
+        L.out = out;
+        L.in = in;
+        L.Mp = (int)round_up(out, 128);
+        L.Kp = (int)round_up(in, 128);
+        L.w_off = off;
+        off += (int64_t)out * in;
+        L.b_off = off;
+        off += out;
+        return L;
+    };
+    for (int l = 0; l < c->L; ++l) t->actor.push_back(layer(c->dims[l + 1], c->dims[l]));
+    t->log_std_off = off;
+    off += c->A;
+    const auto &cr = c->critic;
+    for (int l = 0; l < cr.L - 1; ++l) t->critic.push_back(layer(cr.dims[l + 1], cr.dims[l]));
+    t->head_K = cr.dims[cr.L - 1];
+    t->head_w_off = off;
+    off += t->head_K;
+    t->head_b_off = off;
+    off += 1;
+    t->P = off;
+    t->Kp0 = (int)round_up(c->D, 128);
+    int maxw = 0;
+    for (auto *net : {&t->actor, &t->critic})
+        for (const TrainLayer &L : *net) maxw = std::max({maxw, L.Mp, L.Kp});
+    // allocations
+    const size_t P = (size_t)t->P;
+    if (!alloc(&t->x, 4 * P) || !alloc(&t->m, 4 * P) || !alloc(&t->v, 4 * P) || !alloc(&t->grad, 4 * P) ||
+        !alloc(&t->step, sizeof(int)) || !alloc(&t->opt, sizeof(im::OptScalars)))
+        return oom();
+    size_t sk = 0;
+    for (auto *net : {&t->actor, &t->critic}) {
+        for (size_t l = 0; l < net->size(); ++l) {
+            TrainLayer &L = (*net)[l];
+            const bool out_layer = net == &t->actor && l + 1 == net->size();
+            if (!alloc(&L.wt, (size_t)L.Mp * L.Kp * 2) || !alloc(&L.wtt, (size_t)L.Kp * L.Mp * 2) ||
+                !alloc(&L.bias, sizeof(float) * L.Mp))
+                return oom();
+            if (!out_layer && !alloc(&L.act, (size_t)L.Mp * Mb * 2)) return oom();
+            int S, ks;
+            splitk_plan((L.Mp / 128) * (L.Kp / 128), Mb, &S, &ks);
+            sk = std::max(sk, (size_t)S * L.Mp * L.Kp);
+        }
+    }
+    const int A = c->A;
+    const TrainLayer &al = t->actor.back();
+    if (!alloc(&t->x0, (size_t)t->Kp0 * Mb * 2) || !alloc(&t->act, 4 * (size_t)A * Mb) ||
+        !alloc(&t->mean_old, 4 * (size_t)A * Mb) || !alloc(&t->logp_old, 4 * (size_t)Mb) ||
+        !alloc(&t->adv, 4 * (size_t)Mb) || !alloc(&t->ret, 4 * (size_t)Mb) || !alloc(&t->vold, 4 * (size_t)Mb) ||
+        !alloc(&t->mean_new, 4 * (size_t)A * Mb) || !alloc(&t->value_new, 4 * (size_t)Mb) ||
+        !alloc(&t->dv, 4 * (size_t)Mb) || !alloc(&t->dmu, (size_t)al.Mp * Mb * 2) ||
+        !alloc(&t->dz[0], (size_t)maxw * Mb * 2) || !alloc(&t->dz[1], (size_t)maxw * Mb * 2) ||
+        !alloc(&t->splitk, 4 * sk) ||
+        !alloc(&t->loss_partial, sizeof(double) * (size_t)(Mb / 256) * (A + im::LOSS_STATS)) ||
+        !alloc(&t->mb_stats, sizeof(double) * im::LOSS_STATS) || !alloc(&t->log_std_old, 4 * (size_t)A))
+        return oom();
+    t->splitk_floats = sk;
+    t->norm_blocks = (int)std::min<int64_t>(1024, (t->P + 255) / 256);
+    if (!alloc(&t->norm_partial, sizeof(double) * t->norm_blocks)) return oom();
+    // the rollout copies the update refreshes
+    for (size_t l = 0; l < t->actor.size(); ++l) {
+        t->actor[l].roll = c->d_w[l];
+        t->actor[l].roll_K = c->K_pad[l];
+        t->actor[l].roll_bias = c->d_b[l];
+    }
+    for (size_t l = 0; l < t->critic.size(); ++l) {
+        t->critic[l].roll = cr.d_w[l];
+        t->critic[l].roll_K = cr.K_pad[l];
+        t->critic[l].roll_bias = cr.d_b[l];
+    }
+    // float32 masters from the current weights (bf16 values convert exactly)
+    std::vector<float> x(P, 0.0f);
+    auto unpack = [&](const void *dw, int M_pad_unused, int K_pad, const float *db, const TrainLayer &L) {
+        (void)M_pad_unused;
+        std::vector<uint16_t> w((size_t)L.out * K_pad);
+        std::vector<float> bb(L.out);
+        if (hipMemcpy(w.data(), dw, w.size() * 2, hipMemcpyDeviceToHost) != hipSuccess ||
+            hipMemcpy(bb.data(), db, 4 * bb.size(), hipMemcpyDeviceToHost) != hipSuccess)
+            return false;
+        for (int o = 0; o < L.out; ++o)
+            for (int i = 0; i < L.in; ++i) {
+                const uint32_t u = (uint32_t)w[(size_t)o * K_pad + i] << 16;
+                std::memcpy(&x[L.w_off + (int64_t)o * L.in + i], &u, 4);
+            }
+        std::memcpy(&x[L.b_off], bb.data(), 4 * bb.size());
+        return true;
+    };
+    bool ok = true;
+    for (size_t l = 0; l < t->actor.size() && ok; ++l)
+        ok = unpack(c->d_w[l], c->M_pad[l], c->K_pad[l], c->d_b[l], t->actor[l]);
+    for (size_t l = 0; l < t->critic.size() && ok; ++l)
+        ok = unpack(cr.d_w[l], cr.M_pad[l], cr.K_pad[l], cr.d_b[l], t->critic[l]);
+    ok = ok && hipMemcpy(&x[t->log_std_off], c->d_log_std, 4 * (size_t)A, hipMemcpyDeviceToHost) == hipSuccess;
+    ok = ok && hipMemcpy(&x[t->head_w_off], cr.d_head, 4 * (size_t)t->head_K, hipMemcpyDeviceToHost) == hipSuccess;
+    ok = ok && hipMemcpy(&x[t->head_b_off], cr.d_head + cr.K_head, 4, hipMemcpyDeviceToHost) == hipSuccess;
+    ok = ok && hipMemcpy(t->x, x.data(), 4 * P, hipMemcpyHostToDevice) == hipSuccess;
+    if (!ok) {
+        im::free_train(t);
+        return fail(IM_ERR_HIP, "initialise the master weights");
+    }
+    c->train = t;
+    s = repack_all(c, nullptr);
+    if (s == IM_OK && (e = hipDeviceSynchronize()) != hipSuccess) s = hip_fail(e, "training setup");
+    if (s != IM_OK) {
+        im::free_train(c->train);
+        c->train = nullptr;
+    }
+    return s;
+}
+
+im_status im_ppo_update(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p, void *stream)
+{
+    im_status s = check_ppo(c, b, p);
+    if (s != IM_OK) return s;
+    TrainState *t = c->train;
+    const hipStream_t st = (hipStream_t)stream;
+    IM_CHK(hipMemcpyAsync(t->log_std_old, t->x + t->log_std_off, 4 * (size_t)c->A,
+                          hipMemcpyDeviceToDevice, st));
+    im::FinalizeArgs f{};
+    f.norm_partial = t->norm_partial;
+    f.norm_blocks = t->norm_blocks;
+    f.mb_stats = t->mb_stats;
+    f.max_grad_norm = p->max_grad_norm;
+    f.desired_kl = p->desired_kl;
+    f.lr_min = p->lr_min;
+    f.lr_max = p->lr_max;
+    f.beta1 = p->beta1;
+    f.beta2 = p->beta2;
+    f.eps = p->eps;
+    f.lr = b->lr;
+    f.step = t->step;
+    f.opt = t->opt;
+    f.stats = b->stats;
+    for (int ep = 0; ep < p->epochs; ++ep)
+        for (int mb = 0; mb < p->minibatches; ++mb) {
+            IM_CHS(run_minibatch(c, b, p, ep, mb, st));
+            IM_CHK(im::launch_optimizer(t->grad, t->P, t->norm_partial, t->norm_blocks, f, t->x, t->m, t->v, st));
+            IM_CHS(repack_all(c, st));
+        }
+    return IM_OK;
+}
+
+im_status im_ppo_grad(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p, int32_t epoch,
+                      int32_t minibatch, float *grad, double *stats, void *stream)
+{
+    im_status s = check_ppo(c, b, p);
+    if (s != IM_OK) return s;
+    if (!grad) return fail(IM_ERR_INVALID_ARG, "NULL gradient buffer");
+    if (epoch < 0 || epoch >= p->epochs || minibatch < 0 || minibatch >= p->minibatches)
+        return fail(IM_ERR_INVALID_ARG, "epoch or minibatch out of range");
+    TrainState *t = c->train;
+    const hipStream_t st = (hipStream_t)stream;
+    IM_CHK(hipMemcpyAsync(t->log_std_old, t->x + t->log_std_off, 4 * (size_t)c->A,
+                          hipMemcpyDeviceToDevice, st));
+    IM_CHS(run_minibatch(c, b, p, epoch, minibatch, st));
+    IM_CHK(hipMemcpyAsync(grad, t->grad, 4 * (size_t)t->P, hipMemcpyDeviceToDevice, st));
+    if (stats)
+        IM_CHK(hipMemcpyAsync(stats, t->mb_stats, sizeof(double) * im::LOSS_STATS,
+                              hipMemcpyDeviceToDevice, st));
+    return IM_OK;
+}
+
+im_status im_ppo_params_get(im_ctx *c, float *params, int64_t *n, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    if (!c->train) return fail(IM_ERR_INVALID_ARG, "no training state (im_ppo_setup)");
+    if (n) *n = c->train->P;
+    if (params)
+        IM_CHK(hipMemcpyAsync(params, c->train->x, 4 * (size_t)c->train->P, hipMemcpyDeviceToDevice,
+                              (hipStream_t)stream));
+    return IM_OK;
+}
+
+}  // extern "C"
+#undef IM_CHK
+#undef IM_CHS

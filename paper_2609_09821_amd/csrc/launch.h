@@ -55,10 +55,115 @@ struct GaeArgs {
 };
 
 hipError_t launch_value_head_rows(bool bf16, const void *x, int64_t ld_x, int K, const float *w,
-                                  float bias, int64_t N, float *value, hipStream_t s);
-hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w, float bias,
-                                 bool bf16, int64_t N, float *value, hipStream_t s);
+                                  const float *bias, int64_t N, float *value, hipStream_t s);
+hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w,
+                                 const float *bias, bool bf16, int64_t N, float *value, hipStream_t s);
 hipError_t launch_gae(const GaeArgs &g, hipStream_t s);
+
+// PPO update (train_kernels.hip).
+enum { T_HIDDEN = 0, T_MASK = 1, T_LINEAR = 2, T_PARTIAL = 3 };
+
+// C[m][n] = sum_k A[m][k] B(k, n) over whole 128 x 128 tiles; M, N multiples
+// of 128, K and k_split of 64.
+struct TGemm {
+    const uint16_t *A;   // [M][lda] bf16, k contiguous
+    int64_t lda;
+    uint32_t a_bytes;
+    const uint16_t *B;   // k-major [K][ldb] (n contiguous) or n-major [N][ldb]
+    int64_t ldb;
+    uint32_t b_bytes;
+    int M, N, K, k_split;
+    void *C;             // bf16 [M][ldc] (HIDDEN, MASK), fp32 [M][ldc] (LINEAR),
+    int64_t ldc;         // fp32 [splits][M][ldc] (PARTIAL)
+    const float *bias;   // [M] (HIDDEN, LINEAR)
+    const uint16_t *mask;  // [M][ldm] bf16: the gradient passes where mask > 0 (MASK)
+    int64_t ldm;
+    int M_valid;         // LINEAR: rows written
+};
+
+struct GatherArgs {
+    const float *obs;        // [T+1][D][ld]
+    const float *action, *mean;  // [T][N][A]
+    const float *logp, *adv_src, *ret_src, *value;  // [T][ld] ([T+1][ld] value)
+    const int32_t *perm;     // chunk ids of this minibatch
+    int chunks, chunks_pad;  // chunks of the minibatch, chunks covering Mb_pad
+    int n_chunks;            // chunks of the rollout (perm entries are clamped to it)
+    int64_t cpt, N, ld, Mb_pad;
+    int D, K0, A;
+    uint16_t *x0;            // [K0][Mb_pad] bf16
+    float *act, *mean_old;   // [A][Mb_pad]
+    float *logp_old, *adv, *ret, *vold;  // [Mb_pad]
+};
+
+constexpr int LOSS_STATS = 4;   // surrogate loss, value loss, KL, clip fraction
+
+struct LossArgs {
+    int64_t Mb, Mb_pad;
+    int A;
+    int64_t n_samples;              // advantages of the whole rollout (normalisation)
+    const double *summary;          // IM_SUM_ADVANTAGE, IM_SUM_ADVANTAGE_SQ
+    const float *mean, *act, *mean_old;   // [A][Mb_pad]
+    const float *log_std, *log_std_old;   // [A]
+    const float *logp_old, *adv, *ret, *vold, *value;  // [Mb_pad]
+    float clip, value_coef;
+    int clipped_value_loss;
+    uint16_t *dmu;                  // [A][Mb_pad] bf16 out
+    float *dv;                      // [Mb_pad] out
+    double *partial;                // [blocks][A + LOSS_STATS]
+};
+
+struct LossReduceArgs {
+    const double *partial;
+    int blocks, A;
+    int64_t Mb;
+    float entropy_coef;
+    float *grad_log_std;   // [A]
+    double *mb_stats;      // [LOSS_STATS] minibatch means
+};
+
+struct OptScalars {
+    float scale, lr, bc1, bc2;
+};
+
+struct FinalizeArgs {
+    const double *norm_partial;
+    int norm_blocks;
+    const double *mb_stats;
+    float max_grad_norm, desired_kl, lr_min, lr_max, beta1, beta2, eps;
+    float *lr;             // device learning rate (adapted in place)
+    int *step;             // device Adam step count
+    OptScalars *opt;
+    double *stats;         // IM_PPO_* sums or null
+};
+
+struct RepackArgs {
+    const float *W, *b;    // masters [out][in], [out]
+    int out, in;
+    uint16_t *wt;          // [out..Mp][Kp] training copy or null
+    uint16_t *wtt;         // [Kp][Mp] transposed training copy or null
+    int Mp, Kp;
+    void *roll;            // rollout copy [.][roll_K] or null
+    int roll_K, roll_bf16; // 1: bf16, 2: fp32 of the bf16-rounded value, 0: fp32
+    float *bias_train, *bias_roll;
+};
+
+hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_t s);
+hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
+hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float *w, const float *b,
+                               float *v, hipStream_t s);
+hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
+                                const float *dv, uint16_t *dz, hipStream_t s);
+hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, float *out,
+                         hipStream_t s);
+hipError_t launch_splitk_reduce(const float *P, int S, int64_t M, int64_t N, int rows, int cols,
+                                float *out, hipStream_t s);
+hipError_t launch_loss(const LossArgs &a, hipStream_t s);
+hipError_t launch_loss_reduce(const LossReduceArgs &r, hipStream_t s);
+hipError_t launch_optimizer(const float *grad, int64_t P, double *norm_partial, int norm_blocks,
+                            const FinalizeArgs &f, float *x, float *m, float *v, hipStream_t s);
+hipError_t launch_norm(const float *grad, int64_t P, double *norm_partial, int norm_blocks,
+                       hipStream_t s);
+hipError_t launch_repack(const RepackArgs &r, hipStream_t s);
 
 hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s);

@@ -13,7 +13,7 @@
 namespace im {
 
 // ---------------------------------------------------------------------------
-// Value head, last layer: value[e] = b + sum_k w[k] x[e][k] over the last
+// Value head, last layer: value[e] = b[0] + sum_k w[k] x[e][k] over the last
 // hidden activations x [N][ld_x] (bf16 or fp32 rows, zero beyond the layer's
 // width).  16 lanes per env, each reading 16-byte pieces of the row (256
 // contiguous bytes per env and step of the loop); the 16 partial sums meet
@@ -23,8 +23,8 @@ template <bool BF16>
 __global__ __launch_bounds__(256) void value_head_rows_kernel(const void *__restrict__ x,
                                                               int64_t ld_x, int K,
                                                               const float *__restrict__ w,
-                                                              float bias, int64_t N,
-                                                              float *__restrict__ value)
+                                                              const float *__restrict__ bias,
+                                                              int64_t N, float *__restrict__ value)
 {
     constexpr int EPC = BF16 ? 8 : 4;   // elements per 16-byte piece
     const int sub = threadIdx.x & 15;
@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void value_head_rows_kernel(const void *__rest
     acc += __shfl_xor(acc, 4, 16);
     acc += __shfl_xor(acc, 2, 16);
     acc += __shfl_xor(acc, 1, 16);
-    if (e < N && sub == 0) value[e] = acc + bias;
+    if (e < N && sub == 0) value[e] = acc + bias[0];
 }
 
 // Value head of a one-layer critic: value[e] = b + sum_i w[i] obs[i][e] over
@@ -67,8 +67,8 @@ __global__ __launch_bounds__(256) void value_head_rows_kernel(const void *__rest
 __global__ __launch_bounds__(256) void value_head_obs_kernel(const float *__restrict__ obs,
                                                              int64_t ld, int D,
                                                              const float *__restrict__ w,
-                                                             float bias, int bf16, int64_t N,
-                                                             float *__restrict__ value)
+                                                             const float *__restrict__ bias, int bf16,
+                                                             int64_t N, float *__restrict__ value)
 {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= N) return;
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void value_head_obs_kernel(const float *__rest
         if (bf16) v = bf16_to_f32(f32_to_bf16_rne(v));
         acc += w[i] * v;
     }
-    value[e] = acc + bias;
+    value[e] = acc + bias[0];
 }
 
 // ---------------------------------------------------------------------------
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(256) void summary_reduce_kernel(const double *__res
 // Host-side launchers.
 // ---------------------------------------------------------------------------
 hipError_t launch_value_head_rows(bool bf16, const void *x, int64_t ld_x, int K, const float *w,
-                                  float bias, int64_t N, float *value, hipStream_t s)
+                                  const float *bias, int64_t N, float *value, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
     const dim3 grid((unsigned)((N + 15) / 16));
@@ -238,8 +238,8 @@ hipError_t launch_value_head_rows(bool bf16, const void *x, int64_t ld_x, int K,
     return hipGetLastError();
 }
 
-hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w, float bias,
-                                 bool bf16, int64_t N, float *value, hipStream_t s)
+hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w,
+                                 const float *bias, bool bf16, int64_t N, float *value, hipStream_t s)
 {
     if (N <= 0) return hipSuccess;
     hipLaunchKernelGGL(value_head_obs_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s,

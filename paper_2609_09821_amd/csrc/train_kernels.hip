@@ -1,0 +1,621 @@
+// train_kernels.hip -- the PPO update (the training loop's update_policy of
+// Fig. 3) for bf16 actor-critic MLPs: minibatch gather from the rollout
+// storage, forward and backward GEMMs on MFMA, the clipped-surrogate loss,
+// deterministic gradient reductions, global-norm clip, KL-adaptive learning
+// rate and Adam, all on the device with no host round trip.
+//
+// Layout: every activation and gradient is feature-major, [features][Mb]
+// with the minibatch's samples contiguous (bf16), so the MFMA accumulator
+// (one sample per lane, four consecutive features per register group) is
+// stored without a transpose, and all three products of a layer
+//   forward  Y^T  = W   X^T          (out x Mb)
+//   backward dX^T = W^T dZ^T         (in x Mb, masked by the ReLU)
+//   weights  dW   = dZ^T X           (out x in, reduced over the minibatch)
+// run on one GEMM kernel C[m][n] = sum_k A[m][k] B(k, n): A always has k
+// contiguous (weights, transposed weights, dZ^T), B either k-major [k][n]
+// (activations, gradients) or n-major [n][k] (X^T for the weight gradient).
+#include <hip/hip_runtime.h>
+
+#include "device_math.h"
+#include "launch.h"
+
+namespace im {
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4_v __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_v __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------------------
+// GEMM: 128 x 128 tiles of 4 waves (2 x 2, each 64 x 64 = 2 x 2 MFMA
+// 32x32x16 tiles), K step 64, two LDS stages; loads of stage k+2 are in
+// flight while stage k runs.  LDS rows of 72 bf16 (144 bytes): fragment
+// reads free of bank conflicts.  blockIdx.y splits K (weight gradients:
+// K = the minibatch).  All operands are zero-padded to whole tiles.
+// ---------------------------------------------------------------------------
+template <bool BT, int EPI>
+__global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
+{
+    constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
+    constexpr int STAGE = (BM + BN) * LDK;
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int mblocks = g.M / BM;
+    const int64_t m0 = (int64_t)(blockIdx.x % mblocks) * BM;
+    const int64_t n0 = (int64_t)(blockIdx.x / mblocks) * BN;
+    const int kb = blockIdx.y * g.k_split;
+    const int ke = kb + g.k_split < g.K ? kb + g.k_split : g.K;
+    const int nk = (ke - kb) / BK;
+
+    const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.A, (short)0, (int)g.a_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.B, (short)0, (int)g.b_bytes, 0x00020000);
+
+    // A (and B when n-major): 128 rows x 8 chunks of 16 bytes, 4 per thread
+    uint32_t a_off[4], b_off[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int v = tid + c * 256;
+        a_off[c] = (uint32_t)(((m0 + (v >> 3)) * g.lda + kb + (v & 7) * 8) * 2);
+        if constexpr (!BT) b_off[c] = (uint32_t)(((n0 + (v >> 3)) * g.ldb + kb + (v & 7) * 8) * 2);
+    }
+    // B k-major: thread = (8 consecutive k rows, 4 consecutive n), 8-byte loads
+    const int bq = tid & 31, bg = tid >> 5;
+    const uint32_t bt_off = (uint32_t)((((int64_t)kb + bg * 8) * g.ldb + n0 + bq * 4) * 2);
+    const uint32_t bt_row = (uint32_t)(g.ldb * 2);
+
+    u32x4_v ra[4], rb[4];
+    u32x2_v rt[8];
+    auto load_global = [&](int kt) {
+        const int kofs = kt * BK;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            ra[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(ar, a_off[c], kofs * 2, 0));
+        if constexpr (!BT) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                rb[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(br, b_off[c], kofs * 2, 0));
+        } else {
+            const uint32_t s = (uint32_t)kofs * bt_row;
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+                rt[r] = __builtin_bit_cast(u32x2_v, __builtin_amdgcn_raw_buffer_load_b64(br, bt_off + r * bt_row, s, 0));
+        }
+    };
+    auto store_lds = [&](int buf) {
+        uint16_t *As = lds + buf * STAGE;
+        uint16_t *Bs = As + BM * LDK;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int v = tid + c * 256;
+            *(u32x4_v *)(As + (v >> 3) * LDK + (v & 7) * 8) = ra[c];
+        }
+        if constexpr (!BT) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int v = tid + c * 256;
+                *(u32x4_v *)(Bs + (v >> 3) * LDK + (v & 7) * 8) = rb[c];
+            }
+        } else {
+            // sample bq*4+j gets the 8 consecutive k values bg*8..bg*8+7
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int half = j & 1, word = j >> 1;
+                u32x4_v w;
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    const uint32_t lo = rt[2 * p][word], hi = rt[2 * p + 1][word];
+                    w[p] = half ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+                }
+                *(u32x4_v *)(Bs + (bq * 4 + j) * LDK + bg * 8) = w;
+            }
+        }
+    };
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    auto compute = [&](int buf) {
+        const uint16_t *As = lds + buf * STAGE;
+        const uint16_t *Bs = As + BM * LDK;
+        const int arow = wm * 64 + (lane & 31);
+        const int brow = wn * 64 + (lane & 31);
+        const int kof = 8 * (lane >> 5);
+#pragma unroll
+        for (int s = 0; s < BK / 16; ++s) {
+            bf16x8_t a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    if (nk > 0) {
+        load_global(0);
+        store_lds(0);
+        __syncthreads();
+        if (nk > 1) load_global(1);
+        for (int kt = 0; kt < nk; ++kt) {
+            compute(kt & 1);
+            if (kt + 1 < nk) store_lds((kt + 1) & 1);
+            if (kt + 2 < nk) load_global(kt + 2);
+            __syncthreads();
+        }
+    }
+
+    // epilogue: lane (l & 31) holds sample column n, registers 4*grp + q the
+    // rows 8*grp + 4*(l >> 5) + q of each 32 x 32 tile
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int64_t m = m0 + wm * 64 + i * 32 + 8 * grp + 4 * (lane >> 5) + q;
+                    float v = acc[i][j][4 * grp + q];
+                    if constexpr (EPI == T_HIDDEN) {
+                        v = fmaxf(v + g.bias[m], 0.0f);
+                        ((uint16_t *)g.C)[m * g.ldc + n] = f32_to_bf16_rne(v);
+                    } else if constexpr (EPI == T_MASK) {
+                        const uint16_t h = g.mask[m * g.ldm + n];
+                        const bool on = h != 0 && (h & 0x8000u) == 0;
+                        ((uint16_t *)g.C)[m * g.ldc + n] = on ? f32_to_bf16_rne(v) : (uint16_t)0;
+                    } else if constexpr (EPI == T_LINEAR) {
+                        if (m < g.M_valid) ((float *)g.C)[m * g.ldc + n] = v + g.bias[m];
+                    } else {
+                        ((float *)g.C)[((int64_t)blockIdx.y * g.M + m) * g.ldc + n] = v;
+                    }
+                }
+        }
+}
+
+// ---------------------------------------------------------------------------
+// Minibatch gather.  Column j = 64 c + l of the minibatch is env e0 + l of
+// step t, where chunk c of the minibatch is q = perm[c]: t = q / (N/64),
+// e0 = 64 (q % (N/64)).  One wavefront per chunk; chunks past the
+// minibatch's end write zeros (padding columns).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
+{
+    const int lane = threadIdx.x & 63;
+    const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (c >= a.chunks_pad) return;
+    const int64_t j = (int64_t)c * 64 + lane;
+    const int64_t Mb = a.Mb_pad;
+    if (c >= a.chunks) {
+        for (int i = 0; i < a.K0; ++i) a.x0[i * Mb + j] = 0;
+        for (int k = 0; k < a.A; ++k) {
+            a.act[k * Mb + j] = 0.0f;
+            a.mean_old[k * Mb + j] = 0.0f;
+        }
+        a.logp_old[j] = 0.0f;
+        a.adv[j] = 0.0f;
+        a.ret[j] = 0.0f;
+        a.vold[j] = 0.0f;
+        return;
+    }
+    int q = a.perm[c];
+    q = q < 0 ? 0 : (q >= a.n_chunks ? a.n_chunks - 1 : q);   // memory safety only
+    const int64_t t = q / a.cpt;
+    const int64_t e = (int64_t)(q % a.cpt) * 64 + lane;
+    const float *o = a.obs + t * a.D * a.ld + e;
+    for (int i = 0; i < a.D; ++i) a.x0[i * Mb + j] = f32_to_bf16_rne(o[(int64_t)i * a.ld]);
+    for (int i = a.D; i < a.K0; ++i) a.x0[i * Mb + j] = 0;
+    const float *ac = a.action + (t * a.N + e) * a.A;
+    const float *mo = a.mean + (t * a.N + e) * a.A;
+    for (int k = 0; k < a.A; ++k) {
+        a.act[k * Mb + j] = ac[k];
+        a.mean_old[k * Mb + j] = mo[k];
+    }
+    const int64_t s = t * a.ld + e;
+    a.logp_old[j] = a.logp[s];
+    a.adv[j] = a.adv_src[s];
+    a.ret[j] = a.ret_src[s];
+    a.vold[j] = a.value[s];
+}
+
+// ---------------------------------------------------------------------------
+// Critic head (width-1 output layer) on feature-major activations.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void head_forward_kernel(const uint16_t *__restrict__ h, int K,
+                                                           int64_t Mb, const float *__restrict__ w,
+                                                           const float *__restrict__ b,
+                                                           float *__restrict__ v)
+{
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= Mb) return;
+    float acc = 0.0f;
+    for (int k = 0; k < K; ++k) acc += w[k] * bf16_to_f32(h[k * Mb + j]);
+    v[j] = acc + b[0];
+}
+
+// dZ^T[k][j] = w[k] dV[j] where h[k][j] > 0 (bf16), for the last hidden
+// layer; rows K..gridDim.y-1 (padding) are zero
+__global__ __launch_bounds__(256) void head_backward_kernel(const uint16_t *__restrict__ h, int K,
+                                                            int64_t Mb,
+                                                            const float *__restrict__ w,
+                                                            const float *__restrict__ dv,
+                                                            uint16_t *__restrict__ dz)
+{
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int k = blockIdx.y;
+    if (j >= Mb) return;
+    if (k >= K) {
+        dz[k * Mb + j] = 0;
+        return;
+    }
+    const uint16_t x = h[k * Mb + j];
+    const bool on = x != 0 && (x & 0x8000u) == 0;
+    dz[k * Mb + j] = on ? f32_to_bf16_rne(w[k] * dv[j]) : (uint16_t)0;
+}
+
+// ---------------------------------------------------------------------------
+// Per-row sums over the minibatch, float64 in a fixed order, one block per
+// row: out[r] = sum_j x[r][j] (x bf16 or fp32), optionally times y[j].
+// ---------------------------------------------------------------------------
+template <bool BF16>
+__global__ __launch_bounds__(256) void rowsum_kernel(const void *__restrict__ x, int64_t Mb,
+                                                     const float *__restrict__ y,
+                                                     float *__restrict__ out)
+{
+    __shared__ double red[256];
+    const int r = blockIdx.x;
+    double s = 0.0;
+    for (int64_t j = threadIdx.x; j < Mb; j += 256) {
+        const float v = BF16 ? bf16_to_f32(((const uint16_t *)x)[r * Mb + j]) : ((const float *)x)[r * Mb + j];
+        s += y ? (double)v * (double)y[j] : (double)v;
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[r] = (float)red[0];
+}
+
+// Weight gradient from the split-K partials: out[o][i] = sum_z P[z][o][i]
+// (z in order) for o < rows, i < cols.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restrict__ P, int S,
+                                                            int64_t M, int64_t N, int rows,
+                                                            int cols, float *__restrict__ out)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)rows * cols) return;
+    const int64_t o = idx / cols, i = idx % cols;
+    float s = 0.0f;
+    for (int z = 0; z < S; ++z) s += P[((int64_t)z * M + o) * N + i];
+    out[idx] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Loss: per sample, the clipped surrogate, value loss and KL; writes the
+// bf16 output-layer gradient dmu^T [A][Mb] (zero for padding columns), dV,
+// and per-block float64 partials: the log-std gradient (A) then the stats.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void loss_kernel(LossArgs a)
+{
+    __shared__ double red[256];
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t Mb = a.Mb_pad;
+    const bool live = j < a.Mb;
+    const double n = (double)a.n_samples;
+    const double amean = a.summary[IM_SUM_ADVANTAGE] / n;
+    const double avar = (a.summary[IM_SUM_ADVANTAGE_SQ] - a.summary[IM_SUM_ADVANTAGE] * amean) / (n - 1.0);
+    const double astd = sqrt(avar > 0.0 ? avar : 0.0);
+    const float inv_mb = 1.0f / (float)a.Mb;
+    float g_logp = 0.0f, l_pi = 0.0f, l_v = 0.0f, kl = 0.0f, clipped = 0.0f;
+    float logp = 0.0f, ratio = 1.0f;
+    if (live) {
+        for (int k = 0; k < a.A; ++k) {
+            const float ls = a.log_std[k];
+            const float sig = expf(ls);
+            const float d = a.act[k * Mb + j] - a.mean[k * Mb + j];
+            logp -= d * d / (2.0f * sig * sig) + ls + 0.91893853320467274f;
+        }
+        ratio = expf(logp - a.logp_old[j]);
+        const float A = (float)(((double)a.adv[j] - amean) / (astd + 1e-8));
+        const float rc = fminf(fmaxf(ratio, 1.0f - a.clip), 1.0f + a.clip);
+        const float s1 = -A * ratio, s2 = -A * rc;
+        l_pi = fmaxf(s1, s2);
+        g_logp = (s1 >= s2 ? -A * ratio : 0.0f) * inv_mb;
+        clipped = fabsf(ratio - 1.0f) > a.clip ? 1.0f : 0.0f;
+        // value loss
+        const float V = a.value[j], R = a.ret[j], Vo = a.vold[j];
+        float dv;
+        if (a.clipped_value_loss) {
+            const float dvo = V - Vo;
+            const float Vc = Vo + fminf(fmaxf(dvo, -a.clip), a.clip);
+            const float e1 = (V - R) * (V - R), e2 = (Vc - R) * (Vc - R);
+            l_v = fmaxf(e1, e2);
+            const bool inside = dvo > -a.clip && dvo < a.clip;
+            dv = e1 >= e2 ? 2.0f * (V - R) : (inside ? 2.0f * (Vc - R) : 0.0f);
+        } else {
+            l_v = (V - R) * (V - R);
+            dv = 2.0f * (V - R);
+        }
+        a.dv[j] = a.value_coef * dv * inv_mb;
+        for (int k = 0; k < a.A; ++k) {
+            const float ls = a.log_std[k], lso = a.log_std_old[k];
+            const float sig2 = expf(2.0f * ls), so2 = expf(2.0f * lso);
+            const float dm = a.mean_old[k * Mb + j] - a.mean[k * Mb + j];
+            kl += ls - lso + (so2 + dm * dm) / (2.0f * sig2) - 0.5f;
+        }
+    } else if (j < Mb) {
+        a.dv[j] = 0.0f;
+    }
+    if (j < Mb) {
+        for (int k = 0; k < a.A; ++k) {
+            float gm = 0.0f;
+            if (live) {
+                const float sig2 = expf(2.0f * a.log_std[k]);
+                gm = g_logp * (a.act[k * Mb + j] - a.mean[k * Mb + j]) / sig2;
+            }
+            a.dmu[k * Mb + j] = f32_to_bf16_rne(gm);
+        }
+    }
+    // block partials: log-std gradient per action, then the stats
+    const int nf = a.A + LOSS_STATS;
+    for (int f = 0; f < nf; ++f) {
+        double x = 0.0;
+        if (live) {
+            if (f < a.A) {
+                const float sig2 = expf(2.0f * a.log_std[f]);
+                const float d = a.act[f * Mb + j] - a.mean[f * Mb + j];
+                x = (double)g_logp * ((double)d * d / sig2 - 1.0);
+            } else {
+                const int s = f - a.A;
+                x = s == 0 ? l_pi : s == 1 ? l_v : s == 2 ? kl : clipped;
+            }
+        }
+        red[threadIdx.x] = x;
+        __syncthreads();
+        for (int h = 128; h > 0; h >>= 1) {
+            if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) a.partial[(int64_t)blockIdx.x * nf + f] = red[0];
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Optimizer.  norm_kernel: per-block float64 sums of g^2 over the flat
+// gradient.  finalize_kernel (one block): the minibatch's log-std gradient
+// (loss partials + entropy term) into the flat gradient, the loss stats,
+// the global norm and clip factor, the KL-adaptive learning rate, the Adam
+// step count and bias corrections.  adam_kernel: the step.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void norm_kernel(const float *__restrict__ g, int64_t P,
+                                                   double *__restrict__ partial)
+{
+    __shared__ double red[256];
+    double s = 0.0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < P; i += (int64_t)gridDim.x * 256)
+        s += (double)g[i] * (double)g[i];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
+}
+
+// the log-std gradient and loss stats of the minibatch from the loss partials
+__global__ __launch_bounds__(256) void loss_reduce_kernel(LossReduceArgs r)
+{
+    const int nf = r.A + LOSS_STATS;
+    const int f = threadIdx.x;
+    if (f >= nf) return;
+    double s = 0.0;
+    for (int b = 0; b < r.blocks; ++b) s += r.partial[(int64_t)b * nf + f];
+    if (f < r.A) {
+        r.grad_log_std[f] = (float)(s - (double)r.entropy_coef);
+    } else {
+        const int k = f - r.A;
+        const double mean = s / (double)r.Mb;
+        r.mb_stats[k] = mean;
+    }
+}
+
+__global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs f)
+{
+    __shared__ double red[256];
+    double s = 0.0;
+    for (int b = threadIdx.x; b < f.norm_blocks; b += 256) s += f.norm_partial[b];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x != 0) return;
+    const double norm = sqrt(red[0]);
+    double scale = 1.0;
+    if (f.max_grad_norm > 0.0f) {
+        const double coef = (double)f.max_grad_norm / (norm + 1e-6);
+        if (coef < 1.0) scale = coef;
+    }
+    const double kl = f.mb_stats[2];
+    float lr = *f.lr;
+    if (f.desired_kl > 0.0f) {
+        if (kl > 2.0 * f.desired_kl) lr = fmaxf(f.lr_min, lr / 1.5f);
+        else if (kl > 0.0 && kl < 0.5 * f.desired_kl) lr = fminf(f.lr_max, lr * 1.5f);
+    }
+    *f.lr = lr;
+    const int step = *f.step + 1;
+    *f.step = step;
+    f.opt->scale = (float)scale;
+    f.opt->lr = lr;
+    f.opt->bc1 = (float)(1.0 - pow((double)f.beta1, (double)step));
+    f.opt->bc2 = (float)(1.0 - pow((double)f.beta2, (double)step));
+    if (f.stats) {
+        f.stats[IM_PPO_LOSS_PI] += f.mb_stats[0];
+        f.stats[IM_PPO_LOSS_V] += f.mb_stats[1];
+        f.stats[IM_PPO_KL] += f.mb_stats[2];
+        f.stats[IM_PPO_CLIP_FRAC] += f.mb_stats[3];
+        f.stats[IM_PPO_GRAD_NORM] += norm;
+        f.stats[IM_PPO_MINIBATCHES] += 1.0;
+        f.stats[IM_PPO_LR] = (double)lr;
+    }
+}
+
+__global__ __launch_bounds__(256) void adam_kernel(float *__restrict__ x, float *__restrict__ m,
+                                                   float *__restrict__ v,
+                                                   const float *__restrict__ g, int64_t P,
+                                                   const OptScalars *__restrict__ o, float beta1,
+                                                   float beta2, float eps)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= P) return;
+    const float gi = g[i] * o->scale;
+    const float mi = beta1 * m[i] + (1.0f - beta1) * gi;
+    const float vi = beta2 * v[i] + (1.0f - beta2) * gi * gi;
+    m[i] = mi;
+    v[i] = vi;
+    x[i] -= o->lr * (mi / o->bc1) / (sqrtf(vi / o->bc2) + eps);
+}
+
+// ---------------------------------------------------------------------------
+// Weight refresh from the float32 masters: the training copies W [Mp][Kp]
+// and W^T [Kp][Mp] (bf16), and the rollout's packed copy [M_pad][K_pad]
+// (roll_bf16 1: bf16; 2: float32 holding the bf16-rounded value; 0:
+// float32) with its bias; padding stays zero.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void repack_kernel(RepackArgs r)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)r.out * r.in) return;
+    const int o = (int)(idx / r.in), i = (int)(idx % r.in);
+    const float w = r.W[idx];
+    const uint16_t h = f32_to_bf16_rne(w);
+    if (r.wt) r.wt[(int64_t)o * r.Kp + i] = h;
+    if (r.wtt) r.wtt[(int64_t)i * r.Mp + o] = h;
+    if (r.roll) {
+        if (r.roll_bf16 == 1) ((uint16_t *)r.roll)[(int64_t)o * r.roll_K + i] = h;
+        else if (r.roll_bf16 == 2) ((float *)r.roll)[(int64_t)o * r.roll_K + i] = bf16_to_f32(h);
+        else ((float *)r.roll)[(int64_t)o * r.roll_K + i] = w;
+    }
+    if (i == 0) {
+        if (r.bias_train) r.bias_train[o] = r.b[o];
+        if (r.bias_roll) r.bias_roll[o] = r.b[o];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers.
+// ---------------------------------------------------------------------------
+hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_t s)
+{
+    const dim3 grid((unsigned)((g.M / 128) * (g.N / 128)), (unsigned)splits);
+#define IM_TG(B, E) hipLaunchKernelGGL((tgemm_kernel<B, E>), grid, dim3(256), 0, s, g)
+    if (bt) {
+        if (epi == T_HIDDEN) IM_TG(true, T_HIDDEN);
+        else if (epi == T_MASK) IM_TG(true, T_MASK);
+        else if (epi == T_LINEAR) IM_TG(true, T_LINEAR);
+        else return hipErrorInvalidValue;
+    } else {
+        if (epi == T_PARTIAL) IM_TG(false, T_PARTIAL);
+        else return hipErrorInvalidValue;
+    }
+#undef IM_TG
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((a.chunks_pad + 3) / 4)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float *w, const float *b,
+                               float *v, hipStream_t s)
+{
+    hipLaunchKernelGGL(head_forward_kernel, dim3((unsigned)((Mb + 255) / 256)), dim3(256), 0, s, h, K,
+                       Mb, w, b, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
+                                const float *dv, uint16_t *dz, hipStream_t s)
+{
+    hipLaunchKernelGGL(head_backward_kernel, dim3((unsigned)((Mb + 255) / 256), (unsigned)rows), dim3(256),
+                       0, s, h, K, Mb, w, dv, dz);
+    return hipGetLastError();
+}
+
+hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, float *out,
+                         hipStream_t s)
+{
+    if (rows <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(rowsum_kernel<true>, dim3((unsigned)rows), dim3(256), 0, s, x, Mb, y, out);
+    else
+        hipLaunchKernelGGL(rowsum_kernel<false>, dim3((unsigned)rows), dim3(256), 0, s, x, Mb, y, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce(const float *P, int S, int64_t M, int64_t N, int rows, int cols,
+                                float *out, hipStream_t s)
+{
+    const int64_t n = (int64_t)rows * cols;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, P, S, M,
+                       N, rows, cols, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_loss(const LossArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)(a.Mb_pad / 256)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_loss_reduce(const LossReduceArgs &r, hipStream_t s)
+{
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, r);
+    return hipGetLastError();
+}
+
+hipError_t launch_optimizer(const float *grad, int64_t P, double *norm_partial, int norm_blocks,
+                            const FinalizeArgs &f, float *x, float *m, float *v, hipStream_t s)
+{
+    hipLaunchKernelGGL(norm_kernel, dim3((unsigned)norm_blocks), dim3(256), 0, s, grad, P, norm_partial);
+    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(256), 0, s, f);
+    hipLaunchKernelGGL(adam_kernel, dim3((unsigned)((P + 255) / 256)), dim3(256), 0, s, x, m, v, grad, P,
+                       f.opt, f.beta1, f.beta2, f.eps);
+    return hipGetLastError();
+}
+
+hipError_t launch_norm(const float *grad, int64_t P, double *norm_partial, int norm_blocks,
+                       hipStream_t s)
+{
+    hipLaunchKernelGGL(norm_kernel, dim3((unsigned)norm_blocks), dim3(256), 0, s, grad, P, norm_partial);
+    return hipGetLastError();
+}
+
+hipError_t launch_repack(const RepackArgs &r, hipStream_t s)
+{
+    const int64_t n = (int64_t)r.out * r.in;
+    hipLaunchKernelGGL(repack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, r);
+    return hipGetLastError();
+}
+
+}  // namespace im

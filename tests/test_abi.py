@@ -241,6 +241,15 @@ def test_calls_reject_null_context(lib):
             "NULL context")
     ro = binding.ImRollout()
     _expect(lib, lib.im_gae(None, C.byref(ro), None), binding.IM_ERR_INVALID_ARG, "NULL context")
+    pb, pp = binding.ImPpoBatch(), binding.ppo_params()
+    _expect(lib, lib.im_ppo_setup(None, 64), binding.IM_ERR_INVALID_ARG, "NULL context")
+    _expect(lib, lib.im_ppo_update(None, C.byref(pb), C.byref(pp), None), binding.IM_ERR_INVALID_ARG,
+            "NULL context")
+    _expect(lib, lib.im_ppo_grad(None, C.byref(pb), C.byref(pp), 0, 0, None, None, None),
+            binding.IM_ERR_INVALID_ARG, "NULL context")
+    n = C.c_int64()
+    _expect(lib, lib.im_ppo_params_get(None, None, C.byref(n), None), binding.IM_ERR_INVALID_ARG,
+            "NULL context")
     info = binding.ImInfo()
     _expect(lib, lib.im_get_info(None, C.byref(info)), binding.IM_ERR_INVALID_ARG, "NULL")
 
