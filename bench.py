@@ -46,20 +46,19 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # by what the same counter reads over a plain 512 MiB device copy (bench.py
 # --calibrate-copy 512): FETCH_SIZE reported 262167 KiB for 524288 KiB read, WRITE_SIZE
 # 524288 KiB for 524288 KiB written, so the factors are 2.0 and 1.0.  Each entry is keyed
-# by a hash of the kernel sources the counters were taken on; once a source changes the
-# figure no longer describes the kernel and the bench reports null.
+# by a hash of the kernel's source file and the device headers it includes; once one of
+# them changes the figure no longer describes the kernel and the bench reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 CSRC = os.path.join(ROOT, "paper_2609_09821_amd", "csrc")
-SHARED_SOURCES = [os.path.join(CSRC, f) for f in ("api.hip", "device_math.h", "launch.h", "tables.h")] + [
-    os.path.join(ROOT, "include", "instantmimic.h")]
+SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act, in order (observation
     # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip"], "sha": "4fe3c7f06e8b30ab", "workloads": {
-        4: {"fetch": [46220.7, 36498.4, 98970.0, 74236.7, 33543.5],
-            "write": [49152.1, 134546.3, 133763.8, 67931.2, 35584.0]}}},
-    "env": {"sources": ["env_kernels.hip"], "sha": "08b97772c0998dda", "workloads": {
-        4: {"fetch": [61772.2], "write": [169502.4]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "9490c8dfaa4f6815", "workloads": {
+        4: {"fetch": [46220.5, 36493.4, 98998.0, 74238.4, 33543.5],
+            "write": [49152.1, 134637.9, 133369.6, 68001.4, 35584.0]}}},
+    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "61d79f379ff6c0e4", "workloads": {
+        4: {"fetch": [61775.4], "write": [169487.7]}}},
 }
 
 
