@@ -1025,6 +1025,7 @@ struct TrainState {
     float *splitk = nullptr;
     size_t splitk_floats = 0;
     double *loss_partial = nullptr, *mb_stats = nullptr, *norm_partial = nullptr;
+    double *rowsum_part = nullptr;         // [rows][segments] of the bias-gradient sums
     int norm_blocks = 0;
     float *log_std_old = nullptr;
     std::vector<void *> allocs;
@@ -1140,7 +1141,7 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         g.ldc = L.Kp;
         IM_CHS(tg(false, im::T_PARTIAL, g, S, st));
         IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, L.Kp, L.out, L.in, t->grad + L.w_off, st));
-        IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->grad + L.b_off, st));
+        IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->rowsum_part, t->grad + L.b_off, st));
         if (l == 0) break;
         // dX^T = W^T dZ^T, masked where the layer input (a ReLU output) is 0
         im::TGemm h{};
@@ -1252,8 +1253,9 @@ im_status run_minibatch(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p
     IM_CHK(im::launch_loss_reduce(lr, st));
     // backward: actor from the output-layer gradient, critic from dV
     IM_CHS(net_backward(t, t->actor, t->x0, t->dmu, Mbp, st));
-    IM_CHK(im::launch_rowsum(true, hl.act, t->head_K, Mbp, t->dv, t->grad + t->head_w_off, st));
-    IM_CHK(im::launch_rowsum(false, t->dv, 1, Mbp, nullptr, t->grad + t->head_b_off, st));
+    IM_CHK(im::launch_rowsum(true, hl.act, t->head_K, Mbp, t->dv, t->rowsum_part, t->grad + t->head_w_off,
+                             st));
+    IM_CHK(im::launch_rowsum(false, t->dv, 1, Mbp, nullptr, t->rowsum_part, t->grad + t->head_b_off, st));
     IM_CHK(im::launch_head_backward(hl.act, t->head_K, hl.Mp, Mbp, head, t->dv, t->dz[0], st));
     IM_CHS(net_backward(t, t->critic, t->x0, t->dz[0], Mbp, st));
     return IM_OK;
@@ -1422,6 +1424,8 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     t->splitk_floats = sk;
     t->norm_blocks = (int)std::min<int64_t>(1024, (t->P + 255) / 256);
     if (!alloc(&t->norm_partial, sizeof(double) * t->norm_blocks)) return oom();
+    // row sums: rows x segments <= 2048 + rows for any row count
+    if (!alloc(&t->rowsum_part, sizeof(double) * (2048 + (size_t)maxw + 1))) return oom();
     // the rollout copies the update refreshes
     for (size_t l = 0; l < t->actor.size(); ++l) {
         t->actor[l].roll = c->d_w[l];

@@ -153,8 +153,9 @@ hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float
                                float *v, hipStream_t s);
 hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
                                 const float *dv, uint16_t *dz, hipStream_t s);
-hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, float *out,
-                         hipStream_t s);
+// part: [rows][up to 2048 / rows + 1] float64 scratch
+hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, double *part,
+                         float *out, hipStream_t s);
 hipError_t launch_splitk_reduce(const float *P, int S, int64_t M, int64_t N, int rows, int cols,
                                 float *out, hipStream_t s);
 hipError_t launch_loss(const LossArgs &a, hipStream_t s);

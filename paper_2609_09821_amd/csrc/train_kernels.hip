@@ -216,8 +216,16 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
     const int64_t t = q / a.cpt;
     const int64_t e = (int64_t)(q % a.cpt) * 64 + lane;
     const float *o = a.obs + t * a.D * a.ld + e;
-    for (int i = 0; i < a.D; ++i) a.x0[i * Mb + j] = f32_to_bf16_rne(o[(int64_t)i * a.ld]);
-    for (int i = a.D; i < a.K0; ++i) a.x0[i * Mb + j] = 0;
+    int i = 0;
+    for (; i + 8 <= a.D; i += 8) {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = o[(int64_t)(i + k) * a.ld];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a.x0[(i + k) * Mb + j] = f32_to_bf16_rne(v[k]);
+    }
+    for (; i < a.D; ++i) a.x0[i * Mb + j] = f32_to_bf16_rne(o[(int64_t)i * a.ld]);
+    for (; i < a.K0; ++i) a.x0[i * Mb + j] = 0;
     const float *ac = a.action + (t * a.N + e) * a.A;
     const float *mo = a.mean + (t * a.N + e) * a.A;
     for (int k = 0; k < a.A; ++k) {
@@ -267,20 +275,46 @@ __global__ __launch_bounds__(256) void head_backward_kernel(const uint16_t *__re
 }
 
 // ---------------------------------------------------------------------------
-// Per-row sums over the minibatch, float64 in a fixed order, one block per
-// row: out[r] = sum_j x[r][j] (x bf16 or fp32), optionally times y[j].
+// Per-row sums over the minibatch, float64 in a fixed order:
+// out[r] = sum_j x[r][j] (x bf16 or fp32), optionally times y[j].  Each row
+// is cut into `parts` segments (blockIdx.y), read in 16-byte pieces; the
+// segment sums are added in segment order by rowsum_finish_kernel.
 // ---------------------------------------------------------------------------
 template <bool BF16>
 __global__ __launch_bounds__(256) void rowsum_kernel(const void *__restrict__ x, int64_t Mb,
-                                                     const float *__restrict__ y,
-                                                     float *__restrict__ out)
+                                                     const float *__restrict__ y, int parts,
+                                                     double *__restrict__ part)
 {
     __shared__ double red[256];
-    const int r = blockIdx.x;
+    constexpr int E = BF16 ? 8 : 4;             // elements per 16-byte piece
+    const int r = blockIdx.x, seg = blockIdx.y;
+    const int64_t len = Mb / parts;             // Mb and len are multiples of 256
+    const int64_t j0 = seg * len;
     double s = 0.0;
-    for (int64_t j = threadIdx.x; j < Mb; j += 256) {
-        const float v = BF16 ? bf16_to_f32(((const uint16_t *)x)[r * Mb + j]) : ((const float *)x)[r * Mb + j];
-        s += y ? (double)v * (double)y[j] : (double)v;
+    for (int64_t j = j0 + (int64_t)threadIdx.x * E; j < j0 + len; j += 256 * E) {
+        float v[E];
+        if constexpr (BF16) {
+            const uint4 q = *(const uint4 *)((const uint16_t *)x + r * Mb + j);
+            const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                v[2 * k] = bf16_to_f32((uint16_t)(w[k] & 0xFFFF));
+                v[2 * k + 1] = bf16_to_f32((uint16_t)(w[k] >> 16));
+            }
+        } else {
+            const float4 q = *(const float4 *)((const float *)x + r * Mb + j);
+            v[0] = q.x;
+            v[1] = q.y;
+            v[2] = q.z;
+            v[3] = q.w;
+        }
+        if (y) {
+#pragma unroll
+            for (int k = 0; k < E; ++k) s += (double)v[k] * (double)y[j + k];
+        } else {
+#pragma unroll
+            for (int k = 0; k < E; ++k) s += (double)v[k];
+        }
     }
     red[threadIdx.x] = s;
     __syncthreads();
@@ -288,7 +322,17 @@ __global__ __launch_bounds__(256) void rowsum_kernel(const void *__restrict__ x,
         if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
         __syncthreads();
     }
-    if (threadIdx.x == 0) out[r] = (float)red[0];
+    if (threadIdx.x == 0) part[(int64_t)r * parts + seg] = red[0];
+}
+
+__global__ __launch_bounds__(256) void rowsum_finish_kernel(const double *__restrict__ part, int rows,
+                                                            int parts, float *__restrict__ out)
+{
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= rows) return;
+    double s = 0.0;
+    for (int k = 0; k < parts; ++k) s += part[(int64_t)r * parts + k];
+    out[r] = (float)s;
 }
 
 // Weight gradient from the split-K partials: out[o][i] = sum_z P[z][o][i]
@@ -419,14 +463,23 @@ __global__ __launch_bounds__(256) void norm_kernel(const float *__restrict__ g, 
     if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
 }
 
-// the log-std gradient and loss stats of the minibatch from the loss partials
+// the log-std gradient and loss stats of the minibatch from the loss
+// partials: one block per field, a fixed tree over the blocks' partials
 __global__ __launch_bounds__(256) void loss_reduce_kernel(LossReduceArgs r)
 {
+    __shared__ double red[256];
     const int nf = r.A + LOSS_STATS;
-    const int f = threadIdx.x;
-    if (f >= nf) return;
+    const int f = blockIdx.x;
     double s = 0.0;
-    for (int b = 0; b < r.blocks; ++b) s += r.partial[(int64_t)b * nf + f];
+    for (int b = threadIdx.x; b < r.blocks; b += 256) s += r.partial[(int64_t)b * nf + f];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x != 0) return;
+    s = red[0];
     if (f < r.A) {
         r.grad_log_std[f] = (float)(s - (double)r.entropy_coef);
     } else {
@@ -562,14 +615,20 @@ hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, 
     return hipGetLastError();
 }
 
-hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, float *out,
-                         hipStream_t s)
+hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, double *part,
+                         float *out, hipStream_t s)
 {
     if (rows <= 0) return hipSuccess;
+    // about 2048 blocks; segments of at least 2048 samples
+    int parts = (2048 + rows - 1) / rows;
+    while (parts > 1 && (Mb % ((int64_t)parts * 256) != 0 || Mb / parts < 2048)) --parts;
+    const dim3 grid((unsigned)rows, (unsigned)parts);
     if (bf16)
-        hipLaunchKernelGGL(rowsum_kernel<true>, dim3((unsigned)rows), dim3(256), 0, s, x, Mb, y, out);
+        hipLaunchKernelGGL(rowsum_kernel<true>, grid, dim3(256), 0, s, x, Mb, y, parts, part);
     else
-        hipLaunchKernelGGL(rowsum_kernel<false>, dim3((unsigned)rows), dim3(256), 0, s, x, Mb, y, out);
+        hipLaunchKernelGGL(rowsum_kernel<false>, grid, dim3(256), 0, s, x, Mb, y, parts, part);
+    hipLaunchKernelGGL(rowsum_finish_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, part,
+                       rows, parts, out);
     return hipGetLastError();
 }
 
@@ -590,7 +649,7 @@ hipError_t launch_loss(const LossArgs &a, hipStream_t s)
 
 hipError_t launch_loss_reduce(const LossReduceArgs &r, hipStream_t s)
 {
-    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, r);
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3((unsigned)(r.A + LOSS_STATS)), dim3(256), 0, s, r);
     return hipGetLastError();
 }
 
