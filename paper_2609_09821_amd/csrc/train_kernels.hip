@@ -25,19 +25,29 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4_v __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_v __attribute__((ext_vector_type(2)));
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+#define IM_LDS3 __attribute__((address_space(3)))
 
 // ---------------------------------------------------------------------------
 // GEMM: 128 x 128 tiles of 4 waves (2 x 2, each 64 x 64 = 2 x 2 MFMA
 // 32x32x16 tiles), K step 64, two LDS stages; loads of stage k+2 are in
-// flight while stage k runs.  LDS rows of 72 bf16 (144 bytes): fragment
-// reads free of bank conflicts.  blockIdx.y splits K (weight gradients:
-// K = the minibatch).  All operands are zero-padded to whole tiles.
+// flight while stage k runs.  k-contiguous operands sit in LDS rows of 72
+// bf16 (144 bytes: fragment reads free of bank conflicts).  A k-major B tile
+// is stored as it lies in memory, [64 k][128 n] in rows of 144 bf16, and its
+// MFMA fragments are read with the LDS transpose read: in every 16-lane
+// group, lane 4j+q addresses row k0+j, columns n0+4q..n0+4q+3, and lane l
+// receives rows k0..k0+3 of column n0+l (two reads give the 8 consecutive k
+// of a bf16 fragment; the 32-byte row shift of the padding keeps a group's
+// four rows on distinct banks).  blockIdx.y splits K (weight gradients: K =
+// the minibatch).  All operands are zero-padded to whole tiles.
 // ---------------------------------------------------------------------------
 template <bool BT, int EPI>
 __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
 {
     constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
-    constexpr int STAGE = (BM + BN) * LDK;
+    constexpr int LDN = BN + 16;                // k-major B rows (bf16)
+    static_assert(BK * LDN <= BN * LDK + BK * 16, "stage size");
+    constexpr int STAGE = BM * LDK + (BT ? BK * LDN : BN * LDK);
     __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -62,13 +72,16 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
         a_off[c] = (uint32_t)(((m0 + (v >> 3)) * g.lda + kb + (v & 7) * 8) * 2);
         if constexpr (!BT) b_off[c] = (uint32_t)(((n0 + (v >> 3)) * g.ldb + kb + (v & 7) * 8) * 2);
     }
-    // B k-major: thread = (8 consecutive k rows, 4 consecutive n), 8-byte loads
-    const int bq = tid & 31, bg = tid >> 5;
-    const uint32_t bt_off = (uint32_t)((((int64_t)kb + bg * 8) * g.ldb + n0 + bq * 4) * 2);
+    // B k-major: 64 rows x 16 chunks of 8 samples, 4 per thread
+    uint32_t bt_off[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int v = tid + c * 256;
+        bt_off[c] = (uint32_t)((((int64_t)kb + (v >> 4)) * g.ldb + n0 + (v & 15) * 8) * 2);
+    }
     const uint32_t bt_row = (uint32_t)(g.ldb * 2);
 
     u32x4_v ra[4], rb[4];
-    u32x2_v rt[8];
     auto load_global = [&](int kt) {
         const int kofs = kt * BK;
 #pragma unroll
@@ -81,8 +94,8 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
         } else {
             const uint32_t s = (uint32_t)kofs * bt_row;
 #pragma unroll
-            for (int r = 0; r < 8; ++r)
-                rt[r] = __builtin_bit_cast(u32x2_v, __builtin_amdgcn_raw_buffer_load_b64(br, bt_off + r * bt_row, s, 0));
+            for (int c = 0; c < 4; ++c)
+                rb[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(br, bt_off[c], s, 0));
         }
     };
     auto store_lds = [&](int buf) {
@@ -100,17 +113,10 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
                 *(u32x4_v *)(Bs + (v >> 3) * LDK + (v & 7) * 8) = rb[c];
             }
         } else {
-            // sample bq*4+j gets the 8 consecutive k values bg*8..bg*8+7
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int half = j & 1, word = j >> 1;
-                u32x4_v w;
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    const uint32_t lo = rt[2 * p][word], hi = rt[2 * p + 1][word];
-                    w[p] = half ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-                }
-                *(u32x4_v *)(Bs + (bq * 4 + j) * LDK + bg * 8) = w;
+            for (int c = 0; c < 4; ++c) {
+                const int v = tid + c * 256;
+                *(u32x4_v *)(Bs + (v >> 4) * LDN + (v & 15) * 8) = rb[c];
             }
         }
     };
@@ -123,6 +129,10 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+    // transpose-read addressing of the k-major B fragments (see above):
+    // 16-lane group gi covers columns 16 (gi & 1).. and k rows 8 (gi >> 1)..
+    const int gi = lane >> 4, si = lane & 15;
+    const int tr_off = (8 * (gi >> 1) + (si >> 2)) * LDN + 16 * (gi & 1) + 4 * (si & 3);
     auto compute = [&](int buf) {
         const uint16_t *As = lds + buf * STAGE;
         const uint16_t *Bs = As + BM * LDK;
@@ -135,7 +145,17 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
 #pragma unroll
             for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+            for (int j = 0; j < 2; ++j) {
+                if constexpr (!BT) {
+                    b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
+                } else {
+                    const uint16_t *p = Bs + (s * 16) * LDN + wn * 64 + j * 32 + tr_off;
+                    const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((IM_LDS3 v4s_t *)p);
+                    const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((IM_LDS3 v4s_t *)(p + 4 * LDN));
+                    const short v8[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    b[j] = __builtin_bit_cast(bf16x8_t, v8);
+                }
+            }
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
