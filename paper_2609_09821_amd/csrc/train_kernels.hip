@@ -179,31 +179,69 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
 
     // epilogue: lane (l & 31) holds sample column n, registers 4*grp + q the
     // rows 8*grp + 4*(l >> 5) + q of each 32 x 32 tile
+    if constexpr (EPI == T_HIDDEN || EPI == T_MASK) {
+        // bf16 tile staged in LDS as [m][n] (rows of BN + 8), then written in
+        // 16-byte row pieces; the ReLU mask is read the same way
+        constexpr int LDO = BN + 8;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+            for (int j = 0; j < 2; ++j) {
+                const int nl = wn * 64 + j * 32 + (lane & 31);
 #pragma unroll
-            for (int grp = 0; grp < 4; ++grp)
+                for (int grp = 0; grp < 4; ++grp)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int64_t m = m0 + wm * 64 + i * 32 + 8 * grp + 4 * (lane >> 5) + q;
-                    float v = acc[i][j][4 * grp + q];
-                    if constexpr (EPI == T_HIDDEN) {
-                        v = fmaxf(v + g.bias[m], 0.0f);
-                        ((uint16_t *)g.C)[m * g.ldc + n] = f32_to_bf16_rne(v);
-                    } else if constexpr (EPI == T_MASK) {
-                        const uint16_t h = g.mask[m * g.ldm + n];
-                        const bool on = h != 0 && (h & 0x8000u) == 0;
-                        ((uint16_t *)g.C)[m * g.ldc + n] = on ? f32_to_bf16_rne(v) : (uint16_t)0;
-                    } else if constexpr (EPI == T_LINEAR) {
-                        if (m < g.M_valid) ((float *)g.C)[m * g.ldc + n] = v + g.bias[m];
-                    } else {
-                        ((float *)g.C)[((int64_t)blockIdx.y * g.M + m) * g.ldc + n] = v;
+                    for (int q = 0; q < 4; ++q) {
+                        const int ml = wm * 64 + i * 32 + 8 * grp + 4 * (lane >> 5) + q;
+                        float v = acc[i][j][4 * grp + q];
+                        if constexpr (EPI == T_HIDDEN) v = fmaxf(v + g.bias[m0 + ml], 0.0f);
+                        lds[ml * LDO + nl] = f32_to_bf16_rne(v);
                     }
+            }
+        __syncthreads();
+        // 128 rows x 16 pieces of 8 samples: 8 pieces per thread
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const int v = tid + c * 256;
+            const int ml = v >> 4, pc = v & 15;
+            uint4 o = *(const uint4 *)(lds + ml * LDO + pc * 8);
+            const int64_t off = (m0 + ml) * g.ldc + n0 + pc * 8;
+            if constexpr (EPI == T_MASK) {
+                const uint4 h = *(const uint4 *)(g.mask + (m0 + ml) * g.ldm + n0 + pc * 8);
+                const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
+                uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // keep each half where the activation (bf16) is > 0
+                    const uint32_t lo = hw[k] & 0xFFFFu, hi = hw[k] >> 16;
+                    const uint32_t keep = ((lo != 0 && !(lo & 0x8000u)) ? 0x0000FFFFu : 0u) |
+                                          ((hi != 0 && !(hi & 0x8000u)) ? 0xFFFF0000u : 0u);
+                    ow[k] &= keep;
                 }
+                o = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+            }
+            *(uint4 *)((uint16_t *)g.C + off) = o;
         }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int64_t m = m0 + wm * 64 + i * 32 + 8 * grp + 4 * (lane >> 5) + q;
+                        const float v = acc[i][j][4 * grp + q];
+                        if constexpr (EPI == T_LINEAR) {
+                            if (m < g.M_valid) ((float *)g.C)[m * g.ldc + n] = v + g.bias[m];
+                        } else {
+                            ((float *)g.C)[((int64_t)blockIdx.y * g.M + m) * g.ldc + n] = v;
+                        }
+                    }
+            }
+    }
 }
 
 // ---------------------------------------------------------------------------
