@@ -41,17 +41,19 @@ typedef short v4s_t __attribute__((ext_vector_type(4)));
 // four rows on distinct banks).  blockIdx.y splits K (weight gradients: K =
 // the minibatch).  All operands are zero-padded to whole tiles.
 // ---------------------------------------------------------------------------
-template <bool BT, int EPI>
-__global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
+template <bool BT, int EPI, int WM>
+__global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 {
-    constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
+    // WM x 2 waves, each 64 x 64; tile BM x 128
+    constexpr int NT = 128 * WM;
+    constexpr int BM = 64 * WM, BN = 128, BK = 64, LDK = BK + 8;
     constexpr int LDN = BN + 16;                // k-major B rows (bf16)
     static_assert(BK * LDN <= BN * LDK + BK * 16, "stage size");
     constexpr int STAGE = BM * LDK + (BT ? BK * LDN : BN * LDK);
     __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave >> 1, wn = wave & 1;   // wave: 64 x 64 of the tile
     const int mblocks = g.M / BM;
     const int64_t m0 = (int64_t)(blockIdx.x % mblocks) * BM;
     const int64_t n0 = (int64_t)(blockIdx.x / mblocks) * BN;
@@ -64,60 +66,47 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
     const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.B, (short)0, (int)g.b_bytes, 0x00020000);
 
-    // A (and B when n-major): 128 rows x 8 chunks of 16 bytes, 4 per thread
-    uint32_t a_off[4], b_off[4];
+    // A: BM rows x 8 chunks of 16 bytes; B: 128 rows x 8 chunks (n-major) or
+    // 64 rows x 16 chunks of 8 samples (k-major)
+    constexpr int AC = BM * 8 / NT, BC = 1024 / NT;
+    uint32_t a_off[AC], b_off[BC];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const int v = tid + c * 256;
+    for (int c = 0; c < AC; ++c) {
+        const int v = tid + c * NT;
         a_off[c] = (uint32_t)(((m0 + (v >> 3)) * g.lda + kb + (v & 7) * 8) * 2);
-        if constexpr (!BT) b_off[c] = (uint32_t)(((n0 + (v >> 3)) * g.ldb + kb + (v & 7) * 8) * 2);
     }
-    // B k-major: 64 rows x 16 chunks of 8 samples, 4 per thread
-    uint32_t bt_off[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const int v = tid + c * 256;
-        bt_off[c] = (uint32_t)((((int64_t)kb + (v >> 4)) * g.ldb + n0 + (v & 15) * 8) * 2);
+    for (int c = 0; c < BC; ++c) {
+        const int v = tid + c * NT;
+        if constexpr (!BT) b_off[c] = (uint32_t)(((n0 + (v >> 3)) * g.ldb + kb + (v & 7) * 8) * 2);
+        else b_off[c] = (uint32_t)((((int64_t)kb + (v >> 4)) * g.ldb + n0 + (v & 15) * 8) * 2);
     }
     const uint32_t bt_row = (uint32_t)(g.ldb * 2);
 
-    u32x4_v ra[4], rb[4];
+    u32x4_v ra[AC], rb[BC];
     auto load_global = [&](int kt) {
         const int kofs = kt * BK;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < AC; ++c)
             ra[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(ar, a_off[c], kofs * 2, 0));
-        if constexpr (!BT) {
+        const uint32_t s = BT ? (uint32_t)kofs * bt_row : (uint32_t)kofs * 2;
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-                rb[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(br, b_off[c], kofs * 2, 0));
-        } else {
-            const uint32_t s = (uint32_t)kofs * bt_row;
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                rb[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(br, bt_off[c], s, 0));
-        }
+        for (int c = 0; c < BC; ++c)
+            rb[c] = __builtin_bit_cast(u32x4_v, __builtin_amdgcn_raw_buffer_load_b128(br, b_off[c], s, 0));
     };
     auto store_lds = [&](int buf) {
         uint16_t *As = lds + buf * STAGE;
         uint16_t *Bs = As + BM * LDK;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int v = tid + c * 256;
+        for (int c = 0; c < AC; ++c) {
+            const int v = tid + c * NT;
             *(u32x4_v *)(As + (v >> 3) * LDK + (v & 7) * 8) = ra[c];
         }
-        if constexpr (!BT) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int v = tid + c * 256;
-                *(u32x4_v *)(Bs + (v >> 3) * LDK + (v & 7) * 8) = rb[c];
-            }
-        } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int v = tid + c * 256;
-                *(u32x4_v *)(Bs + (v >> 4) * LDN + (v & 15) * 8) = rb[c];
-            }
+        for (int c = 0; c < BC; ++c) {
+            const int v = tid + c * NT;
+            if constexpr (!BT) *(u32x4_v *)(Bs + (v >> 3) * LDK + (v & 7) * 8) = rb[c];
+            else *(u32x4_v *)(Bs + (v >> 4) * LDN + (v & 15) * 8) = rb[c];
         }
     };
 
@@ -199,10 +188,10 @@ __global__ __launch_bounds__(256) void tgemm_kernel(TGemm g)
                     }
             }
         __syncthreads();
-        // 128 rows x 16 pieces of 8 samples: 8 pieces per thread
+        // BM rows x 16 pieces of 8 samples
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            const int v = tid + c * 256;
+        for (int c = 0; c < BM * 16 / NT; ++c) {
+            const int v = tid + c * NT;
             const int ml = v >> 4, pc = v & 15;
             uint4 o = *(const uint4 *)(lds + ml * LDO + pc * 8);
             const int64_t off = (m0 + ml) * g.ldc + n0 + pc * 8;
@@ -636,8 +625,15 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackArgs r)
 // ---------------------------------------------------------------------------
 hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_t s)
 {
-    const dim3 grid((unsigned)((g.M / 128) * (g.N / 128)), (unsigned)splits);
-#define IM_TG(B, E) hipLaunchKernelGGL((tgemm_kernel<B, E>), grid, dim3(256), 0, s, g)
+    // 256-row tiles of 8 waves where M allows, else 128-row tiles of 4
+    const bool big = g.M % 256 == 0;
+    const int bm = big ? 256 : 128;
+    const dim3 grid((unsigned)((g.M / bm) * (g.N / 128)), (unsigned)splits);
+#define IM_TG(B, E)                                                                            \
+    do {                                                                                      \
+        if (big) hipLaunchKernelGGL((tgemm_kernel<B, E, 4>), grid, dim3(512), 0, s, g);       \
+        else hipLaunchKernelGGL((tgemm_kernel<B, E, 2>), grid, dim3(256), 0, s, g);           \
+    } while (0)
     if (bt) {
         if (epi == T_HIDDEN) IM_TG(true, T_HIDDEN);
         else if (epi == T_MASK) IM_TG(true, T_MASK);
