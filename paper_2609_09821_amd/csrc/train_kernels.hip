@@ -41,12 +41,13 @@ typedef short v4s_t __attribute__((ext_vector_type(4)));
 // four rows on distinct banks).  blockIdx.y splits K (weight gradients: K =
 // the minibatch).  All operands are zero-padded to whole tiles.
 // ---------------------------------------------------------------------------
-template <bool BT, int EPI, int WM>
+template <bool BT, int EPI, int WM, int BN>
 __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 {
-    // WM x 2 waves, each 64 x 64; tile BM x 128
+    // WM x 2 waves, each 64 x BN/2 (TN = BN/64 MFMA tiles across); tile BM x BN
     constexpr int NT = 128 * WM;
-    constexpr int BM = 64 * WM, BN = 128, BK = 64, LDK = BK + 8;
+    constexpr int TN = BN / 64;
+    constexpr int BM = 64 * WM, BK = 64, LDK = BK + 8;
     constexpr int LDN = BN + 16;                // k-major B rows (bf16)
     static_assert(BK * LDN <= BN * LDK + BK * 16, "stage size");
     constexpr int STAGE = BM * LDK + (BT ? BK * LDN : BN * LDK);
@@ -66,9 +67,10 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
     const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.B, (short)0, (int)g.b_bytes, 0x00020000);
 
-    // A: BM rows x 8 chunks of 16 bytes; B: 128 rows x 8 chunks (n-major) or
-    // 64 rows x 16 chunks of 8 samples (k-major)
-    constexpr int AC = BM * 8 / NT, BC = 1024 / NT;
+    // A: BM rows x 8 chunks of 16 bytes; B: BN rows x 8 chunks (n-major) or
+    // 64 rows x BN/8 chunks of 8 samples (k-major)
+    constexpr int AC = BM * 8 / NT, BC = BN * 8 / NT;
+    constexpr int BQ = BN / 8;                  // k-major chunks per row
     uint32_t a_off[AC], b_off[BC];
 #pragma unroll
     for (int c = 0; c < AC; ++c) {
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
     for (int c = 0; c < BC; ++c) {
         const int v = tid + c * NT;
         if constexpr (!BT) b_off[c] = (uint32_t)(((n0 + (v >> 3)) * g.ldb + kb + (v & 7) * 8) * 2);
-        else b_off[c] = (uint32_t)((((int64_t)kb + (v >> 4)) * g.ldb + n0 + (v & 15) * 8) * 2);
+        else b_off[c] = (uint32_t)((((int64_t)kb + v / BQ) * g.ldb + n0 + (v % BQ) * 8) * 2);
     }
     const uint32_t bt_row = (uint32_t)(g.ldb * 2);
 
@@ -106,39 +108,40 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
         for (int c = 0; c < BC; ++c) {
             const int v = tid + c * NT;
             if constexpr (!BT) *(u32x4_v *)(Bs + (v >> 3) * LDK + (v & 7) * 8) = rb[c];
-            else *(u32x4_v *)(Bs + (v >> 4) * LDN + (v & 15) * 8) = rb[c];
+            else *(u32x4_v *)(Bs + (v / BQ) * LDN + (v % BQ) * 8) = rb[c];
         }
     };
 
-    f32x16_t acc[2][2];
+    f32x16_t acc[2][TN];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     // transpose-read addressing of the k-major B fragments (see above):
     // 16-lane group gi covers columns 16 (gi & 1).. and k rows 8 (gi >> 1)..
     const int gi = lane >> 4, si = lane & 15;
+    static_assert(BM * (BN + 8) <= 2 * STAGE, "epilogue tile fits the stages");
     const int tr_off = (8 * (gi >> 1) + (si >> 2)) * LDN + 16 * (gi & 1) + 4 * (si & 3);
     auto compute = [&](int buf) {
         const uint16_t *As = lds + buf * STAGE;
         const uint16_t *Bs = As + BM * LDK;
         const int arow = wm * 64 + (lane & 31);
-        const int brow = wn * 64 + (lane & 31);
+        const int brow = wn * (BN / 2) + (lane & 31);
         const int kof = 8 * (lane >> 5);
 #pragma unroll
         for (int s = 0; s < BK / 16; ++s) {
-            bf16x8_t a[2], b[2];
+            bf16x8_t a[2], b[TN];
 #pragma unroll
             for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8_t *)(As + (arow + i * 32) * LDK + s * 16 + kof);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
+            for (int j = 0; j < TN; ++j) {
                 if constexpr (!BT) {
                     b[j] = *(const bf16x8_t *)(Bs + (brow + j * 32) * LDK + s * 16 + kof);
                 } else {
-                    const uint16_t *p = Bs + (s * 16) * LDN + wn * 64 + j * 32 + tr_off;
+                    const uint16_t *p = Bs + (s * 16) * LDN + wn * (BN / 2) + j * 32 + tr_off;
                     const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((IM_LDS3 v4s_t *)p);
                     const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((IM_LDS3 v4s_t *)(p + 4 * LDN));
                     const short v8[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -148,7 +151,7 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     };
@@ -175,8 +178,8 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int nl = wn * 64 + j * 32 + (lane & 31);
+            for (int j = 0; j < TN; ++j) {
+                const int nl = wn * (BN / 2) + j * 32 + (lane & 31);
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp)
 #pragma unroll
@@ -188,11 +191,11 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
                     }
             }
         __syncthreads();
-        // BM rows x 16 pieces of 8 samples
+        // BM rows x BN/8 pieces of 8 samples
 #pragma unroll
-        for (int c = 0; c < BM * 16 / NT; ++c) {
+        for (int c = 0; c < BM * BQ / NT; ++c) {
             const int v = tid + c * NT;
-            const int ml = v >> 4, pc = v & 15;
+            const int ml = v / BQ, pc = v % BQ;
             uint4 o = *(const uint4 *)(lds + ml * LDO + pc * 8);
             const int64_t off = (m0 + ml) * g.ldc + n0 + pc * 8;
             if constexpr (EPI == T_MASK) {
@@ -215,8 +218,8 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+            for (int j = 0; j < TN; ++j) {
+                const int64_t n = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp)
 #pragma unroll
@@ -625,14 +628,16 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackArgs r)
 // ---------------------------------------------------------------------------
 hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_t s)
 {
-    // 256-row tiles of 8 waves where M allows, else 128-row tiles of 4
-    const bool big = g.M % 256 == 0;
-    const int bm = big ? 256 : 128;
-    const dim3 grid((unsigned)((g.M / bm) * (g.N / 128)), (unsigned)splits);
+    // 256-row tiles of 8 waves and 256-column tiles where the shape allows
+    const bool bigm = g.M % 256 == 0, bign = g.N % 256 == 0;
+    const int bm = bigm ? 256 : 128, bn = bign ? 256 : 128;
+    const dim3 grid((unsigned)((g.M / bm) * (g.N / bn)), (unsigned)splits);
 #define IM_TG(B, E)                                                                            \
     do {                                                                                      \
-        if (big) hipLaunchKernelGGL((tgemm_kernel<B, E, 4>), grid, dim3(512), 0, s, g);       \
-        else hipLaunchKernelGGL((tgemm_kernel<B, E, 2>), grid, dim3(256), 0, s, g);           \
+        if (bigm && bign) hipLaunchKernelGGL((tgemm_kernel<B, E, 4, 256>), grid, dim3(512), 0, s, g); \
+        else if (bigm) hipLaunchKernelGGL((tgemm_kernel<B, E, 4, 128>), grid, dim3(512), 0, s, g);    \
+        else if (bign) hipLaunchKernelGGL((tgemm_kernel<B, E, 2, 256>), grid, dim3(256), 0, s, g);    \
+        else hipLaunchKernelGGL((tgemm_kernel<B, E, 2, 128>), grid, dim3(256), 0, s, g);              \
     } while (0)
     if (bt) {
         if (epi == T_HIDDEN) IM_TG(true, T_HIDDEN);
