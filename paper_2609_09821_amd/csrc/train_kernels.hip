@@ -305,23 +305,35 @@ __global__ __launch_bounds__(256) void head_forward_kernel(const uint16_t *__res
 }
 
 // dZ^T[k][j] = w[k] dV[j] where h[k][j] > 0 (bf16), for the last hidden
-// layer; rows K..gridDim.y-1 (padding) are zero
+// layer; rows K..gridDim.y-1 (padding) are zero.  8 samples per thread.
 __global__ __launch_bounds__(256) void head_backward_kernel(const uint16_t *__restrict__ h, int K,
                                                             int64_t Mb,
                                                             const float *__restrict__ w,
                                                             const float *__restrict__ dv,
                                                             uint16_t *__restrict__ dz)
 {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
     const int k = blockIdx.y;
     if (j >= Mb) return;
+    uint4 *out = (uint4 *)(dz + k * Mb + j);
     if (k >= K) {
-        dz[k * Mb + j] = 0;
+        *out = make_uint4(0u, 0u, 0u, 0u);
         return;
     }
-    const uint16_t x = h[k * Mb + j];
-    const bool on = x != 0 && (x & 0x8000u) == 0;
-    dz[k * Mb + j] = on ? f32_to_bf16_rne(w[k] * dv[j]) : (uint16_t)0;
+    const uint4 x = *(const uint4 *)(h + k * Mb + j);
+    const float4 d0 = *(const float4 *)(dv + j), d1 = *(const float4 *)(dv + j + 4);
+    const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+    const float wk = w[k];
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t lo = xw[q] & 0xFFFFu, hi = xw[q] >> 16;
+        const uint32_t a = (lo != 0 && !(lo & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q]) : 0u;
+        const uint32_t b = (hi != 0 && !(hi & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q + 1]) : 0u;
+        o[q] = a | (b << 16);
+    }
+    *out = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -669,8 +681,9 @@ hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float
 hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
                                 const float *dv, uint16_t *dz, hipStream_t s)
 {
-    hipLaunchKernelGGL(head_backward_kernel, dim3((unsigned)((Mb + 255) / 256), (unsigned)rows), dim3(256),
-                       0, s, h, K, Mb, w, dv, dz);
+    // Mb is a multiple of 256: 8 samples per thread
+    hipLaunchKernelGGL(head_backward_kernel, dim3((unsigned)((Mb / 8 + 255) / 256), (unsigned)rows),
+                       dim3(256), 0, s, h, K, Mb, w, dv, dz);
     return hipGetLastError();
 }
 
