@@ -126,6 +126,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
     return (uint16_t)(u >> 16);
 }
 
+// Two fp32 values -> packed bf16 pair (a in the low half), rounded to nearest
+// even by the hardware conversion (v_cvt_pk_bf16_f32); equal to two
+// f32_to_bf16_rne for finite inputs, a quiet NaN for NaN.
+typedef __bf16 im_bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float im_f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    const im_f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, im_bf16x2_t));
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 }  // namespace im

@@ -402,10 +402,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     u32x4_t w;
-                    w[0] = (uint32_t)f32_to_bf16_rne(o[0][e]) | ((uint32_t)f32_to_bf16_rne(o[1][e]) << 16);
-                    w[1] = (uint32_t)f32_to_bf16_rne(o[2][e]) | ((uint32_t)f32_to_bf16_rne(o[3][e]) << 16);
-                    w[2] = (uint32_t)f32_to_bf16_rne(o[4][e]) | ((uint32_t)f32_to_bf16_rne(o[5][e]) << 16);
-                    w[3] = (uint32_t)f32_to_bf16_rne(o[6][e]) | ((uint32_t)f32_to_bf16_rne(o[7][e]) << 16);
+                    w[0] = pack_bf16x2(o[0][e], o[1][e]);
+                    w[1] = pack_bf16x2(o[2][e], o[3][e]);
+                    w[2] = pack_bf16x2(o[4][e], o[5][e]);
+                    w[3] = pack_bf16x2(o[6][e], o[7][e]);
                     *(u32x4_t *)(Bs + (ng * 4 + e) * LDK + kg * 8) = w;
                 }
             }
@@ -487,8 +487,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
                     const float v1 = fmaxf(acc[i][j][4 * grp + 1] + bb.y, 0.0f);
                     const float v2 = fmaxf(acc[i][j][4 * grp + 2] + bb.z, 0.0f);
                     const float v3 = fmaxf(acc[i][j][4 * grp + 3] + bb.w, 0.0f);
-                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
-                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+                    const uint32_t lo = pack_bf16x2(v0, v1);
+                    const uint32_t hi = pack_bf16x2(v2, v3);
                     const int chunk = (ml >> 3) ^ (nl & (CPR - 1));
                     *(uint2 *)(lds + nl * BM + chunk * 8 + 4 * (lane >> 5)) = make_uint2(lo, hi);
                 }
@@ -699,8 +699,8 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
                     const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
                     const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
                     const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
-                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
-                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+                    const uint32_t lo = pack_bf16x2(v0, v1);
+                    const uint32_t hi = pack_bf16x2(v2, v3);
                     const int chunk = q ^ (nl & 3);
                     *(uint2 *)(ep + nl * 64 + chunk * 16 + 8 * (lane >> 5)) = make_uint2(lo, hi);
                 }
@@ -825,8 +825,7 @@ __global__ __launch_bounds__(256) void stage_obs_bf16_kernel(const float *__rest
             uint32_t w[8];
 #pragma unroll
             for (int h = 0; h < 8; ++h)
-                w[h] = (uint32_t)f32_to_bf16_rne(t[r0 + 2 * h][nl]) |
-                       ((uint32_t)f32_to_bf16_rne(t[r0 + 2 * h + 1][nl]) << 16);
+                w[h] = pack_bf16x2(t[r0 + 2 * h][nl], t[r0 + 2 * h + 1][nl]);
             uint4 *dst = (uint4 *)(x16 + n * K_pad + k0 + r0);
             dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
             dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
