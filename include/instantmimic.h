@@ -114,9 +114,16 @@ typedef struct {
     float m_jrot, m_jvel, m_com, m_eepos, m_eerot;  /* multiplicative weights (finite) */
     int32_t obs_future;       /* future reference frames in the observation, 0..4 */
     int32_t obs_prev_action;  /* 1: the previous action ends the observation */
+    int32_t env_split;        /* threads per env of im_env_step_fused: IM_SPLIT_AUTO (by
+                                 batch size), IM_SPLIT_ONE, IM_SPLIT_HALVES (two walks),
+                                 IM_SPLIT_PATHS (one walk per root-to-leaf path; needs
+                                 2..8 leaves, else IM_ERR_UNSUPPORTED at im_create).  The
+                                 results are the same up to the order of the reward's
+                                 fp32 sums over bodies. */
 } im_config;
 
 enum { IM_REWARD_GROUPED = 0, IM_REWARD_MULTIPLICATIVE = 1 };
+enum { IM_SPLIT_AUTO = 0, IM_SPLIT_ONE = 1, IM_SPLIT_HALVES = 2, IM_SPLIT_PATHS = 3 };
 
 /* Host arrays; copied at creation. */
 typedef struct {

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libinstantmimic.so")
 IM_OK, IM_ERR_INVALID_ARG, IM_ERR_UNSUPPORTED, IM_ERR_OOM, IM_ERR_HIP = range(5)
 IM_DTYPE_F32, IM_DTYPE_BF16 = 0, 1
 IM_JOINT_FREE, IM_JOINT_SPHERICAL, IM_JOINT_REVOLUTE, IM_JOINT_FIXED = range(4)
+IM_SPLIT_AUTO, IM_SPLIT_ONE, IM_SPLIT_HALVES, IM_SPLIT_PATHS = range(4)
 
 
 class ImConfig(C.Structure):
@@ -30,7 +31,8 @@ class ImConfig(C.Structure):
                 ("c_com", C.c_float), ("w_com", C.c_float), ("seed", C.c_uint64),
                 ("reward_form", C.c_int32), ("m_jrot", C.c_float), ("m_jvel", C.c_float),
                 ("m_com", C.c_float), ("m_eepos", C.c_float), ("m_eerot", C.c_float),
-                ("obs_future", C.c_int32), ("obs_prev_action", C.c_int32)]
+                ("obs_future", C.c_int32), ("obs_prev_action", C.c_int32),
+                ("env_split", C.c_int32)]
 
 
 class ImSkeleton(C.Structure):
@@ -320,7 +322,8 @@ class Description:
                             int(cfg.get("reward_form", 0)), float(cfg.get("m_jrot", 0.0)),
                             float(cfg.get("m_jvel", 0.0)), float(cfg.get("m_com", 0.0)),
                             float(cfg.get("m_eepos", 0.0)), float(cfg.get("m_eerot", 0.0)),
-                            int(cfg.get("obs_future", 0)), int(cfg.get("obs_prev_action", 0)))
+                            int(cfg.get("obs_future", 0)), int(cfg.get("obs_prev_action", 0)),
+                            int(cfg.get("env_split", 0)))
         self.skel = ImSkeleton(int(sk["n_bodies"]), _ptr(k(_i32(sk["parent"])), C.c_int32),
                                _ptr(k(_i32(sk["jtype"])), C.c_int32),
                                _ptr(k(_f32(sk["axis"])), C.c_float),

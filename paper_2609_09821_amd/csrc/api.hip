@@ -30,6 +30,8 @@ struct im_ctx {
     int device = -1;
     int B = 0, D = 0, A = 0, n_clips = 0, L = 0, dtype = 0, n_slots = 0, max_depth = 0;
     int half_slots = 0;   // parked-frame slots of the fused step's half walks
+    int n_paths = 0;      // root-to-leaf walks of the path-split fused step (0: none)
+    int path_slots = 0;
     int64_t max_envs = 0;
     im_config cfg{};
     SkelTab *d_skel = nullptr;
@@ -242,19 +244,20 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
     }
     std::vector<int> pos_of(B, 0);
     for (int i = 0; i < B; ++i) pos_of[order[i]] = i;
-    t->half_slots = 0;
-    for (int h = 0; h < 2; ++h) {
-        // walk set: owned bodies and their ancestors (closed under parent)
-        std::vector<int> in(B, 0);
+    // The walk of the bodies with own_of[b] == h and their ancestors, in the
+    // full preorder; *slots = the parked-frame slots it needs.
+    auto build_walk = [&](const std::vector<int> &own_of, int h, SkelTab::PartWalk &w,
+                          int *slots) -> std::string {
+        std::vector<int> in(B, 0);   // walk set: owned bodies and their ancestors
         for (int b = 0; b < B; ++b)
-            if (owner[b] == h)
+            if (own_of[b] == h)
                 for (int x = b; x >= 0 && !in[x]; x = x > 0 ? sk->parent[x] : -1) in[x] = 1;
         in[0] = 1;
         std::vector<std::vector<int>> chw(B);
         for (int b = 1; b < B; ++b)
             if (in[b]) chw[sk->parent[b]].push_back(b);
         std::vector<int> nestw(B, 0), slotw(B, -1), ordw;
-        for (int i = 0; i < B; ++i) {            // full preorder restricted to the walk set
+        for (int i = 0; i < B; ++i) {
             const int b = order[i];
             if (!in[b]) continue;
             ordw.push_back(b);
@@ -269,19 +272,18 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
                 slotw[b] = nestw[b];
                 ns = std::max(ns, nestw[b] + 1);
             }
-        t->half_slots = std::max(t->half_slots, ns);
-        auto &w = t->half[h];
+        *slots = ns;
         w.n = (int)ordw.size();
         for (int i = 0; i < w.n; ++i) {
             const int b = ordw[i];
             w.body[i] = b;
             w.rec[i] = pos_of[b];
-            w.own[i] = owner[b] == h ? 1 : 0;
+            w.own[i] = own_of[b] == h ? 1 : 0;
             w.bslot[i] = slotw[b];
             w.pslot[i] = -1;
             if (i > 0 && sk->parent[b] != ordw[i - 1]) {
                 const int p = sk->parent[b];
-                if (slotw[p] < 0) return "internal: half-walk parent is not a branch point";
+                if (slotw[p] < 0) return "internal: part-walk parent is not a branch point";
                 w.pslot[i] = slotw[p];
             }
             w.jtype[i] = sk->jtype[b];
@@ -290,6 +292,34 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
             w.offset[i][3] = 0.0f;
             w.massw[i] = (float)((double)sk->mass[b] / msum);
         }
+        return "";
+    };
+    t->half_slots = 0;
+    for (int h = 0; h < 2; ++h) {
+        int ns = 0;
+        const std::string err = build_walk(owner, h, t->half[h], &ns);
+        if (!err.empty()) return err;
+        t->half_slots = std::max(t->half_slots, ns);
+    }
+    // Path walks: one per leaf (preorder), each owning the bodies of its
+    // root-to-leaf path not owned by an earlier path.
+    std::vector<int> leaves;
+    for (int i = 0; i < B; ++i)
+        if (ch[order[i]].empty() && order[i] != 0) leaves.push_back(order[i]);
+    t->n_paths = 0;
+    t->path_slots = 0;
+    if (leaves.size() >= 2 && leaves.size() <= (size_t)IM_MAX_PATHS) {
+        std::vector<int> own_path(B, -1);
+        for (int p = 0; p < (int)leaves.size(); ++p)
+            for (int x = leaves[p]; x >= 0; x = x > 0 ? sk->parent[x] : -1)
+                if (own_path[x] < 0) own_path[x] = p;
+        for (int p = 0; p < (int)leaves.size(); ++p) {
+            int ns = 0;
+            const std::string err = build_walk(own_path, p, t->path[p], &ns);
+            if (!err.empty()) return err;
+            t->path_slots = std::max(t->path_slots, ns);
+        }
+        t->n_paths = (int)leaves.size();
     }
     return "";
 }
@@ -373,6 +403,8 @@ std::string validate(const im_config *cfg, const im_skeleton *sk, const im_clip 
         if (!finite_f(w)) return "multiplicative reward weights must be finite";
     if (cfg->obs_future < 0 || cfg->obs_future > 4) return "obs_future must be in [0, 4]";
     if (cfg->obs_prev_action != 0 && cfg->obs_prev_action != 1) return "obs_prev_action must be 0 or 1";
+    if (cfg->env_split < IM_SPLIT_AUTO || cfg->env_split > IM_SPLIT_PATHS)
+        return "env_split must be one of IM_SPLIT_AUTO, IM_SPLIT_ONE, IM_SPLIT_HALVES, IM_SPLIT_PATHS";
     if (cfg->obs_future > 0 && B == 1) {
         *code = IM_ERR_UNSUPPORTED;
         return "future reference frames need at least two bodies";
@@ -507,6 +539,9 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     if (tab.n_slots > IM_MAX_BRANCH_NESTING || tab.half_slots > IM_MAX_BRANCH_NESTING)
         return fail(IM_ERR_UNSUPPORTED, "branch points nested deeper than " +
                                             std::to_string(IM_MAX_BRANCH_NESTING));
+    if (cfg->env_split == IM_SPLIT_PATHS && tab.n_paths < 2)
+        return fail(IM_ERR_UNSUPPORTED, "env_split IM_SPLIT_PATHS needs 2.." +
+                                            std::to_string(IM_MAX_PATHS) + " leaves");
 
     im_ctx *c = new im_ctx();
     hipError_t e = hipGetDevice(&c->device);
@@ -524,6 +559,8 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
     c->dtype = pol->dtype;
     c->n_slots = tab.n_slots;
     c->half_slots = tab.half_slots;
+    c->n_paths = tab.n_paths;
+    c->path_slots = tab.path_slots;
     c->max_depth = max_depth;
     c->max_envs = max_envs;
     c->cfg = *cfg;
@@ -677,8 +714,25 @@ im_status im_env_step_fused(im_ctx *c, const im_env_bufs *b, void *stream)
     im_status s = check_env_bufs(c, b, true);
     if (s != IM_OK) return s;
     if ((s = check_device(c)) != IM_OK) return s;
-    const EnvArgs a = env_args(c, b);
-    hipError_t e = launch_env_step(c->n_slots, c->half_slots, a, (hipStream_t)stream);
+    EnvArgs a = env_args(c, b);
+    // threads per env: the configured split, or by batch size (path walks for
+    // small batches, two halves up to SPLIT_ENV_MAX, then one thread)
+    int split = c->cfg.env_split;
+    if (split == IM_SPLIT_AUTO)
+        split = (a.n <= PATH_ENV_MAX && c->n_paths >= 2) ? IM_SPLIT_PATHS
+                : (a.n <= SPLIT_ENV_MAX ? IM_SPLIT_HALVES : IM_SPLIT_ONE);
+    int walk_slots = 0;
+    a.n_parts = 1;
+    if (split == IM_SPLIT_HALVES) {
+        a.walks = c->d_skel->half;
+        a.n_parts = 2;
+        walk_slots = c->half_slots;
+    } else if (split == IM_SPLIT_PATHS) {
+        a.walks = c->d_skel->path;
+        a.n_parts = c->n_paths;
+        walk_slots = c->path_slots;
+    }
+    hipError_t e = launch_env_step(c->n_slots, walk_slots, a, (hipStream_t)stream);
     return e == hipSuccess ? IM_OK : hip_fail(e, "env_step launch");
 }
 

@@ -9,9 +9,10 @@
 //
 // Forward kinematics walks the bodies in depth-first preorder: a body's
 // parent is the previous body, or a branch point whose frame was parked in
-// LDS.  The fused step runs every env on two threads (the same lane of two
-// wavefronts), each walking the bodies of one half of the skeleton plus their
-// ancestors; the two partial error sums are combined through LDS.
+// LDS.  For small batches the fused step runs every env on several threads
+// (the same lane of consecutive wavefronts), each walking the bodies of one
+// part of the skeleton plus their ancestors (two halves, or one root-to-leaf
+// path each); the partial error sums are combined through LDS.
 //
 // Reference positions are kept relative to an anchor (the clip root
 // position at frame i0) and the simulator positions are differenced against
@@ -405,14 +406,14 @@ struct SimPV {
     f3 P, V;
 };
 
-using HalfWalk = SkelTab::HalfWalk;
+using PartWalk = SkelTab::PartWalk;
 
-// Forward kinematics over one half walk (root first, preorder), with the same
+// Forward kinematics over one part walk (root first, preorder), with the same
 // depth-2 prefetch as walk_prefetch; load(body) is called for owned bodies
 // only, and visit(i, body, own, frame, anchor, data, joint rotation, joint
 // angular velocity) for every position.
 template <class D, class Load, class Visit>
-__device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const float4 *rec,
+__device__ __forceinline__ void walk_part(const PartWalk *__restrict__ w, const float4 *rec,
                                           float alpha, Load &&load, Visit &&visit)
 {
     const LdsStack<13> st{im_lds + threadIdx.x, (int)blockDim.x};
@@ -486,9 +487,9 @@ __device__ __forceinline__ void walk_half(const HalfWalk *__restrict__ w, const 
     }
 }
 
-// Observation rows of the bodies a half owns, from the sim state (env not
-// reset); h = the heading of the sim root.
-__device__ __forceinline__ void obs_half_from_sim(const EnvArgs &a, const HalfWalk *__restrict__ w,
+// Observation rows of the bodies a part walk owns, from the sim state (env
+// not reset); h = the heading of the sim root.
+__device__ __forceinline__ void obs_part_from_sim(const EnvArgs &a, const PartWalk *__restrict__ w,
                                                   int64_t e, const Heading &h)
 {
     const int64_t ld = a.ld;
@@ -502,11 +503,11 @@ __device__ __forceinline__ void obs_half_from_sim(const EnvArgs &a, const HalfWa
     }
 }
 
-// Reference state initialisation of the bodies a half owns at (clip k, phase
-// ph), and their observation rows from the same fp32 values the sim state
-// receives (the heading from the root, which both halves walk first; it is
-// returned).
-__device__ __forceinline__ Heading rsi_obs_half(const EnvArgs &a, const HalfWalk *__restrict__ w,
+// Reference state initialisation of the bodies a part walk owns at (clip k,
+// phase ph), and their observation rows from the same fp32 values the sim
+// state receives (the heading from the root, which every walk visits first;
+// it is returned).
+__device__ __forceinline__ Heading rsi_obs_part(const EnvArgs &a, const PartWalk *__restrict__ w,
                                                 int64_t e, int k, float ph)
 {
     const ClipTab ci = a.clips[k];
@@ -516,7 +517,7 @@ __device__ __forceinline__ Heading rsi_obs_half(const EnvArgs &a, const HalfWalk
     const float4 *rec = a.seg + ci.seg_base + (int64_t)j0 * seg_stride(a.sk->B);
     const int64_t ld = a.ld;
     Heading h{};
-    walk_half<NoData>(w, rec, al, [](int) { return NoData{}; },
+    walk_part<NoData>(w, rec, al, [](int) { return NoData{}; },
                       [&](int i, int b, int own, const Frame &f, f3 A, const NoData &, q4, f3) {
         const f3 P = A + f.P;
         if (i == 0) h = heading_of(f.Q, P);
@@ -587,34 +588,39 @@ struct MulErr {
     }
 };
 
-// The fused step for small batches: env e runs on two wavefronts of its
-// block, lane l of wave 2p and of wave 2p+1, the first walking
-// SkelTab::half[0] and the second half[1] (the half is wave-uniform, so its
-// tables are read with scalar loads); 64 envs per wave pair, 128 per block.
-// The partial error sums meet in LDS.  Twice the wavefronts of the one-thread
-// kernel for the same envs: below a few waves per SIMD that hides more of the
-// walks' latency, above it the duplicated root and ancestor work costs more.
-// Future reference frames of the observation alternate between the halves.
+// The fused step for small batches: env e runs on P = a.n_parts threads, lane
+// l of P consecutive wavefronts of its block, the p-th walking a.walks[p]
+// (two halves of the skeleton, or its root-to-leaf paths).  The walk is
+// wave-uniform, so its tables are read with scalar loads.  A block holds
+// G = max(1, 4 / P) groups of 64 envs.  The partial error sums meet in LDS
+// and every thread adds them in walk order, so all P threads hold the same
+// bits.  More wavefronts than the one-thread kernel for the same envs, each
+// with a shorter walk: below a few waves per SIMD that hides more of the
+// walks' latency, above it the repeated ancestor work costs more.  Future
+// reference frames of the observation are dealt round-robin to the walks.
 // MUL: the multiplicative reward.
 template <bool MUL>
-__global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
+__global__ __launch_bounds__(512) void env_step_parts_kernel(EnvArgs a)
 {
-    __shared__ float part[7][256];
+    __shared__ float part[7][512];
     const int tid = threadIdx.x;
+    const int P = a.n_parts;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int hf = wave & 1;
-    const int64_t e = (int64_t)blockIdx.x * 128 + (wave >> 1) * 64 + (tid & 63);
-    const bool active = e < a.n;      // the same for both threads of an env
+    const int pw_i = wave % P, grp = wave / P;
+    const int G = (int)(blockDim.x >> 6) / P;
+    const int lane = tid & 63;
+    const int64_t e = ((int64_t)blockIdx.x * G + grp) * 64 + lane;
+    const bool active = e < a.n;      // the same for all P threads of an env
     const int64_t ld = a.ld;
     const SkelTab *__restrict__ sk = a.sk;
-    const HalfWalk *__restrict__ hw = &sk->half[hf];
+    const PartWalk *__restrict__ hw = &a.walks[pw_i];
 
-    // 1. discrete state advance (fp32, exact contract), in both lanes
+    // 1. discrete state advance (fp32, exact contract), in every thread
     int k = 0, t1 = 0, i0 = 0;
     uint32_t n1 = 0;
     float phi1 = 0.0f, alpha = 0.0f;
     bool trunc = false;
-    // 2.-3. reference FK and this half's error sums against the sim state
+    // 2.-3. reference FK and this walk's error sums against the sim state
     float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
     f3 dc = mk3(0.0f, 0.0f, 0.0f);
     MulErr me;
@@ -638,7 +644,7 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
                 s.V = ld3(a.linvel, b, ld, e);
                 return s;
             };
-            walk_half<SimPV>(hw, rec, alpha, load_pv,
+            walk_part<SimPV>(hw, rec, alpha, load_pv,
                              [&](int i, int, int own, const Frame &f, f3 A, const SimPV &sb, q4,
                                  f3) {
                 if (!own) return;
@@ -651,15 +657,21 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
                 e_vel += dot3(dv, dv);
             });
         } else {
-            walk_half<SimMul>(hw, rec, alpha, [&](int b) { return load_mul(a, b, e); },
+            walk_part<SimMul>(hw, rec, alpha, [&](int b) { return load_mul(a, b, e); },
                               [&](int i, int b, int own, const Frame &f, f3 A, const SimMul &sb,
                                   q4 qr, f3 wr) {
                 if (own) me.add(b, hw->leaf[i], hw->massw[i], f, A, sb, qr, wr);
             });
         }
     }
-    // both halves' sums (a + b in one thread, b + a in the other: the same bits)
-    const int o = tid ^ 64;
+    // the walks' sums, added in walk order by every thread of the env
+    const int nb = (int)blockDim.x;
+    const int g0 = grp * P * 64 + lane;
+    auto sum_parts = [&](int c) {
+        float v = part[c][g0];
+        for (int q = 1; q < P; ++q) v += part[c][g0 + q * 64];
+        return v;
+    };
     float r;
     if constexpr (!MUL) {
         part[0][tid] = e_pos;
@@ -669,12 +681,10 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
         part[4][tid] = dc.y;
         part[5][tid] = dc.z;
         __syncthreads();
-        e_pos += part[0][o];
-        e_ee += part[1][o];
-        e_vel += part[2][o];
-        dc.x += part[3][o];
-        dc.y += part[4][o];
-        dc.z += part[5][o];
+        e_pos = sum_parts(0);
+        e_ee = sum_parts(1);
+        e_vel = sum_parts(2);
+        dc = mk3(sum_parts(3), sum_parts(4), sum_parts(5));
         const float e_com = dot3(dc, dc);
         r = a.c_pose * expf(-(a.w_pos * e_pos + a.w_ee * e_ee)) +
             a.c_vel * expf(-(a.w_vel * e_vel)) + a.c_com * expf(-(a.w_com * e_com));
@@ -687,20 +697,19 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
         part[5][tid] = me.dc.y;
         part[6][tid] = me.dc.z;
         __syncthreads();
-        me.jrot += part[0][o];
-        me.jvel += part[1][o];
-        me.eepos += part[2][o];
-        me.eerot += part[3][o];
-        me.dc.x += part[4][o];
-        me.dc.y += part[5][o];
-        me.dc.z += part[6][o];
+        me.jrot = sum_parts(0);
+        me.jvel = sum_parts(1);
+        me.eepos = sum_parts(2);
+        me.eerot = sum_parts(3);
+        me.dc = mk3(sum_parts(4), sum_parts(5), sum_parts(6));
         r = me.reward(a);
     }
+    (void)nb;
     if (!active) return;
     const float z_root = a.pos[2 * ld + e];
     const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
 
-    // 4. masked reset (the same draw in both lanes)
+    // 4. masked reset (the same draw in every thread of the env)
     int k_out = k, t_out = t1;
     float ph_out = phi1;
     const bool done = term || trunc;
@@ -711,7 +720,7 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
         ph_out = (float)(x.y >> 8) * 0x1p-24f;
         t_out = 0;
     }
-    if (hf == 0) {
+    if (pw_i == 0) {
         a.env_clip[e] = k_out;
         a.env_phase[e] = ph_out;
         a.env_t[e] = t_out;
@@ -726,14 +735,14 @@ __global__ __launch_bounds__(256) void env_step_split_kernel(EnvArgs a)
     //    reference state written in the same walk, others from the sim state
     Heading h;
     if (done) {
-        h = rsi_obs_half(a, hw, e, k_out, ph_out);
+        h = rsi_obs_part(a, hw, e, k_out, ph_out);
     } else {
         h = sim_heading(a, e);
-        obs_half_from_sim(a, hw, e, h);
+        obs_part_from_sim(a, hw, e, h);
     }
-    // future frames j = hf, hf + 2, ...; the previous action in the second half
+    // future frames j = p, p + P, ...; the previous action in the last walk
     if (a.obs_future > 0 || a.obs_prev)
-        obs_extras(a, e, k_out, ph_out, done, h, hf, 2, a.obs_prev && hf == 1);
+        obs_extras(a, e, k_out, ph_out, done, h, pw_i, P, a.obs_prev && pw_i == P - 1);
 }
 
 // The fused step, one thread per env (large batches and the training terms).
@@ -1108,20 +1117,22 @@ static hipError_t launch_env(void (*k)(EnvArgs), int n_slots, int frame_floats,
     return hipGetLastError();
 }
 
-hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s)
+hipError_t launch_env_step(int n_slots, int walk_slots, const EnvArgs &a, hipStream_t s)
 {
     if (a.n <= 0) return hipSuccess;
     const bool mul = a.reward_form == IM_REWARD_MULTIPLICATIVE;
-    if (a.n > SPLIT_ENV_MAX)
+    const int P = a.n_parts;
+    if (P <= 1)
         return launch_env(mul ? env_step_kernel<true> : env_step_kernel<false>, n_slots, 13, a, s);
-    // two threads per env: 128 envs per 256-thread block; the future-frame
-    // walks of the observation go over the whole skeleton (n_slots)
-    const int bs = 256;
-    int slots = half_slots;
+    // P threads per env: G groups of 64 envs per block of 64 P G threads; the
+    // future-frame walks of the observation go over the whole skeleton (n_slots)
+    const int G = P >= 4 ? 1 : 4 / P;
+    const int bs = 64 * P * G;
+    int slots = walk_slots;
     if (a.obs_future > 0 && n_slots > slots) slots = n_slots;
     const size_t lds = (size_t)(slots > 0 ? slots : 1) * 13 * sizeof(float) * bs;
-    hipLaunchKernelGGL(mul ? env_step_split_kernel<true> : env_step_split_kernel<false>,
-                       dim3((unsigned)((a.n + 127) / 128)), dim3(bs), lds, s, a);
+    hipLaunchKernelGGL(mul ? env_step_parts_kernel<true> : env_step_parts_kernel<false>,
+                       dim3((unsigned)((a.n + 64 * G - 1) / (64 * G))), dim3(bs), lds, s, a);
     return hipGetLastError();
 }
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s)

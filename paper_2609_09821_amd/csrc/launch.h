@@ -14,6 +14,8 @@ namespace im {
 constexpr int64_t SMALL_BATCH = 16384;
 // Batches up to this many envs run the fused step on two threads per env.
 constexpr int64_t SPLIT_ENV_MAX = 32768;
+// Batches up to this many envs run it on one thread per root-to-leaf path.
+constexpr int64_t PATH_ENV_MAX = 16384;
 
 struct GemmArgs {
     const void *x;       // layer input: obs [K][ld_x] fp32 (first layer) or [N][ld_x] of T
@@ -166,7 +168,7 @@ hipError_t launch_norm(const float *grad, int64_t P, double *norm_partial, int n
                        hipStream_t s);
 hipError_t launch_repack(const RepackArgs &r, hipStream_t s);
 
-hipError_t launch_env_step(int n_slots, int half_slots, const EnvArgs &a, hipStream_t s);
+hipError_t launch_env_step(int n_slots, int walk_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_reset(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_standin(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_pack_segments(const SkelTab *sk, int F, double fps, const float *root_pos,

@@ -8,6 +8,9 @@
 
 namespace im {
 
+// Most root-to-leaf walks of the path-split fused step.
+constexpr int IM_MAX_PATHS = 8;
+
 // Skeleton, reordered into depth-first preorder: a body's parent is then
 // either the previous body or a branch point whose frame was parked.  Read
 // with wave-uniform loads.
@@ -30,22 +33,30 @@ struct SkelTab {
     int32_t ee_slot[IM_MAX_BODIES];  // observation slot of the future frames: 0 the
                                      // root, 1.. the end effectors in body order, -1 none
     int32_t n_ee;                  // end effectors (leaves)
-    // The fused step splits every env over two threads: half h walks the
-    // bodies it owns and their ancestors (see HalfWalk).
-    int32_t half_slots;            // parked-frame slots needed by either half walk
-    struct HalfWalk {
+    // The fused step for small batches runs every env on several threads, each
+    // walking the bodies it owns plus their ancestors (a PartWalk): either two
+    // halves, or one walk per root-to-leaf path of the skeleton.
+    struct PartWalk {
         int32_t n;                     // positions of the walk (root first, preorder)
         int32_t body[IM_MAX_BODIES];   // body at position i
         int32_t rec[IM_MAX_BODIES];    // its position in the full preorder (segment record)
         int32_t own[IM_MAX_BODIES];    // 1: errors, reset and observation of this body
-                                       // belong to this half; 0: an ancestor passed through
+                                       // belong to this walk; 0: an ancestor passed through
         int32_t bslot[IM_MAX_BODIES];  // as above, for the walk's own branch points
         int32_t pslot[IM_MAX_BODIES];
         int32_t jtype[IM_MAX_BODIES];
         int32_t leaf[IM_MAX_BODIES];   // leaf of the whole skeleton (end effector)
         float offset[IM_MAX_BODIES][4];
         float massw[IM_MAX_BODIES];
-    } half[2];
+    };
+    int32_t half_slots;            // parked-frame slots needed by either half walk
+    PartWalk half[2];
+    // Path walks: path p runs from the root to the p-th leaf in preorder and owns
+    // the bodies on it that no earlier path owns.  n_paths = 0 when the skeleton
+    // has more than IM_MAX_PATHS leaves.
+    int32_t n_paths;
+    int32_t path_slots;            // 0: a path has no branch point
+    PartWalk path[IM_MAX_PATHS];
 };
 
 // Per clip.  seg_base: float4 index of segment 0 in the segment table.
@@ -98,6 +109,9 @@ struct EnvArgs {
     int32_t obs_base;          // first observation row after the phase (15 B + 1)
     int32_t A;                 // action width (previous-action rows)
     const float *prev_action;  // [n][A] (read by the step when obs_prev)
+    // split fused step: its walks and their count (threads per env)
+    const SkelTab::PartWalk *walks;
+    int32_t n_parts;
 };
 
 }  // namespace im

@@ -97,6 +97,8 @@ def test_create_rejects_null_pointers(lib):
     ("m_jvel", float("inf"), binding.IM_ERR_INVALID_ARG, "multiplicative"),
     ("obs_future", 5, binding.IM_ERR_INVALID_ARG, "obs_future"),
     ("obs_prev_action", 3, binding.IM_ERR_INVALID_ARG, "obs_prev_action"),
+    ("env_split", 4, binding.IM_ERR_INVALID_ARG, "env_split"),
+    ("env_split", -1, binding.IM_ERR_INVALID_ARG, "env_split"),
 ])
 def test_create_rejects_bad_config(lib, field, value, code, words):
     d = binding.Description(_world())
@@ -126,6 +128,18 @@ def test_create_rejects_bad_skeletons(lib):
         w2 = dict(w, skeleton=dict(sk, **{key: val}))
         _, (st, out) = _status(w2)
         _expect(lib, st, binding.IM_ERR_INVALID_ARG, words)
+
+
+def test_create_path_split_needs_at_most_eight_leaves(lib):
+    # every body a child of the root: 14 leaves, more than the path split takes
+    w = _world()
+    sk = w["skeleton"]
+    star = dict(w, skeleton=dict(sk, parent=np.where(np.arange(sk["n_bodies"]) == 0, -1, 0)
+                                 .astype(np.int32)))
+    star["config"] = dict(w["config"], env_split=binding.IM_SPLIT_PATHS)
+    _, (st, out) = _status(star)
+    _expect(lib, st, binding.IM_ERR_UNSUPPORTED, "leaves")
+    assert out.value is None
 
 
 def test_create_rejects_non_unit_revolute_axis(lib):

@@ -43,10 +43,8 @@ def test_reset_envs_parity(cfg):
     H.compare_sim_obs(g, st, np.ones(N, bool), "reset")
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
-def test_env_step_parity(cfg):
-    N, T = SIZES[cfg], STEPS[cfg]
-    d, w, ctx, bufs = _setup(cfg, N)
+def _step_parity(cfg, N, T, **over):
+    d, w, ctx, bufs = _setup(cfg, N, **over)
     c = d["config"]
     st = w.state(N)
     w.reset_envs(st)
@@ -72,6 +70,20 @@ def test_env_step_parity(cfg):
     assert live.mean() > 0.99
     print("cfg %d: %d resets over %d steps, %d envs excluded at ties" % (cfg, n_done, T,
                                                                          int((~live).sum())))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+def test_env_step_parity(cfg):
+    _step_parity(cfg, SIZES[cfg], STEPS[cfg])
+
+
+# Every split of the fused step (one thread per env, two halves, one thread per
+# root-to-leaf path) on the same sizes, whatever the batch-size rule would pick.
+@pytest.mark.parametrize("split", [binding.IM_SPLIT_ONE, binding.IM_SPLIT_HALVES,
+                                   binding.IM_SPLIT_PATHS])
+@pytest.mark.parametrize("cfg", [3, 4, 6])
+def test_env_step_split_parity(cfg, split):
+    _step_parity(cfg, SIZES[cfg], STEPS[cfg], env_split=split)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5, 6])
