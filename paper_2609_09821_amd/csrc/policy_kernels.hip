@@ -150,8 +150,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
 
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)W, (short)0, (int)g.w_bytes, 0x00020000);
-    f32x4_t ra[A_CH], rb[IN_OBS ? O_CH : B_CH];
-    auto load_global = [&](int k0) {
+    // three register stages: the global loads of chunk k+3 go out while chunk
+    // k is multiplied and chunk k+1 (loaded two chunks earlier) is stored to LDS
+    constexpr int RB = IN_OBS ? O_CH : B_CH;
+    f32x4_t ra0[A_CH], rb0[RB], ra1[A_CH], rb1[RB], ra2[A_CH], rb2[RB];
+    auto load_global = [&](int k0, f32x4_t (&ra)[A_CH], f32x4_t (&rb)[RB]) {
 #pragma unroll
         for (int c = 0; c < A_CH; ++c) {
             const int v = tid + c * NTHR;
@@ -184,7 +187,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
             }
         }
     };
-    auto store_lds = [&](int buf) {
+    auto store_lds = [&](int buf, const f32x4_t (&ra)[A_CH], const f32x4_t (&rb)[RB]) {
         float *As = lds + buf * STAGE;
         float *Bs = As + BM * LDA;
 #pragma unroll
@@ -219,36 +222,51 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+    // MFMA 4t + q of a chunk takes, in each half h = lane / 32 of the wave,
+    // element q of the 16-byte run at k = 8t + 4h (operands A and B alike), so
+    // one 16-byte LDS read per operand feeds four MFMAs.  Rows of 36 floats put
+    // 16 consecutive rows of one run on distinct bank groups.
     auto compute = [&](int buf) {
         const float *As = lds + buf * STAGE;
         const float *Bs = As + BM * LDA;
         const int arow = wm * (MT * 32) + (lane & 31), brow = wn * (NT * 32) + (lane & 31);
+        const int kh = 4 * (lane >> 5);
 #pragma unroll
-        for (int ks = 0; ks < KC; ks += 2) {
-            const int kof = ks + (lane >> 5);
-            float af[MT], bfr[NT];
+        for (int t = 0; t < KC / 8; ++t) {
+            f32x4_t af[MT], bfr[NT];
 #pragma unroll
-            for (int i = 0; i < MT; ++i) af[i] = As[(arow + i * 32) * LDA + kof];
+            for (int i = 0; i < MT; ++i) af[i] = *(const f32x4_t *)(As + (arow + i * 32) * LDA + 8 * t + kh);
 #pragma unroll
-            for (int j = 0; j < NT; ++j) bfr[j] = Bs[(brow + j * 32) * LDA + kof];
+            for (int j = 0; j < NT; ++j) bfr[j] = *(const f32x4_t *)(Bs + (brow + j * 32) * LDA + 8 * t + kh);
 #pragma unroll
-            for (int i = 0; i < MT; ++i)
+            for (int q = 0; q < 4; ++q)
 #pragma unroll
-                for (int j = 0; j < NT; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[j], acc[i][j], 0, 0, 0);
+                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][q], bfr[j][q], acc[i][j], 0, 0, 0);
         }
     };
 
     const int nk = g.K_pad / KC;
-    load_global(0);
-    store_lds(0);
+    load_global(0, ra0, rb0);
+    store_lds(0, ra0, rb0);
     __syncthreads();
-    if (nk > 1) load_global(KC);
-    for (int kt = 0; kt < nk; ++kt) {
+    if (nk > 1) load_global(KC, ra1, rb1);
+    if (nk > 2) load_global(2 * KC, ra2, rb2);
+    // chunk kt: registers of chunk kt+1 in stage (kt+1) % 3, loads of kt+3 into
+    // stage kt % 3 (stored to LDS in the previous iteration)
+    auto step = [&](int kt, const f32x4_t (&sa)[A_CH], const f32x4_t (&sb)[RB], f32x4_t (&la)[A_CH],
+                    f32x4_t (&lb)[RB]) {
         compute(kt & 1);
-        if (kt + 1 < nk) store_lds((kt + 1) & 1);
-        if (kt + 2 < nk) load_global((kt + 2) * KC);
+        if (kt + 1 < nk) store_lds((kt + 1) & 1, sa, sb);
+        if (kt + 3 < nk) load_global((kt + 3) * KC, la, lb);
         __syncthreads();
+    };
+    for (int kt = 0; kt < nk; kt += 3) {
+        step(kt, ra1, rb1, ra0, rb0);
+        if (kt + 1 < nk) step(kt + 1, ra2, rb2, ra1, rb1);
+        if (kt + 2 < nk) step(kt + 2, ra0, rb0, ra2, rb2);
     }
 
     if constexpr (!SAMPLE) {
@@ -275,6 +293,87 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g)
         const int64_t nv = g.N - n0 < BN ? g.N - n0 : BN;
         sample_epilogue<NTHR, MT, NT>(g, lds, n0, nv, wn * NT * 32, tid, acc);
     }
+}
+
+// Last fp32 layer + sampling for small batches: one column of 32 envs and all
+// MT x 32 (padded) actions per block of SK waves, the waves splitting K.  No
+// LDS staging: for MFMA s = 4t + q of its K range a lane supplies element q of
+// a 16-byte load at k = 8t + 4 (lane / 32), for the weight row (lane % 32) and
+// the env row (lane % 32) alike, so the two halves of the wave cover k = 8t ..
+// 8t + 7 over four MFMAs.  A wave issues every load of its range before its
+// first MFMA (one memory latency instead of one per K chunk).  The partial
+// accumulators are added in LDS in wave order, then the sampling epilogue.
+template <int MT, int SK>
+__global__ __launch_bounds__(64 * SK) void sample_f32_splitk_kernel(GemmArgs g)
+{
+    constexpr int RED = (SK - 1) * MT * 16 * 64;
+    constexpr int SO = 32 * 32 * MT;    // 32 envs x M_pad >= 32 x A floats
+    constexpr int TCH = 16;             // 16-byte loads per operand row and chunk
+    __shared__ __attribute__((aligned(16))) float lds[RED > SO ? RED : SO];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t n0 = (int64_t)blockIdx.x * 32;
+    const int nt = g.K_pad / (8 * SK);  // 8-deep k groups per wave
+    const int kb = wave * nt * 8;
+    const int h = lane >> 5, r = lane & 31;
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.w, (short)0, (int)g.w_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
+    // env rows past N lie past the extent and read as zero
+    const uint32_t boff = (uint32_t)(((n0 + r) * g.ld_x + kb + 4 * h) * 4);
+    uint32_t aoff[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) aoff[i] = (uint32_t)(((i * 32 + r) * g.K_pad + kb + 4 * h) * 4);
+
+    f32x16_t acc[MT][1];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[i][0][q] = 0.0f;
+    for (int t0 = 0; t0 < nt; t0 += TCH) {
+        f32x4_t av[MT][TCH], bv[TCH];
+        // past the wave's range the loads are skipped and their MFMAs add zero
+#pragma unroll
+        for (int u = 0; u < TCH; ++u) {
+            const bool in = t0 + u < nt;
+            const uint32_t dk = (uint32_t)(8 * (t0 + u) * 4);
+            bv[u] = in ? __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, boff + dk, 0, 0))
+                       : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                av[i][u] = in ? __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, aoff[i] + dk, 0, 0))
+                              : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+#pragma unroll
+        for (int u = 0; u < TCH; ++u)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][u][q], bv[u][q], acc[i][0], 0, 0, 0);
+    }
+    // partial sums: waves 1.. park theirs ([wave-1][i][reg][lane]), wave 0 adds
+    // them in wave order
+    if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) lds[(((wave - 1) * MT + i) * 16 + q) * 64 + lane] = acc[i][0][q];
+    }
+    __syncthreads();
+    if (wave == 0) {
+        for (int w = 1; w < SK; ++w)
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) acc[i][0][q] += lds[(((w - 1) * MT + i) * 16 + q) * 64 + lane];
+    }
+    __syncthreads();
+    // every wave joins the epilogue's barriers and wide stores; only wave 0's
+    // columns are valid
+    const int64_t nv = g.N - n0 < 32 ? g.N - n0 : 32;
+    sample_epilogue<64 * SK, MT, 1>(g, lds, n0, nv, wave == 0 ? 0 : (1 << 20), tid, acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -892,9 +991,26 @@ static hipError_t launch_sample_mt(const GemmArgs &g, hipStream_t s)
     return launch_sample_t<BF16, IN_OBS, MT, 4>(g, s);
 }
 
+template <int MT>
+static hipError_t launch_sample_splitk(const GemmArgs &g, hipStream_t s)
+{
+    hipLaunchKernelGGL((sample_f32_splitk_kernel<MT, 4>), dim3((unsigned)((g.N + 31) / 32)),
+                       dim3(256), 0, s, g);
+    return hipGetLastError();
+}
+
 template <bool BF16, bool IN_OBS>
 static hipError_t launch_sample(const GemmArgs &g, int M_pad, hipStream_t s)
 {
+    // small batches, hidden input (K_pad a multiple of 32: 8-deep groups per wave)
+    if (!IN_OBS && g.N <= SMALL_BATCH && (g.K_pad & 31) == 0) {
+        switch (M_pad / 32) {
+            case 1: return launch_sample_splitk<1>(g, s);
+            case 2: return launch_sample_splitk<2>(g, s);
+            case 3: return launch_sample_splitk<3>(g, s);
+            default: return launch_sample_splitk<4>(g, s);
+        }
+    }
     switch (M_pad / 32) {
         case 1: return launch_sample_mt<BF16, IN_OBS, 1>(g, s);
         case 2: return launch_sample_mt<BF16, IN_OBS, 2>(g, s);
