@@ -54,11 +54,11 @@ SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act, in order (observation
     # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "9490c8dfaa4f6815", "workloads": {
-        4: {"fetch": [46220.5, 36493.4, 98998.0, 74238.4, 33543.5],
-            "write": [49152.1, 134637.9, 133369.6, 68001.4, 35584.0]}}},
-    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "61d79f379ff6c0e4", "workloads": {
-        4: {"fetch": [61775.4], "write": [169487.7]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "17bed9c94a7b5ff6", "workloads": {
+        4: {"fetch": [46224.5, 36428.7, 99364.4, 74206.0, 33539.5],
+            "write": [49152.1, 135390.2, 133192.3, 67977.6, 35584.0]}}},
+    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "bb51d8717ece16c6", "workloads": {
+        4: {"fetch": [61779.8], "write": [169487.7]}}},
 }
 
 
