@@ -233,3 +233,30 @@ def test_terminated_reset_draws_are_uniform():
     ph = bufs.env_phase[:N].cpu().numpy()
     assert ph.min() >= 0.0 and ph.max() < 1.0
     assert np.all(bufs.env_t[:N].cpu().numpy() == 0)
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_policy_unaligned_leading_dimension(cfg):
+    # ld_obs odd: observation rows not aligned for the vector loads; the policy
+    # output equals the one with ld_obs = n_envs
+    N = 1000
+    d = synth.make_world(cfg, n_envs=N)
+    ctx = binding.Context(d, max_envs=N)
+    D, A = ctx.info.obs_dim, d["policy"]["dims"][-1]
+    g = torch.Generator().manual_seed(cfg)
+    obs = torch.randn((D, N), generator=g)
+    env_n = torch.arange(N, dtype=torch.int32).cuda()
+    outs = []
+    for ld in (N, N + 1):
+        o = torch.zeros((D, ld))
+        o[:, :N] = obs
+        mean = torch.zeros((N, A), device="cuda")
+        act = torch.zeros((N, A), device="cuda")
+        logp = torch.zeros(N, device="cuda")
+        e = torch.zeros(ld, dtype=torch.int32, device="cuda")
+        e[:N] = env_n
+        ctx.policy_act(o.cuda(), e, N, mean, act, logp)
+        torch.cuda.synchronize()
+        outs.append((mean.cpu(), act.cpu(), logp.cpu()))
+    ctx.close()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
