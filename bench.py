@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
                     [--no-cpu-baseline] [--no-secondary] [--no-graph] [--no-rollout]
+                    [--mall-flush MB]
 
 One step = im_policy_act (MLP forward + Gaussian sampling) followed by
 im_env_step_fused (reference sampling, FK, reward, termination, masked reset,
@@ -20,9 +21,10 @@ dominant call, MFMA-bound),
 work (FLOPs / bytes) over the mean duration measured with HIP events on the
 launch stream during the timed loop.  `traffic` is the HBM bytes per launch
 measured with the profiler's byte counters on the same kernels (null when the
-kernel sources changed since).  `rollout` times a whole PPO rollout of the
-workload (policy, value head and env step per step written in place into the
-rollout storage, then GAE and the rollout summaries).  `cpu_baseline` times
+kernel sources changed since).  `mall_flushed` repeats the timed calls with
+the last-level cache flushed before each step.  `rollout` times a whole PPO
+rollout of the workload (policy, value head and env step per step written in
+place into the rollout storage, then GAE and the rollout summaries).  `cpu_baseline` times
 the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
@@ -94,7 +96,7 @@ def mlp_flops(dims, n_envs):
     return 2.0 * n_envs * sum(dims[i] * dims[i + 1] for i in range(len(dims) - 1))
 
 
-def run_gpu(wid, steps, warmup, graph=True):
+def run_gpu(wid, steps, warmup, graph=True, flush_mb=0):
     import torch
     from paper_2609_09821_amd import binding, synth
 
@@ -137,8 +139,14 @@ def run_gpu(wid, steps, warmup, graph=True):
         bufs.prev_action = action
         A_prev = A
 
+    # flush_mb > 0: a write of that many MB between steps (outside the per-call
+    # events) evicts the last-level cache, so each call starts cold
+    scratch = torch.empty(flush_mb << 18, device="cuda") if flush_mb > 0 else None
+
     def step(t, ev=None):
         bufs.body_pos, bufs.body_quat, bufs.body_linvel, bufs.body_angvel = rec[t]
+        if scratch is not None:
+            scratch.fill_(float(t))
         if ev is not None:
             ev[0].record(stream)
         ctx.policy_act(bufs.obs, bufs.env_n, N, mean, action, logp, stream=stream)
@@ -422,6 +430,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-rollout", action="store_true")
+    ap.add_argument("--mall-flush", type=int, default=512, metavar="MB",
+                    help="also time the calls with the last-level cache flushed before each step "
+                         "by a write of MB megabytes (0: skip)")
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay of the timed steps")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
@@ -448,6 +459,9 @@ def main():
         return
 
     r = run_gpu(args.workload, args.steps, args.warmup, graph=not args.no_graph)
+    cold = None
+    if args.mall_flush > 0:
+        cold = run_gpu(args.workload, args.steps, args.warmup, graph=False, flush_mb=args.mall_flush)
     desc = r["desc"]
     spec = desc["spec"]
     mlp_tflops = r["flops"] / (r["pol_ms"] * 1e-3) / 1e12
@@ -499,6 +513,17 @@ def main():
             "per_launch_ms": r["env_ms"], "work_per_launch": r["env_bytes"],
         },
     }
+    if cold is not None:
+        c_gbs = cold["env_bytes"] / (cold["env_ms"] * 1e-3) / 1e9
+        c_tf = cold["flops"] / (cold["pol_ms"] * 1e-3) / 1e12
+        out["mall_flushed"] = {
+            "flush_mb": args.mall_flush,
+            "policy_ms": cold["pol_ms"], "env_step_ms": cold["env_ms"],
+            "env_steps_per_s_of_calls": cold["N"] / ((cold["pol_ms"] + cold["env_ms"]) * 1e-3),
+            "policy_tflops": c_tf, "policy_frac": c_tf / peak,
+            "env_gbs": c_gbs, "env_frac": c_gbs / HBM_PEAK_GBS,
+            "note": "the same calls with the last-level cache (Infinity Cache) flushed by a "
+                    "write before each step; throughput from the per-call events"}
     if not args.no_secondary and args.workload != 2:
         s = run_gpu(2, args.steps, args.warmup, graph=not args.no_graph)
         out["also"] = [{
