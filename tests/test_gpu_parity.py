@@ -43,8 +43,14 @@ def test_reset_envs_parity(cfg):
     H.compare_sim_obs(g, st, np.ones(N, bool), "reset")
 
 
-def _step_parity(cfg, N, T, **over):
-    d, w, ctx, bufs = _setup(cfg, N, **over)
+def _step_parity(cfg, N, T, desc=None, **over):
+    if desc is None:
+        d, w, ctx, bufs = _setup(cfg, N, **over)
+    else:
+        d = desc
+        w = oracle.World(d)
+        ctx = binding.Context(d, max_envs=N)
+        bufs = ctx.buffers(N)
     c = d["config"]
     st = w.state(N)
     w.reset_envs(st)
@@ -84,6 +90,18 @@ def test_env_step_parity(cfg):
 @pytest.mark.parametrize("cfg", [3, 4, 6])
 def test_env_step_split_parity(cfg, split):
     _step_parity(cfg, SIZES[cfg], STEPS[cfg], env_split=split)
+
+
+# A 15-body tree with eight leaves (six two-body chains and two leaves on the
+# root): eight path walks, 512-thread blocks of the parts kernel.
+@pytest.mark.parametrize("split", [binding.IM_SPLIT_ONE, binding.IM_SPLIT_HALVES,
+                                   binding.IM_SPLIT_PATHS])
+def test_env_step_eight_leaf_tree(split):
+    d = synth.make_world(3, n_envs=700, env_split=split)
+    parent = np.array([-1, 0, 0, 0, 0, 0, 0, 1, 2, 3, 4, 5, 6, 0, 0], np.int32)
+    assert len(parent) == d["skeleton"]["n_bodies"]
+    d["skeleton"] = dict(d["skeleton"], parent=parent)
+    _step_parity(3, 700, 4, desc=d)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5, 6])
