@@ -98,15 +98,17 @@ __device__ __forceinline__ float uniform_open(uint32_t x)
     return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
 }
 
-// Box-Muller: two words -> two standard normals (cos, sin branch).
+// Box-Muller: two words -> two standard normals (cos, sin branch).  The
+// hardware sine and cosine take the angle in revolutions, so sin(2 pi v) is
+// one instruction on v itself (measured max abs error 1.3e-7 over the open
+// grid of v); the square root is the hardware one (1.5 ulp); the logarithm
+// stays the accurate library one (ln u near u = 1 is a small difference).
 __device__ __forceinline__ void box_muller(uint32_t a, uint32_t b, float *z0, float *z1)
 {
     const float u = uniform_open(a), v = uniform_open(b);
-    const float r = sqrtf(-2.0f * logf(u));
-    float s, c;
-    sincospif(2.0f * v, &s, &c);
-    *z0 = r * c;
-    *z1 = r * s;
+    const float r = __builtin_amdgcn_sqrtf(-2.0f * logf(u));
+    *z0 = r * __builtin_amdgcn_cosf(v);
+    *z1 = r * __builtin_amdgcn_sinf(v);
 }
 
 __device__ __forceinline__ void normals4(uint64_t seed, uint32_t e, uint32_t n, uint32_t blk,

@@ -47,7 +47,8 @@ __device__ __forceinline__ void copy_rows_out(float *dst, const float *so, int64
 }
 
 // Epilogue of the last layer: mean = acc + b, Gaussian noise from Philox, action
-// = mean + exp(log_std) z, logp.  The accumulators follow the 32x32 MFMA layout
+// = mean + exp(log_std) z, logp (sigma and the noise-free part of logp are
+// formed once per block).  The accumulators follow the 32x32 MFMA layout
 // (lane column = env, rows 8*grp + 4*(lane/32) + q = actions); the block covers
 // every action of its envs (m0 == 0).  The block's envs n0 .. n0+nv-1 own the
 // contiguous ranges mean[n0*A .. (n0+nv)*A) and action[...], so both are staged
@@ -60,6 +61,17 @@ __device__ __forceinline__ void sample_epilogue(const GemmArgs &g, float *so, in
 {
     const int lane = tid & 63;
     const int A = g.A;
+    // per action sigma = exp(log_std), and the noise-free part of -logp,
+    // sum over actions of (log_std + log(2 pi) / 2), once per block
+    __shared__ float sig[TM * 32];
+    __shared__ float lp0;
+    for (int m = tid; m < A; m += NTHR) sig[m] = expf(g.log_std[m]);
+    if (tid == 0) {
+        float c = 0.0f;
+        for (int m = 0; m < A; ++m) c += g.log_std[m] + HALF_LOG_2PI;
+        lp0 = c;
+    }
+    __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int nl = col0 + j * 32 + (lane & 31);
@@ -80,15 +92,14 @@ __device__ __forceinline__ void sample_epilogue(const GemmArgs &g, float *so, in
                     const int m = mb + q;
                     if (m < A) {
                         const float mu = acc[i][j][4 * grp + q] + g.bias[m];
-                        const float ls = g.log_std[m];
                         so[nl * A + m] = mu;
-                        acc[i][j][4 * grp + q] = mu + expf(ls) * z[q];
-                        lp += 0.5f * z[q] * z[q] + ls + HALF_LOG_2PI;
+                        acc[i][j][4 * grp + q] = mu + sig[m] * z[q];
+                        lp += 0.5f * z[q] * z[q];
                     }
                 }
             }
         lp += __shfl_xor(lp, 32);
-        if (valid_n && lane < 32 && g.logp) g.logp[n] = -lp;
+        if (valid_n && lane < 32 && g.logp) g.logp[n] = -(lp + lp0);
     }
     __syncthreads();
     copy_rows_out<NTHR>(g.mean + n0 * A, so, nv * A, tid);
