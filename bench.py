@@ -350,7 +350,10 @@ def run_ppo_update(ctx, desc, ro, reps=2):
     batch = binding.ppo_batch(ro, perm, lr, stats)
     params = binding.ppo_params(**p)
     stream = torch.cuda.current_stream()
-    ctx.ppo_update(batch, params, stream=stream)       # warm-up
+    # the first update runs on the rollout's own (on-policy) data: its loss
+    # statistics are the ones reported; the timed repeats reuse the same batch
+    ctx.ppo_update(batch, params, stream=stream)
+    st = stats.cpu().numpy()
     times = []
     for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -363,7 +366,6 @@ def run_ppo_update(ctx, desc, ro, reps=2):
     samples = p["epochs"] * T * N
     flops = samples * (ppo_flops_per_sample(desc["policy"]["dims"]) +
                        ppo_flops_per_sample(desc["critic"]["dims"]))
-    st = stats.cpu().numpy()
     return {
         "ms": t * 1e3, "samples_per_s": samples / t, "epochs": p["epochs"],
         "minibatches": p["minibatches"], "minibatch_samples": mb,
@@ -371,7 +373,8 @@ def run_ppo_update(ctx, desc, ro, reps=2):
         "mean_kl": float(st[2] / st[5]), "mean_clip_frac": float(st[3] / st[5]),
         "note": "forward, backward and Adam of actor and critic on MFMA; flops = 2 in out per "
                 "layer for the forward, input and weight gradients (no input gradient for the "
-                "first layer), per sample and epoch",
+                "first layer), per sample and epoch; mean_kl and mean_clip_frac from the first "
+                "update, which runs on the rollout's own data (the timed repeats reuse it)",
     }
 
 
