@@ -226,7 +226,8 @@ def run_gpu(wid, steps, warmup, graph=True, flush_mb=0):
 
 def run_rollout(wid, reps=2):
     """A whole PPO rollout of the workload (T = its step count) written in
-    place into the rollout storage: per step policy_act, value and
+    place into the rollout storage: per step policy_act_value (action, logp and
+    value of the observation, one staging of it for both networks) and
     env_step_fused, then the value of the last observation, GAE with the
     rollout summaries and the copy of the last observation into slot 0 for the
     next rollout.  The stand-in physics is recorded beforehand and excluded,
@@ -269,17 +270,14 @@ def run_rollout(wid, reps=2):
             bufs.body_pos, bufs.body_quat, bufs.body_linvel, bufs.body_angvel = rec[t]
             if ev is not None:
                 ev[t][0].record(stream)
-            ctx.policy_act(ro.obs[t], bufs.env_n, N, ro.mean[t], ro.action[t], ro.logp[t],
-                           stream=stream)
+            ctx.policy_act_value(ro.obs[t], bufs.env_n, N, ro.mean[t], ro.action[t],
+                                 ro.logp[t], ro.value[t], stream=stream)
             if ev is not None:
                 ev[t][1].record(stream)
-            ctx.value(ro.obs[t], N, ro.value[t], stream=stream)
-            if ev is not None:
-                ev[t][2].record(stream)
             ro.env_bufs(bufs, t)
             ctx.env_step_fused(bufs, stream=stream, with_ref_frame=False)
             if ev is not None:
-                ev[t][3].record(stream)
+                ev[t][2].record(stream)
         ctx.value(ro.obs[T], N, ro.value[T], stream=stream)
         if ev is not None:
             ev[T][0].record(stream)
@@ -290,17 +288,16 @@ def run_rollout(wid, reps=2):
 
     restore()
     one()                                   # warm-up
-    walls, pol, val, env, gae = [], [], [], [], []
+    walls, polval, env, gae = [], [], [], []
     for _ in range(reps):
         restore()
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(T + 1)]
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(T + 1)]
         t0 = time.perf_counter()
         one(ev)
         torch.cuda.synchronize()
         walls.append(time.perf_counter() - t0)
-        pol.append(np.mean([ev[t][0].elapsed_time(ev[t][1]) for t in range(T)]))
-        val.append(np.mean([ev[t][1].elapsed_time(ev[t][2]) for t in range(T)]))
-        env.append(np.mean([ev[t][2].elapsed_time(ev[t][3]) for t in range(T)]))
+        polval.append(np.mean([ev[t][0].elapsed_time(ev[t][1]) for t in range(T)]))
+        env.append(np.mean([ev[t][1].elapsed_time(ev[t][2]) for t in range(T)]))
         gae.append(ev[T][0].elapsed_time(ev[T][1]))
     summ = ro.summary.cpu().numpy()
     ppo = None
@@ -311,13 +308,12 @@ def run_rollout(wid, reps=2):
     return {
         "workload": desc["spec"]["name"], "n_envs": N, "T": T,
         "value": N * T / wall, "unit": "env-steps/s", "ms_per_rollout": wall * 1e3,
-        "policy_us_per_step": float(np.mean(pol)) * 1e3,
-        "value_us_per_step": float(np.mean(val)) * 1e3,
+        "policy_value_us_per_step": float(np.mean(polval)) * 1e3,
         "env_step_us_per_step": float(np.mean(env)) * 1e3,
         "gae_summary_us": float(np.mean(gae)) * 1e3,
         "episodes_ended": int(summ[3]), "mean_reward": float(summ[0] / (N * T)),
         "ppo_update": ppo,
-        "note": "policy_act + value + env_step_fused per step into the rollout storage, value of "
+        "note": "policy_act_value + env_step_fused per step into the rollout storage, value of "
                 "the last observation, GAE + summaries, last observation to slot 0; stand-in "
                 "physics excluded; best of %d rollouts" % reps,
     }
@@ -374,7 +370,10 @@ def run_ppo_update(ctx, desc, ro, reps=2):
         "note": "forward, backward and Adam of actor and critic on MFMA; flops = 2 in out per "
                 "layer for the forward, input and weight gradients (no input gradient for the "
                 "first layer), per sample and epoch; mean_kl and mean_clip_frac from the first "
-                "update, which runs on the rollout's own data (the timed repeats reuse it)",
+                "update, which runs on the rollout's own data (the timed repeats reuse it); with "
+                "sigma = 0.05 and a random-init policy, Adam's first steps at the paper's rate "
+                "move the mean by more than sigma, so both are large: a load figure, not a "
+                "learning one",
     }
 
 

@@ -102,7 +102,8 @@ class ImInfo(C.Structure):
 
 
 EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_policy_act",
-            "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value", "im_gae",
+            "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value",
+            "im_policy_act_value", "im_gae",
             "im_ppo_setup", "im_ppo_update", "im_ppo_grad", "im_ppo_params_get",
             "im_status_str", "im_last_error"]
 
@@ -140,6 +141,9 @@ def lib():
     L.im_set_critic.restype = st
     L.im_value.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p]
     L.im_value.restype = st
+    L.im_policy_act_value.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int64,
+                                      C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.im_policy_act_value.restype = st
     L.im_gae.argtypes = [C.c_void_p, C.POINTER(ImRollout), C.c_void_p]
     L.im_gae.restype = st
     L.im_ppo_setup.argtypes = [C.c_void_p, C.c_int64]
@@ -213,6 +217,12 @@ def im_set_critic(ctx, critic):
 
 def im_value(ctx, obs_ptr, ld_obs, n_envs, value_ptr, stream=None):
     _check(lib().im_value(ctx, obs_ptr, int(ld_obs), int(n_envs), value_ptr, stream))
+
+
+def im_policy_act_value(ctx, obs_ptr, ld_obs, env_n_ptr, n_envs, mean_ptr, action_ptr, logp_ptr,
+                        value_ptr, stream=None):
+    _check(lib().im_policy_act_value(ctx, obs_ptr, int(ld_obs), env_n_ptr, int(n_envs), mean_ptr,
+                                     action_ptr, logp_ptr, value_ptr, stream))
 
 
 def im_gae(ctx, rollout, stream=None):
@@ -418,6 +428,10 @@ class Context:
 
     def value(self, obs, n_envs, value, stream=None):
         im_value(self.ptr, _dptr(obs), obs.shape[1], n_envs, _dptr(value), _stream(stream))
+
+    def policy_act_value(self, obs, env_n, n_envs, mean, action, logp, value, stream=None):
+        im_policy_act_value(self.ptr, _dptr(obs), obs.shape[1], _dptr(env_n), n_envs, _dptr(mean),
+                            _dptr(action), _dptr(logp), _dptr(value), _stream(stream))
 
     def ppo_setup(self, max_minibatch):
         im_ppo_setup(self.ptr, max_minibatch)

@@ -764,18 +764,25 @@ im_status im_standin_physics(im_ctx *c, const im_env_bufs *b, float sigma_joint,
     return e == hipSuccess ? IM_OK : hip_fail(e, "stand-in launch");
 }
 
-im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
-                        int64_t n_envs, float *mean, float *action, float *logp, void *stream)
+}  // extern "C"
+
+namespace {
+
+// Checks of im_policy_act's arguments (context not null).
+im_status check_act_args(const im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                         int64_t n_envs, const float *mean, const float *action)
 {
-    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
     if (!obs || !env_n || !mean || !action) return fail(IM_ERR_INVALID_ARG, "NULL buffer");
     if (n_envs < 0 || n_envs > c->max_envs) return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
     if (ld_obs < n_envs || ld_obs < 1) return fail(IM_ERR_INVALID_ARG, "ld_obs must be >= n_envs");
-    im_status s = check_device(c);
-    if (s != IM_OK) return s;
+    return IM_OK;
+}
+
+// Extents of the policy's layer inputs: buffer loads address with 32-bit byte offsets.
+im_status check_act_sizes(const im_ctx *c, int64_t ld_obs, int64_t n_envs)
+{
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
     const uint64_t esz = bf16 ? 2 : 4;
-    // buffer loads address with 32-bit byte offsets
     for (int l = 0; l < c->L; ++l) {
         const uint64_t xb = l == 0 ? (uint64_t)c->D * (uint64_t)ld_obs * 4
                                    : (uint64_t)n_envs * (uint64_t)c->M_pad[l - 1] * esz;
@@ -785,6 +792,17 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
     }
     if (c->d_obs16 && (uint64_t)n_envs * (uint64_t)c->K_pad[0] * 2 > 0xFFFFFFF0ull)
         return fail(IM_ERR_UNSUPPORTED, "staged policy input exceeds 4 GiB");
+    return IM_OK;
+}
+
+// The policy's layers; *staged: the first layer read the observation through
+// the bf16 staging buffer (which then holds it).
+im_status policy_layers(im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                        int64_t n_envs, float *mean, float *action, float *logp,
+                        hipStream_t stream, bool *staged)
+{
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
+    const uint64_t esz = bf16 ? 2 : 4;
     for (int l = 0; l < c->L; ++l) {
         GemmArgs g{};
         const bool last = l == c->L - 1;
@@ -812,10 +830,27 @@ im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
             g.A = c->A;
             g.seed = c->cfg.seed;
         }
-        hipError_t e = launch_policy_layer(bf16, l == 0, last, g, c->M_pad[l], (hipStream_t)stream);
+        hipError_t e = launch_policy_layer(bf16, l == 0, last, g, c->M_pad[l], stream,
+                                           l == 0 ? staged : nullptr);
         if (e != hipSuccess) return hip_fail(e, "policy layer launch");
     }
     return IM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_policy_act(im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                        int64_t n_envs, float *mean, float *action, float *logp, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_act_args(c, obs, ld_obs, env_n, n_envs, mean, action);
+    if (s != IM_OK) return s;
+    if ((s = check_device(c)) != IM_OK) return s;
+    if ((s = check_act_sizes(c, ld_obs, n_envs)) != IM_OK) return s;
+    return policy_layers(c, obs, ld_obs, env_n, n_envs, mean, action, logp, (hipStream_t)stream,
+                         nullptr);
 }
 
 }  // extern "C"
@@ -824,10 +859,11 @@ namespace {
 
 // Hidden layers 0..n_hidden-1 of a packed MLP (bias, ReLU, the dtype's
 // rounding) on the observation; the last activations end in d_ws[(n_hidden-1) & 1].
+// staged: the bf16 staging buffer already holds this observation.
 im_status mlp_hidden(im_ctx *c, int n_hidden, const std::vector<int> &M_pad,
                      const std::vector<int> &K_pad, const std::vector<void *> &d_w,
                      const std::vector<float *> &d_b, const float *obs, int64_t ld_obs,
-                     int64_t n_envs, hipStream_t stream)
+                     int64_t n_envs, hipStream_t stream, bool staged)
 {
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
     const uint64_t esz = bf16 ? 2 : 4;
@@ -844,6 +880,7 @@ im_status mlp_hidden(im_ctx *c, int n_hidden, const std::vector<int> &M_pad,
         g.K_valid = l == 0 ? c->D : K_pad[l];
         g.N = n_envs;
         g.x16 = l == 0 ? c->d_obs16 : nullptr;
+        g.x16_staged = l == 0 && staged;
         g.n_cu = c->n_cu;
         g.y = c->d_ws[l & 1];
         g.ld_y = M_pad[l];
@@ -970,19 +1007,25 @@ im_status im_set_critic(im_ctx *c, const im_policy *k)
     return IM_OK;
 }
 
-im_status im_value(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, float *value,
-                   void *stream)
+}  // extern "C"
+
+namespace {
+
+// Checks of im_value's arguments (context not null).
+im_status check_value_args(const im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs,
+                           const float *value)
 {
-    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
-    const auto &cr = c->critic;
-    if (cr.L == 0) return fail(IM_ERR_INVALID_ARG, "no critic (im_set_critic)");
+    if (c->critic.L == 0) return fail(IM_ERR_INVALID_ARG, "no critic (im_set_critic)");
     if (!obs || !value) return fail(IM_ERR_INVALID_ARG, "NULL buffer");
     if (n_envs < 0 || n_envs > c->max_envs) return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
     if (ld_obs < n_envs || ld_obs < 1) return fail(IM_ERR_INVALID_ARG, "ld_obs must be >= n_envs");
-    im_status s = check_device(c);
-    if (s != IM_OK) return s;
-    const bool bf16 = c->dtype == IM_DTYPE_BF16;
-    const uint64_t esz = bf16 ? 2 : 4;
+    return IM_OK;
+}
+
+im_status check_value_sizes(const im_ctx *c, int64_t ld_obs, int64_t n_envs)
+{
+    const auto &cr = c->critic;
+    const uint64_t esz = c->dtype == IM_DTYPE_BF16 ? 2 : 4;
     if ((uint64_t)c->D * (uint64_t)ld_obs * 4 > 0xFFFFFFF0ull)
         return fail(IM_ERR_UNSUPPORTED, "critic input exceeds 4 GiB");
     for (int l = 1; l < cr.L - 1; ++l)
@@ -990,19 +1033,60 @@ im_status im_value(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, 
             return fail(IM_ERR_UNSUPPORTED, "critic layer input exceeds 4 GiB");
     if (c->d_obs16 && (uint64_t)n_envs * (uint64_t)round_up(c->D, 64) * 2 > 0xFFFFFFF0ull)
         return fail(IM_ERR_UNSUPPORTED, "staged critic input exceeds 4 GiB");
-    const hipStream_t st = (hipStream_t)stream;
+    return IM_OK;
+}
+
+// The critic's layers; staged: the bf16 staging buffer already holds obs.
+im_status value_layers(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, float *value,
+                       hipStream_t st, bool staged)
+{
+    const auto &cr = c->critic;
+    const bool bf16 = c->dtype == IM_DTYPE_BF16;
     hipError_t e;
     if (cr.L == 1) {
         e = launch_value_head_obs(obs, ld_obs, c->D, cr.d_head, cr.d_head + cr.K_head, bf16, n_envs,
                                   value, st);
     } else {
-        if ((s = mlp_hidden(c, cr.L - 1, cr.M_pad, cr.K_pad, cr.d_w, cr.d_b, obs, ld_obs, n_envs,
-                            st)) != IM_OK)
-            return s;
+        im_status s = mlp_hidden(c, cr.L - 1, cr.M_pad, cr.K_pad, cr.d_w, cr.d_b, obs, ld_obs,
+                                 n_envs, st, staged);
+        if (s != IM_OK) return s;
         e = launch_value_head_rows(bf16, c->d_ws[(cr.L - 2) & 1], cr.K_head, cr.K_head, cr.d_head,
                                    cr.d_head + cr.K_head, n_envs, value, st);
     }
     return e == hipSuccess ? IM_OK : hip_fail(e, "value head launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_value(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_envs, float *value,
+                   void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_value_args(c, obs, ld_obs, n_envs, value);
+    if (s != IM_OK) return s;
+    if ((s = check_device(c)) != IM_OK) return s;
+    if ((s = check_value_sizes(c, ld_obs, n_envs)) != IM_OK) return s;
+    return value_layers(c, obs, ld_obs, n_envs, value, (hipStream_t)stream, false);
+}
+
+im_status im_policy_act_value(im_ctx *c, const float *obs, int64_t ld_obs, const uint32_t *env_n,
+                              int64_t n_envs, float *mean, float *action, float *logp,
+                              float *value, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_act_args(c, obs, ld_obs, env_n, n_envs, mean, action);
+    if (s != IM_OK) return s;
+    if ((s = check_value_args(c, obs, ld_obs, n_envs, value)) != IM_OK) return s;
+    if ((s = check_device(c)) != IM_OK) return s;
+    if ((s = check_act_sizes(c, ld_obs, n_envs)) != IM_OK) return s;
+    if ((s = check_value_sizes(c, ld_obs, n_envs)) != IM_OK) return s;
+    const hipStream_t st = (hipStream_t)stream;
+    bool staged = false;
+    if ((s = policy_layers(c, obs, ld_obs, env_n, n_envs, mean, action, logp, st, &staged)) != IM_OK)
+        return s;
+    return value_layers(c, obs, ld_obs, n_envs, value, st, staged);
 }
 
 im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)

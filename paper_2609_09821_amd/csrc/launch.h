@@ -39,6 +39,8 @@ struct GemmArgs {
                          // observation (null: the GEMM reads the observation itself)
     int n_cu;            // compute units of the device (persistent grids)
     uint32_t y_bytes;    // extent of y in bytes (set by the launcher)
+    int x16_staged;      // non-zero: x16 already holds this observation (staged by an
+                         // earlier layer of the same call), the staging pass is skipped
 };
 
 // Rollout end (rollout_kernels.hip).
@@ -174,7 +176,10 @@ hipError_t launch_standin(int n_slots, const EnvArgs &a, hipStream_t s);
 hipError_t launch_pack_segments(const SkelTab *sk, int F, double fps, const float *root_pos,
                                 const float *root_quat, const float *local_quat, float4 *seg,
                                 hipStream_t s);
+// *staged (if not null) is set when the layer read the observation through
+// the bf16 staging buffer g.x16 (so that a later first layer on the same
+// observation may pass x16_staged).
 hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmArgs &g, int M_pad,
-                               hipStream_t s);
+                               hipStream_t s, bool *staged = nullptr);
 
 }  // namespace im

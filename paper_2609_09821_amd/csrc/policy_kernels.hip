@@ -1032,7 +1032,7 @@ static hipError_t launch_sample(const GemmArgs &g, int M_pad, hipStream_t s)
 
 // Host entry used by the C ABI layer: one layer.
 hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmArgs &g, int M_pad,
-                               hipStream_t s)
+                               hipStream_t s, bool *staged)
 {
     if (g.N <= 0) return hipSuccess;
     if (bf16) {
@@ -1049,11 +1049,14 @@ hipError_t launch_policy_layer(bool bf16, bool in_obs, bool sample, const GemmAr
             if (!in_obs) return launch_bf16<256, 256, 64, 2, 4, false, false>(g, M_pad, s);
             if (!g.x16 || !pp)
                 return launch_bf16<256, 256, 64, 2, 4, true, false>(g, M_pad, s);
-            hipLaunchKernelGGL(stage_obs_bf16_kernel, dim3((unsigned)((g.N + 63) / 64)), dim3(256), 0, s,
-                               (const float *)g.x, g.ld_x, g.K_valid, g.N, g.K_pad, g.x_bytes,
-                               (uint16_t *)g.x16);
-            hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return e;
+            if (!g.x16_staged) {
+                hipLaunchKernelGGL(stage_obs_bf16_kernel, dim3((unsigned)((g.N + 63) / 64)), dim3(256),
+                                   0, s, (const float *)g.x, g.ld_x, g.K_valid, g.N, g.K_pad,
+                                   g.x_bytes, (uint16_t *)g.x16);
+                hipError_t e = hipGetLastError();
+                if (e != hipSuccess) return e;
+            }
+            if (staged) *staged = true;
             GemmArgs h = g;
             h.x = g.x16;
             h.ld_x = g.K_pad;

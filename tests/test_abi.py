@@ -253,6 +253,8 @@ def test_calls_reject_null_context(lib):
             "NULL context")
     _expect(lib, lib.im_value(None, None, 1, 1, None, None), binding.IM_ERR_INVALID_ARG,
             "NULL context")
+    _expect(lib, lib.im_policy_act_value(None, None, 1, None, 1, None, None, None, None, None),
+            binding.IM_ERR_INVALID_ARG, "NULL context")
     ro = binding.ImRollout()
     _expect(lib, lib.im_gae(None, C.byref(ro), None), binding.IM_ERR_INVALID_ARG, "NULL context")
     pb, pp = binding.ImPpoBatch(), binding.ppo_params()

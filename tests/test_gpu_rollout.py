@@ -295,3 +295,51 @@ def test_rollout_written_in_place(cfg, N):
     s = ro.summary.cpu().numpy()
     assert s[SUM["n_terminated"]] == te.sum() and s[SUM["n_episodes"]] == dn.sum()
     ctx.close()
+
+
+# ------------------------------------------------- policy and value in one call
+def _gpu_obs(ctx, d, N, steps):
+    bufs = ctx.buffers(N)
+    ctx.reset_envs(bufs)
+    for _ in range(steps):
+        ctx.standin_physics(bufs, d["sigma_joint"], d["sigma_vel"])
+        ctx.env_step_fused(bufs)
+    return bufs.obs.clone(), bufs.env_n.clone()
+
+
+@pytest.mark.parametrize("cfg,N", [(2, 1000), (3, 1300), (4, 20000), (5, 17000)])
+def test_policy_act_value_equals_separate_calls(cfg, N):
+    """One call of both networks gives the bits of the two calls made apart,
+    also right after a call on another observation (the staged observation
+    is always this call's own)."""
+    print("policy_act_value cfg %d N %d" % (cfg, N), flush=True)
+    d = synth.make_world(cfg, n_envs=N)
+    ctx = binding.Context(d, max_envs=N)
+    A = d["policy"]["dims"][-1]
+    obs1, n1 = _gpu_obs(ctx, d, N, 1)
+    obs2, n2 = _gpu_obs(ctx, d, N, 3)
+
+    def outs():
+        return (torch.full((N, A), -9.0, device="cuda"), torch.full((N, A), -9.0, device="cuda"),
+                torch.full((N,), -9.0, device="cuda"), torch.full((N,), -9.0, device="cuda"))
+
+    def separate(obs, n):
+        m, a, lp, v = outs()
+        ctx.policy_act(obs, n, N, m, a, lp)
+        ctx.value(obs, N, v)
+        return m, a, lp, v
+
+    def combined(obs, n):
+        m, a, lp, v = outs()
+        ctx.policy_act_value(obs, n, N, m, a, lp, v)
+        return m, a, lp, v
+
+    ref1 = separate(obs1, n1)
+    got2 = combined(obs2, n2)
+    ref2 = separate(obs2, n2)
+    got1 = combined(obs1, n1)
+    torch.cuda.synchronize()
+    for got, ref in ((got1, ref1), (got2, ref2)):
+        for name, g, r in zip(("mean", "action", "logp", "value"), got, ref):
+            assert torch.equal(g, r), "%s differs from the separate calls" % name
+    assert not torch.equal(ref1[3], ref2[3])
