@@ -240,12 +240,19 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
 // Minibatch gather.  Column j = 64 c + l of the minibatch is env e0 + l of
 // step t, where chunk c of the minibatch is q = perm[c]: t = q / (N/64),
 // e0 = 64 (q % (N/64)).  One wavefront per chunk; chunks past the
-// minibatch's end write zeros (padding columns).
+// minibatch's end write zeros (padding columns).  The chunk's actions and
+// means ([64][A] floats, contiguous in the [T][N][A] storage) are read 32
+// columns at a time with loads of whole 128-byte row pieces into the wave's
+// LDS slice (rows of 33 floats: the transposed reads hit 64 distinct banks)
+// and written out as [A][Mb] rows of 64 samples.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
 {
+    constexpr int KC = 32, LDC = KC + 1;
+    __shared__ float gather_lds[4][64 * LDC];
     const int lane = threadIdx.x & 63;
     const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+    float *sh = gather_lds[threadIdx.x >> 6];
     if (c >= a.chunks_pad) return;
     const int64_t j = (int64_t)c * 64 + lane;
     const int64_t Mb = a.Mb_pad;
@@ -276,11 +283,22 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a)
     }
     for (; i < a.D; ++i) a.x0[i * Mb + j] = f32_to_bf16_rne(o[(int64_t)i * a.ld]);
     for (; i < a.K0; ++i) a.x0[i * Mb + j] = 0;
-    const float *ac = a.action + (t * a.N + e) * a.A;
-    const float *mo = a.mean + (t * a.N + e) * a.A;
-    for (int k = 0; k < a.A; ++k) {
-        a.act[k * Mb + j] = ac[k];
-        a.mean_old[k * Mb + j] = mo[k];
+    const int64_t blk = (t * a.N + (e - lane)) * a.A;   // the chunk's [64][A] block
+#pragma unroll 1
+    for (int arr = 0; arr < 2; ++arr) {
+        const float *src = (arr == 0 ? a.action : a.mean) + blk;
+        float *dst = arr == 0 ? a.act : a.mean_old;
+        for (int k0 = 0; k0 < a.A; k0 += KC) {
+            const int kc = a.A - k0 < KC ? a.A - k0 : KC;
+            // the LDS slice is the wave's own and a wave's LDS operations complete
+            // in order: no barrier between these writes and the reads below
+#pragma unroll 4
+            for (int x = lane; x < 64 * KC; x += 64) {
+                const int r = x / KC, cc = x % KC;
+                if (cc < kc) sh[r * LDC + cc] = src[(int64_t)r * a.A + k0 + cc];
+            }
+            for (int cc = 0; cc < kc; ++cc) dst[(int64_t)(k0 + cc) * Mb + j] = sh[lane * LDC + cc];
+        }
     }
     const int64_t s = t * a.ld + e;
     a.logp_old[j] = a.logp[s];
