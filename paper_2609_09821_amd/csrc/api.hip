@@ -1164,6 +1164,8 @@ struct TrainState {
     size_t splitk_floats = 0;
     double *loss_partial = nullptr, *mb_stats = nullptr, *norm_partial = nullptr;
     double *rowsum_part = nullptr;         // [rows][segments] of the bias-gradient sums
+    double *rs_tile = nullptr;             // [rows][column tiles]: row sums of a masked
+                                           // gradient, left by the GEMM that wrote it
     int norm_blocks = 0;
     float *log_std_old = nullptr;
     std::vector<void *> allocs;
@@ -1257,6 +1259,7 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
                        const uint16_t *dz, int64_t Mb, hipStream_t st)
 {
     int pp = dz == t->dz[0] ? 1 : 0;
+    bool dz_sums = false;     // dz came from a masked-gradient GEMM that left its row sums
     for (int l = (int)net.size() - 1; l >= 0; --l) {
         const TrainLayer &L = net[l];
         const uint16_t *X = l == 0 ? x0 : net[l - 1].act;
@@ -1279,7 +1282,11 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         g.ldc = L.Kp;
         IM_CHS(tg(false, im::T_PARTIAL, g, S, st));
         IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, L.Kp, L.out, L.in, t->grad + L.w_off, st));
-        IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->rowsum_part, t->grad + L.b_off, st));
+        if (dz_sums)
+            IM_CHK(im::launch_rowsum_finish(t->rs_tile, L.out, (int)(Mb / im::tgemm_bn(Mb)),
+                                            t->grad + L.b_off, st));
+        else
+            IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->rowsum_part, t->grad + L.b_off, st));
         if (l == 0) break;
         // dX^T = W^T dZ^T, masked where the layer input (a ReLU output) is 0
         im::TGemm h{};
@@ -1297,7 +1304,9 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         h.ldc = Mb;
         h.mask = X;
         h.ldm = Mb;
+        h.rs_part = t->rs_tile;     // the bias gradient of layer l - 1, by column tile
         IM_CHS(tg(true, im::T_MASK, h, 1, st));
+        dz_sums = true;
         dz = t->dz[pp];
         pp ^= 1;
     }
@@ -1564,6 +1573,7 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     if (!alloc(&t->norm_partial, sizeof(double) * t->norm_blocks)) return oom();
     // row sums: rows x segments <= 2048 + rows for any row count
     if (!alloc(&t->rowsum_part, sizeof(double) * (2048 + (size_t)maxw + 1))) return oom();
+    if (!alloc(&t->rs_tile, sizeof(double) * (size_t)maxw * (size_t)(Mb / 128 + 1))) return oom();
     // the rollout copies the update refreshes
     for (size_t l = 0; l < t->actor.size(); ++l) {
         t->actor[l].roll = c->d_w[l];

@@ -83,7 +83,12 @@ struct TGemm {
     const uint16_t *mask;  // [M][ldm] bf16: the gradient passes where mask > 0 (MASK)
     int64_t ldm;
     int M_valid;         // LINEAR: rows written
+    double *rs_part;     // MASK, optional: per-tile row sums of the stored (masked, bf16)
+                         // output, rs_part[row * (N / tgemm_bn(N)) + column tile]
 };
+
+// Column tile width of the training GEMM for N columns.
+inline int tgemm_bn(int64_t N) { return N % 256 == 0 ? 256 : 128; }
 
 struct GatherArgs {
     const float *obs;        // [T+1][D][ld]
@@ -160,6 +165,8 @@ hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, 
 // part: [rows][up to 2048 / rows + 1] float64 scratch
 hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, double *part,
                          float *out, hipStream_t s);
+// out[r] = sum over k < parts of part[r * parts + k] (float64, k in order), r < rows.
+hipError_t launch_rowsum_finish(const double *part, int rows, int parts, float *out, hipStream_t s);
 hipError_t launch_splitk_reduce(const float *P, int S, int64_t M, int64_t N, int rows, int cols,
                                 float *out, hipStream_t s);
 hipError_t launch_loss(const LossArgs &a, hipStream_t s);

@@ -16,6 +16,8 @@
 // (activations, gradients) or n-major [n][k] (X^T for the weight gradient).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "device_math.h"
 #include "launch.h"
 
@@ -27,6 +29,32 @@ typedef unsigned int u32x4_v __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_v __attribute__((ext_vector_type(2)));
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 #define IM_LDS3 __attribute__((address_space(3)))
+
+// Sum of x over each group of W (16 or 32) consecutive lanes, aligned to W,
+// returned in the group's last lane: an inclusive scan within each 16-lane
+// row (DPP row shifts by 1, 2, 4, 8; lanes shifted in from outside the row
+// read zero), then for W = 32 the total of the even row added into the odd
+// row (row broadcast of lane 15).  The order of the additions is fixed.
+template <int W>
+__device__ __forceinline__ float lane_group_sum(float x)
+{
+    static_assert(W == 16 || W == 32, "lane group");
+    auto shr = [](float v, float acc, auto ctrl) {
+        const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), decltype(ctrl)::value,
+                                                  0xF, 0xF, true);
+        return acc + __builtin_bit_cast(float, t);
+    };
+    x = shr(x, x, std::integral_constant<int, 0x111>{});   // row_shr:1
+    x = shr(x, x, std::integral_constant<int, 0x112>{});   // row_shr:2
+    x = shr(x, x, std::integral_constant<int, 0x114>{});   // row_shr:4
+    x = shr(x, x, std::integral_constant<int, 0x118>{});   // row_shr:8
+    if constexpr (W == 32) {
+        // row_bcast:15 into rows 1 and 3 only (row mask 0b1010); rows 0 and 2 add 0
+        const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x142, 0xA, 0xF, false);
+        x += __builtin_bit_cast(float, t);
+    }
+    return x;
+}
 
 // ---------------------------------------------------------------------------
 // GEMM: 128 x 128 tiles of 4 waves (2 x 2, each 64 x 64 = 2 x 2 MFMA
@@ -211,6 +239,17 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
                     ow[k] &= keep;
                 }
                 o = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+                if (g.rs_part) {
+                    // the row's sum over this tile's columns: the BQ consecutive lanes
+                    // holding the row's pieces are summed by a fixed DPP pattern into
+                    // the group's last lane
+                    float rs = 0.0f;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        rs += bf16_to_f32((uint16_t)(ow[k] & 0xFFFFu)) + bf16_to_f32((uint16_t)(ow[k] >> 16));
+                    rs = lane_group_sum<BQ>(rs);
+                    if (pc == BQ - 1) g.rs_part[(m0 + ml) * (g.N / BN) + n0 / BN] = (double)rs;
+                }
             }
             *(uint4 *)((uint16_t *)g.C + off) = o;
         }
@@ -403,6 +442,24 @@ __global__ __launch_bounds__(256) void rowsum_kernel(const void *__restrict__ x,
         __syncthreads();
     }
     if (threadIdx.x == 0) part[(int64_t)r * parts + seg] = red[0];
+}
+
+// One block per row: thread i adds parts i, i + 256, ... in order, then a
+// fixed tree over the block.
+__global__ __launch_bounds__(256) void rowsum_finish_rows_kernel(const double *__restrict__ part,
+                                                                 int parts, float *__restrict__ out)
+{
+    __shared__ double red[256];
+    const int r = blockIdx.x;
+    double s = 0.0;
+    for (int k = threadIdx.x; k < parts; k += 256) s += part[(int64_t)r * parts + k];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[r] = (float)red[0];
 }
 
 __global__ __launch_bounds__(256) void rowsum_finish_kernel(const double *__restrict__ part, int rows,
@@ -659,7 +716,7 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackArgs r)
 hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_t s)
 {
     // 256-row tiles of 8 waves and 256-column tiles where the shape allows
-    const bool bigm = g.M % 256 == 0, bign = g.N % 256 == 0;
+    const bool bigm = g.M % 256 == 0, bign = tgemm_bn(g.N) == 256;
     const int bm = bigm ? 256 : 128, bn = bign ? 256 : 128;
     const dim3 grid((unsigned)((g.M / bm) * (g.N / bn)), (unsigned)splits);
 #define IM_TG(B, E)                                                                            \
@@ -719,6 +776,13 @@ hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const f
         hipLaunchKernelGGL(rowsum_kernel<false>, grid, dim3(256), 0, s, x, Mb, y, parts, part);
     hipLaunchKernelGGL(rowsum_finish_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, part,
                        rows, parts, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_rowsum_finish(const double *part, int rows, int parts, float *out, hipStream_t s)
+{
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(rowsum_finish_rows_kernel, dim3((unsigned)rows), dim3(256), 0, s, part, parts, out);
     return hipGetLastError();
 }
 
