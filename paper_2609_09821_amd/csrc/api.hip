@@ -1252,6 +1252,10 @@ im_status net_forward(const std::vector<TrainLayer> &net, const uint16_t *x0, in
     return IM_OK;
 }
 
+// Columns of a layer's weight-gradient GEMM: its input width padded to the
+// 256-column tile.
+int wgrad_cols(const TrainLayer &L) { return (int)round_up(L.Kp, 256); }
+
 // backward of one network's GEMM layers from dz (gradient of the last GEMM
 // layer's pre-activation, [Mp][Mb] bf16): weight and bias gradients into
 // t->grad; dz buffers alternate in t->dz starting after `dz`
@@ -1263,8 +1267,10 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
     for (int l = (int)net.size() - 1; l >= 0; --l) {
         const TrainLayer &L = net[l];
         const uint16_t *X = l == 0 ? x0 : net[l - 1].act;
-        // dW = dZ^T X over the minibatch (split over it)
-        const int tiles = (L.Mp / 128) * (L.Kp / 128);
+        // dW = dZ^T X over the minibatch (split over it), on whole 256-column tiles:
+        // the columns past Kp read zero (outside the operand's buffer range)
+        const int Nw = wgrad_cols(L);
+        const int tiles = (L.Mp / 128) * (Nw / 128);
         int S, ks;
         splitk_plan(tiles, Mb, &S, &ks);
         im::TGemm g{};
@@ -1275,13 +1281,13 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         g.ldb = Mb;
         g.b_bytes = (uint32_t)((uint64_t)L.Kp * Mb * 2);
         g.M = L.Mp;
-        g.N = L.Kp;
+        g.N = Nw;
         g.K = (int)Mb;
         g.k_split = ks;
         g.C = t->splitk;
-        g.ldc = L.Kp;
+        g.ldc = Nw;
         IM_CHS(tg(false, im::T_PARTIAL, g, S, st));
-        IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, L.Kp, L.out, L.in, t->grad + L.w_off, st));
+        IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, Nw, L.out, L.in, t->grad + L.w_off, st));
         if (dz_sums)
             IM_CHK(im::launch_rowsum_finish(t->rs_tile, L.out, (int)(Mb / im::tgemm_bn(Mb)),
                                             t->grad + L.b_off, st));
@@ -1552,8 +1558,8 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
                 return oom();
             if (!out_layer && !alloc(&L.act, (size_t)L.Mp * Mb * 2)) return oom();
             int S, ks;
-            splitk_plan((L.Mp / 128) * (L.Kp / 128), Mb, &S, &ks);
-            sk = std::max(sk, (size_t)S * L.Mp * L.Kp);
+            splitk_plan((L.Mp / 128) * (wgrad_cols(L) / 128), Mb, &S, &ks);
+            sk = std::max(sk, (size_t)S * L.Mp * wgrad_cols(L));
         }
     }
     const int A = c->A;
