@@ -56,11 +56,11 @@ SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act, in order (observation
     # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "d446b427c09b1490", "workloads": {
-        4: {"fetch": [46224.5, 36422.5, 99237.8, 74201.6, 33469.5],
-            "write": [49152.0, 135387.5, 133341.4, 68212.3, 35584.0]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "d43ba3290b195f2e", "workloads": {
+        4: {"fetch": [46224.5, 36439.5, 99053.6, 74205.0, 33469.5],
+            "write": [49152.1, 136046.8, 133602.5, 68081.7, 35584.0]}}},
     "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "e4c8c3753f5872ec", "workloads": {
-        4: {"fetch": [61784.1], "write": [169487.7]}}},
+        4: {"fetch": [61791.3], "write": [169487.7]}}},
 }
 
 
