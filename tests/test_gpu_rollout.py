@@ -343,3 +343,32 @@ def test_policy_act_value_equals_separate_calls(cfg, N):
         for name, g, r in zip(("mean", "action", "logp", "value"), got, ref):
             assert torch.equal(g, r), "%s differs from the separate calls" % name
     assert not torch.equal(ref1[3], ref2[3])
+
+
+def test_policy_act_value_errors_before_any_launch():
+    """Without a critic, or with a null value buffer, the combined call fails
+    with the two calls' errors and writes nothing."""
+    d = synth.make_world(2, n_envs=64)
+    N, A = 64, d["policy"]["dims"][-1]
+    obs, env_n = None, None
+    for critic in (False, True):
+        ctx = binding.Context(d, max_envs=N, critic=critic)
+        bufs = ctx.buffers(N)
+        ctx.reset_envs(bufs)
+        obs, env_n = bufs.obs, bufs.env_n
+        m = torch.full((N, A), -9.0, device="cuda")
+        a = torch.full((N, A), -9.0, device="cuda")
+        lp = torch.full((N,), -9.0, device="cuda")
+        v = torch.full((N,), -9.0, device="cuda")
+        if not critic:
+            with pytest.raises(binding.ImError, match="critic"):
+                ctx.policy_act_value(obs, env_n, N, m, a, lp, v)
+        else:
+            with pytest.raises(binding.ImError, match="NULL buffer"):
+                binding.im_policy_act_value(ctx.ptr, obs.data_ptr(), obs.shape[1], env_n.data_ptr(), N,
+                                            m.data_ptr(), a.data_ptr(), lp.data_ptr(), None)
+            with pytest.raises(binding.ImError, match="n_envs"):
+                ctx.policy_act_value(obs, env_n, N + 1, m, a, lp, v)
+        torch.cuda.synchronize()
+        assert bool((m == -9.0).all()) and bool((v == -9.0).all())
+        ctx.close()
