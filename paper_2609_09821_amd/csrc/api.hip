@@ -1139,6 +1139,7 @@ struct TrainLayer {
     uint16_t *wtt = nullptr;               // [Kp][Mp] bf16
     float *bias = nullptr;                 // [Mp]
     uint16_t *act = nullptr;               // hidden output [Mp][Mb] bf16 (null: output layer)
+    uint4 *mbits = nullptr;                // its ReLU mask as bits, tile-major (Mp % 256 == 0)
     void *roll = nullptr;                  // the rollout's packed copy [.][roll_K]
     int roll_K = 0;
     float *roll_bias = nullptr;
@@ -1216,6 +1217,13 @@ im_status tg(bool bt, int epi, const im::TGemm &g, int splits, hipStream_t st)
         if (s_ != IM_OK) return s_;    \
     } while (0)
 
+// Whether a hidden layer's forward writes (and the next layer's input gradient
+// reads) its ReLU mask as bits: 256x256 tiles only.
+bool mbits_ok(const TrainLayer &L, int64_t Mb)
+{
+    return L.mbits && L.Mp % 256 == 0 && Mb % 256 == 0;
+}
+
 // forward of one network's GEMM layers; returns the output of the last one
 im_status net_forward(const std::vector<TrainLayer> &net, const uint16_t *x0, int Kp0, int64_t Mb,
                       bool linear_last, float *out_last, int M_valid, hipStream_t st)
@@ -1244,6 +1252,7 @@ im_status net_forward(const std::vector<TrainLayer> &net, const uint16_t *x0, in
             IM_CHS(tg(true, im::T_LINEAR, g, 1, st));
         } else {
             g.C = L.act;
+            g.mbits = mbits_ok(L, Mb) ? L.mbits : nullptr;
             IM_CHS(tg(true, im::T_HIDDEN, g, 1, st));
         }
         x = L.act;
@@ -1310,6 +1319,8 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         h.ldc = Mb;
         h.mask = X;
         h.ldm = Mb;
+        // the mask bits the forward of layer l - 1 wrote on the same tiles
+        if (mbits_ok(net[l - 1], Mb) && net[l - 1].Mp == L.Kp) h.mbits = net[l - 1].mbits;
         h.rs_part = t->rs_tile;     // the bias gradient of layer l - 1, by column tile
         IM_CHS(tg(true, im::T_MASK, h, 1, st));
         dz_sums = true;
@@ -1557,6 +1568,7 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
                 !alloc(&L.bias, sizeof(float) * L.Mp))
                 return oom();
             if (!out_layer && !alloc(&L.act, (size_t)L.Mp * Mb * 2)) return oom();
+            if (!out_layer && L.Mp % 256 == 0 && !alloc(&L.mbits, (size_t)L.Mp * Mb / 8)) return oom();
             int S, ks;
             splitk_plan((L.Mp / 128) * (wgrad_cols(L) / 128), Mb, &S, &ks);
             sk = std::max(sk, (size_t)S * L.Mp * wgrad_cols(L));

@@ -85,6 +85,9 @@ struct TGemm {
     int M_valid;         // LINEAR: rows written
     double *rs_part;     // MASK, optional: per-tile row sums of the stored (masked, bf16)
                          // output, rs_part[row * (N / tgemm_bn(N)) + column tile]
+    uint4 *mbits;        // optional, 256x256 tiles only: the sign of the stored output as
+                         // bits, tile-major.  HIDDEN writes them (bit = output > 0); MASK
+                         // reads them instead of `mask` (the bits its M x N producer wrote)
 };
 
 // Column tile width of the training GEMM for N columns.

@@ -89,6 +89,12 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
     const int kb = blockIdx.y * g.k_split;
     const int ke = kb + g.k_split < g.K ? kb + g.k_split : g.K;
     const int nk = (ke - kb) / BK;
+    // mask bits (256x256 tiles): the 16 pieces this thread writes in the
+    // epilogue, one byte of 8 samples each, 16 contiguous bytes per thread
+    constexpr bool MBITS = BM == 256 && BN == 256 && (EPI == T_HIDDEN || EPI == T_MASK);
+    uint4 mbits_in = make_uint4(0u, 0u, 0u, 0u);
+    if constexpr (MBITS && EPI == T_MASK)
+        if (g.mbits) mbits_in = g.mbits[(int64_t)blockIdx.x * NT + tid];
 
     const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.A, (short)0, (int)g.a_bytes, 0x00020000);
@@ -220,23 +226,45 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
             }
         __syncthreads();
         // BM rows x BN/8 pieces of 8 samples
+        uint32_t mbits_out[4] = {0u, 0u, 0u, 0u};
+        const uint32_t mbits_w[4] = {mbits_in.x, mbits_in.y, mbits_in.z, mbits_in.w};
 #pragma unroll
         for (int c = 0; c < BM * BQ / NT; ++c) {
             const int v = tid + c * NT;
             const int ml = v / BQ, pc = v % BQ;
             uint4 o = *(const uint4 *)(lds + ml * LDO + pc * 8);
             const int64_t off = (m0 + ml) * g.ldc + n0 + pc * 8;
-            if constexpr (EPI == T_MASK) {
-                const uint4 h = *(const uint4 *)(g.mask + (m0 + ml) * g.ldm + n0 + pc * 8);
-                const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
-                uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+            if constexpr (MBITS && EPI == T_HIDDEN) {
+                // bit 2k (2k+1) of the piece's byte: the low (high) half of word k is > 0
+                const uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+                uint32_t byte = 0u;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    // keep each half where the activation (bf16) is > 0
-                    const uint32_t lo = hw[k] & 0xFFFFu, hi = hw[k] >> 16;
-                    const uint32_t keep = ((lo != 0 && !(lo & 0x8000u)) ? 0x0000FFFFu : 0u) |
-                                          ((hi != 0 && !(hi & 0x8000u)) ? 0xFFFF0000u : 0u);
-                    ow[k] &= keep;
+                    const uint32_t lo = ow[k] & 0xFFFFu, hi = ow[k] >> 16;
+                    byte |= ((lo != 0 && !(lo & 0x8000u)) ? 1u : 0u) << (2 * k);
+                    byte |= ((hi != 0 && !(hi & 0x8000u)) ? 1u : 0u) << (2 * k + 1);
+                }
+                mbits_out[c >> 2] |= byte << (8 * (c & 3));
+            }
+            if constexpr (EPI == T_MASK) {
+                uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+                if (MBITS && g.mbits) {
+                    const uint32_t byte = (mbits_w[c >> 2] >> (8 * (c & 3))) & 0xFFu;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        ow[k] &= ((byte >> (2 * k)) & 1u ? 0x0000FFFFu : 0u) |
+                                 ((byte >> (2 * k + 1)) & 1u ? 0xFFFF0000u : 0u);
+                } else {
+                    const uint4 h = *(const uint4 *)(g.mask + (m0 + ml) * g.ldm + n0 + pc * 8);
+                    const uint32_t hw[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        // keep each half where the activation (bf16) is > 0
+                        const uint32_t lo = hw[k] & 0xFFFFu, hi = hw[k] >> 16;
+                        const uint32_t keep = ((lo != 0 && !(lo & 0x8000u)) ? 0x0000FFFFu : 0u) |
+                                              ((hi != 0 && !(hi & 0x8000u)) ? 0xFFFF0000u : 0u);
+                        ow[k] &= keep;
+                    }
                 }
                 o = make_uint4(ow[0], ow[1], ow[2], ow[3]);
                 if (g.rs_part) {
@@ -253,6 +281,10 @@ __global__ __launch_bounds__(128 * WM) void tgemm_kernel(TGemm g)
             }
             *(uint4 *)((uint16_t *)g.C + off) = o;
         }
+        if constexpr (MBITS && EPI == T_HIDDEN)
+            if (g.mbits)
+                g.mbits[(int64_t)blockIdx.x * NT + tid] =
+                    make_uint4(mbits_out[0], mbits_out[1], mbits_out[2], mbits_out[3]);
     } else {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
