@@ -16,8 +16,6 @@
 // (activations, gradients) or n-major [n][k] (X^T for the weight gradient).
 #include <hip/hip_runtime.h>
 
-#include <type_traits>
-
 #include "device_math.h"
 #include "launch.h"
 
@@ -35,24 +33,25 @@ typedef short v4s_t __attribute__((ext_vector_type(4)));
 // row (DPP row shifts by 1, 2, 4, 8; lanes shifted in from outside the row
 // read zero), then for W = 32 the total of the even row added into the odd
 // row (row broadcast of lane 15).  The order of the additions is fixed.
+// x plus the value DPP control CTRL brings in (0 where it brings none: lanes
+// outside ROW_MASK, or shifted in from outside the row).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float x)
+{
+    const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW_MASK, 0xF, true);
+    return x + __builtin_bit_cast(float, t);
+}
+
 template <int W>
 __device__ __forceinline__ float lane_group_sum(float x)
 {
     static_assert(W == 16 || W == 32, "lane group");
-    auto shr = [](float v, float acc, auto ctrl) {
-        const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), decltype(ctrl)::value,
-                                                  0xF, 0xF, true);
-        return acc + __builtin_bit_cast(float, t);
-    };
-    x = shr(x, x, std::integral_constant<int, 0x111>{});   // row_shr:1
-    x = shr(x, x, std::integral_constant<int, 0x112>{});   // row_shr:2
-    x = shr(x, x, std::integral_constant<int, 0x114>{});   // row_shr:4
-    x = shr(x, x, std::integral_constant<int, 0x118>{});   // row_shr:8
-    if constexpr (W == 32) {
-        // row_bcast:15 into rows 1 and 3 only (row mask 0b1010); rows 0 and 2 add 0
-        const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x142, 0xA, 0xF, false);
-        x += __builtin_bit_cast(float, t);
-    }
+    x = dpp_add<0x111, 0xF>(x);     // row_shr:1
+    x = dpp_add<0x112, 0xF>(x);     // row_shr:2
+    x = dpp_add<0x114, 0xF>(x);     // row_shr:4
+    x = dpp_add<0x118, 0xF>(x);     // row_shr:8
+    if constexpr (W == 32)
+        x = dpp_add<0x142, 0xA>(x); // row_bcast:15 into rows 1 and 3 (row mask 0b1010)
     return x;
 }
 
