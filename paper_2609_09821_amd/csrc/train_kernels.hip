@@ -385,11 +385,26 @@ __global__ __launch_bounds__(256) void head_forward_kernel(const uint16_t *__res
                                                            const float *__restrict__ b,
                                                            float *__restrict__ v)
 {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    // 8 consecutive samples per thread (16-byte loads); each sample's sum runs
+    // over k in order, as one sample per thread would
+    const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
     if (j >= Mb) return;
-    float acc = 0.0f;
-    for (int k = 0; k < K; ++k) acc += w[k] * bf16_to_f32(h[k * Mb + j]);
-    v[j] = acc + b[0];
+    float acc[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+    for (int k = 0; k < K; ++k) {
+        const uint4 x = *(const uint4 *)(h + k * Mb + j);
+        const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+        const float wk = w[k];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc[2 * q] += wk * bf16_to_f32((uint16_t)(xw[q] & 0xFFFFu));
+            acc[2 * q + 1] += wk * bf16_to_f32((uint16_t)(xw[q] >> 16));
+        }
+    }
+    const float4 o0 = make_float4(acc[0] + b[0], acc[1] + b[0], acc[2] + b[0], acc[3] + b[0]);
+    const float4 o1 = make_float4(acc[4] + b[0], acc[5] + b[0], acc[6] + b[0], acc[7] + b[0]);
+    *(float4 *)(v + j) = o0;
+    *(float4 *)(v + j + 4) = o1;
 }
 
 // dZ^T[k][j] = w[k] dV[j] where h[k][j] > 0 (bf16), for the last hidden
@@ -779,7 +794,7 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s)
 hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float *w, const float *b,
                                float *v, hipStream_t s)
 {
-    hipLaunchKernelGGL(head_forward_kernel, dim3((unsigned)((Mb + 255) / 256)), dim3(256), 0, s, h, K,
+    hipLaunchKernelGGL(head_forward_kernel, dim3((unsigned)((Mb / 8 + 255) / 256)), dim3(256), 0, s, h, K,
                        Mb, w, b, v);
     return hipGetLastError();
 }
