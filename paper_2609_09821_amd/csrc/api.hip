@@ -420,7 +420,7 @@ std::string validate(const im_config *cfg, const im_skeleton *sk, const im_clip 
     }
     for (int l = 0; l <= L; ++l)
         if (pol->dims[l] < 1 || pol->dims[l] > 16384) return "layer widths must be in [1, 16384]";
-    if (pol->dims[L] > 128) {
+    if (pol->dims[L] > im::MAX_ACTIONS) {
         *code = IM_ERR_UNSUPPORTED;
         return "action width above 128";
     }

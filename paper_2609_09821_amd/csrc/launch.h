@@ -108,6 +108,7 @@ struct GatherArgs {
 };
 
 constexpr int LOSS_STATS = 4;   // surrogate loss, value loss, KL, clip fraction
+constexpr int MAX_ACTIONS = 128;  // widest policy output (action vector)
 
 struct LossArgs {
     int64_t Mb, Mb_pad;

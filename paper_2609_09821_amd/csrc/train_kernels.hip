@@ -539,7 +539,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void loss_kernel(LossArgs a)
 {
-    __shared__ double red[256];
+    __shared__ double red[4][MAX_ACTIONS + LOSS_STATS];
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int64_t Mb = a.Mb_pad;
     const bool live = j < a.Mb;
@@ -588,39 +588,39 @@ __global__ __launch_bounds__(256) void loss_kernel(LossArgs a)
     } else if (j < Mb) {
         a.dv[j] = 0.0f;
     }
-    if (j < Mb) {
-        for (int k = 0; k < a.A; ++k) {
-            float gm = 0.0f;
-            if (live) {
-                const float sig2 = expf(2.0f * a.log_std[k]);
-                gm = g_logp * (a.act[k * Mb + j] - a.mean[k * Mb + j]) / sig2;
-            }
-            a.dmu[k * Mb + j] = f32_to_bf16_rne(gm);
-        }
-    }
-    // block partials: log-std gradient per action, then the stats
-    const int nf = a.A + LOSS_STATS;
-    for (int f = 0; f < nf; ++f) {
+    // Per action: the mean's gradient (bf16) and the block partial of the
+    // log-std gradient; then the four stats.  Each partial is summed over a
+    // wavefront by a fixed butterfly, and the block's four wave sums are added
+    // in wave order.
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    auto wave_sum = [](double x) {
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+        return x;
+    };
+    for (int k = 0; k < a.A; ++k) {
+        float gm = 0.0f;
         double x = 0.0;
         if (live) {
-            if (f < a.A) {
-                const float sig2 = expf(2.0f * a.log_std[f]);
-                const float d = a.act[f * Mb + j] - a.mean[f * Mb + j];
-                x = (double)g_logp * ((double)d * d / sig2 - 1.0);
-            } else {
-                const int s = f - a.A;
-                x = s == 0 ? l_pi : s == 1 ? l_v : s == 2 ? kl : clipped;
-            }
+            const float sig2 = expf(2.0f * a.log_std[k]);
+            const float d = a.act[k * Mb + j] - a.mean[k * Mb + j];
+            gm = g_logp * d / sig2;
+            x = (double)g_logp * ((double)d * d / sig2 - 1.0);
         }
-        red[threadIdx.x] = x;
-        __syncthreads();
-        for (int h = 128; h > 0; h >>= 1) {
-            if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
-            __syncthreads();
-        }
-        if (threadIdx.x == 0) a.partial[(int64_t)blockIdx.x * nf + f] = red[0];
-        __syncthreads();
+        if (j < Mb) a.dmu[k * Mb + j] = f32_to_bf16_rne(gm);
+        x = wave_sum(x);
+        if (lane == 0) red[wave][k] = x;
     }
+    const float st[LOSS_STATS] = {l_pi, l_v, kl, clipped};
+#pragma unroll
+    for (int q = 0; q < LOSS_STATS; ++q) {
+        const double x = wave_sum(live ? (double)st[q] : 0.0);
+        if (lane == 0) red[wave][a.A + q] = x;
+    }
+    __syncthreads();
+    const int nf = a.A + LOSS_STATS;
+    for (int f = threadIdx.x; f < nf; f += 256)
+        a.partial[(int64_t)blockIdx.x * nf + f] = ((red[0][f] + red[1][f]) + red[2][f]) + red[3][f];
 }
 
 // ---------------------------------------------------------------------------
