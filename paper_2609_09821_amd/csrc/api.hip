@@ -1166,7 +1166,8 @@ struct TrainState {
     double *loss_partial = nullptr, *mb_stats = nullptr, *norm_partial = nullptr;
     double *rowsum_part = nullptr;         // [rows][segments] of the bias-gradient sums
     double *rs_tile = nullptr;             // [rows][column tiles]: row sums of a masked
-                                           // gradient, left by the GEMM that wrote it
+                                           // gradient, left by the kernel that wrote it
+    double *head_part = nullptr;           // [head_K][blocks]: the critic head's weight gradient
     int norm_blocks = 0;
     float *log_std_old = nullptr;
     std::vector<void *> allocs;
@@ -1269,10 +1270,13 @@ int wgrad_cols(const TrainLayer &L) { return (int)round_up(L.Kp, 256); }
 // layer's pre-activation, [Mp][Mb] bf16): weight and bias gradients into
 // t->grad; dz buffers alternate in t->dz starting after `dz`
 im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const uint16_t *x0,
-                       const uint16_t *dz, int64_t Mb, hipStream_t st)
+                       const uint16_t *dz, int64_t Mb, hipStream_t st, int top_parts = 0)
 {
     int pp = dz == t->dz[0] ? 1 : 0;
-    bool dz_sums = false;     // dz came from a masked-gradient GEMM that left its row sums
+    // dz came with its row sums in t->rs_tile, by `parts` column blocks: given
+    // for the top layer (top_parts), then left by each masked-gradient GEMM
+    bool dz_sums = top_parts > 0;
+    int parts = top_parts;
     for (int l = (int)net.size() - 1; l >= 0; --l) {
         const TrainLayer &L = net[l];
         const uint16_t *X = l == 0 ? x0 : net[l - 1].act;
@@ -1298,8 +1302,7 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         IM_CHS(tg(false, im::T_PARTIAL, g, S, st));
         IM_CHK(im::launch_splitk_reduce(t->splitk, S, L.Mp, Nw, L.out, L.in, t->grad + L.w_off, st));
         if (dz_sums)
-            IM_CHK(im::launch_rowsum_finish(t->rs_tile, L.out, (int)(Mb / im::tgemm_bn(Mb)),
-                                            t->grad + L.b_off, st));
+            IM_CHK(im::launch_rowsum_finish(t->rs_tile, L.out, parts, t->grad + L.b_off, st));
         else
             IM_CHK(im::launch_rowsum(true, dz, L.out, Mb, nullptr, t->rowsum_part, t->grad + L.b_off, st));
         if (l == 0) break;
@@ -1324,6 +1327,7 @@ im_status net_backward(TrainState *t, const std::vector<TrainLayer> &net, const 
         h.rs_part = t->rs_tile;     // the bias gradient of layer l - 1, by column tile
         IM_CHS(tg(true, im::T_MASK, h, 1, st));
         dz_sums = true;
+        parts = (int)(Mb / im::tgemm_bn(Mb));
         dz = t->dz[pp];
         pp ^= 1;
     }
@@ -1417,11 +1421,14 @@ im_status run_minibatch(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p
     IM_CHK(im::launch_loss_reduce(lr, st));
     // backward: actor from the output-layer gradient, critic from dV
     IM_CHS(net_backward(t, t->actor, t->x0, t->dmu, Mbp, st));
-    IM_CHK(im::launch_rowsum(true, hl.act, t->head_K, Mbp, t->dv, t->rowsum_part, t->grad + t->head_w_off,
-                             st));
     IM_CHK(im::launch_rowsum(false, t->dv, 1, Mbp, nullptr, t->rowsum_part, t->grad + t->head_b_off, st));
-    IM_CHK(im::launch_head_backward(hl.act, t->head_K, hl.Mp, Mbp, head, t->dv, t->dz[0], st));
-    IM_CHS(net_backward(t, t->critic, t->x0, t->dz[0], Mbp, st));
+    // the head's weight gradient and the top hidden layer's bias-gradient sums
+    // come out of the kernel that forms that layer's gradient
+    const int hparts = (int)((Mbp / 8 + 255) / 256);
+    IM_CHK(im::launch_head_backward(hl.act, t->head_K, hl.Mp, Mbp, head, t->dv, t->dz[0], t->head_part,
+                                    t->rs_tile, st));
+    IM_CHK(im::launch_rowsum_finish(t->head_part, t->head_K, hparts, t->grad + t->head_w_off, st));
+    IM_CHS(net_backward(t, t->critic, t->x0, t->dz[0], Mbp, st, hparts));
     return IM_OK;
 }
 
@@ -1592,6 +1599,7 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     // row sums: rows x segments <= 2048 + rows for any row count
     if (!alloc(&t->rowsum_part, sizeof(double) * (2048 + (size_t)maxw + 1))) return oom();
     if (!alloc(&t->rs_tile, sizeof(double) * (size_t)maxw * (size_t)(Mb / 128 + 1))) return oom();
+    if (!alloc(&t->head_part, sizeof(double) * (size_t)maxw * (size_t)(Mb / 2048 + 1))) return oom();
     // the rollout copies the update refreshes
     for (size_t l = 0; l < t->actor.size(); ++l) {
         t->actor[l].roll = c->d_w[l];

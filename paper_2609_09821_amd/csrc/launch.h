@@ -164,8 +164,10 @@ hipError_t launch_tgemm(bool bt, int epi, const TGemm &g, int splits, hipStream_
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float *w, const float *b,
                                float *v, hipStream_t s);
+// pw, pb (optional): [K][Mb / 2048] float64 partials of the head's weight
+// gradient and of the rows' sums of the stored dz.
 hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
-                                const float *dv, uint16_t *dz, hipStream_t s);
+                                const float *dv, uint16_t *dz, double *pw, double *pb, hipStream_t s);
 // part: [rows][up to 2048 / rows + 1] float64 scratch
 hipError_t launch_rowsum(bool bf16, const void *x, int rows, int64_t Mb, const float *y, double *part,
                          float *out, hipStream_t s);

@@ -409,34 +409,65 @@ __global__ __launch_bounds__(256) void head_forward_kernel(const uint16_t *__res
 
 // dZ^T[k][j] = w[k] dV[j] where h[k][j] > 0 (bf16), for the last hidden
 // layer; rows K..gridDim.y-1 (padding) are zero.  8 samples per thread.
+// Optionally the block's float64 partial sums of row k < K, at
+// [k][blockIdx.x]: pw of h[k][j] dV[j] (the head's weight gradient), pb of
+// the stored dZ^T[k][j] (the layer's bias gradient); each thread's 8 terms in
+// order, a fixed wavefront butterfly, the 4 wave sums in wave order.
 __global__ __launch_bounds__(256) void head_backward_kernel(const uint16_t *__restrict__ h, int K,
                                                             int64_t Mb,
                                                             const float *__restrict__ w,
                                                             const float *__restrict__ dv,
-                                                            uint16_t *__restrict__ dz)
+                                                            uint16_t *__restrict__ dz,
+                                                            double *__restrict__ pw,
+                                                            double *__restrict__ pb)
 {
+    __shared__ double red[2][4];
     const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
     const int k = blockIdx.y;
-    if (j >= Mb) return;
-    uint4 *out = (uint4 *)(dz + k * Mb + j);
-    if (k >= K) {
-        *out = make_uint4(0u, 0u, 0u, 0u);
-        return;
-    }
-    const uint4 x = *(const uint4 *)(h + k * Mb + j);
-    const float4 d0 = *(const float4 *)(dv + j), d1 = *(const float4 *)(dv + j + 4);
-    const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
-    const float wk = w[k];
-    uint32_t o[4];
+    double sw = 0.0, sb = 0.0;
+    if (j < Mb) {
+        uint4 *out = (uint4 *)(dz + k * Mb + j);
+        if (k >= K) {
+            *out = make_uint4(0u, 0u, 0u, 0u);
+        } else {
+            const uint4 x = *(const uint4 *)(h + k * Mb + j);
+            const float4 d0 = *(const float4 *)(dv + j), d1 = *(const float4 *)(dv + j + 4);
+            const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+            const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+            const float wk = w[k];
+            uint32_t o[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const uint32_t lo = xw[q] & 0xFFFFu, hi = xw[q] >> 16;
-        const uint32_t a = (lo != 0 && !(lo & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q]) : 0u;
-        const uint32_t b = (hi != 0 && !(hi & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q + 1]) : 0u;
-        o[q] = a | (b << 16);
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t lo = xw[q] & 0xFFFFu, hi = xw[q] >> 16;
+                const uint32_t a = (lo != 0 && !(lo & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q]) : 0u;
+                const uint32_t b = (hi != 0 && !(hi & 0x8000u)) ? f32_to_bf16_rne(wk * d[2 * q + 1]) : 0u;
+                o[q] = a | (b << 16);
+                sw += (double)bf16_to_f32((uint16_t)lo) * (double)d[2 * q];
+                sw += (double)bf16_to_f32((uint16_t)hi) * (double)d[2 * q + 1];
+                sb += (double)bf16_to_f32((uint16_t)a);
+                sb += (double)bf16_to_f32((uint16_t)b);
+            }
+            *out = make_uint4(o[0], o[1], o[2], o[3]);
+        }
     }
-    *out = make_uint4(o[0], o[1], o[2], o[3]);
+    if (k >= K || (!pw && !pb)) return;     // uniform over the block
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        sw += __shfl_xor(sw, o);
+        sb += __shfl_xor(sb, o);
+    }
+    if (lane == 0) {
+        red[0][wave] = sw;
+        red[1][wave] = sb;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        const double t = ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) +
+                         red[threadIdx.x][3];
+        double *p = threadIdx.x == 0 ? pw : pb;
+        if (p) p[(int64_t)k * gridDim.x + blockIdx.x] = t;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -800,11 +831,11 @@ hipError_t launch_head_forward(const uint16_t *h, int K, int64_t Mb, const float
 }
 
 hipError_t launch_head_backward(const uint16_t *h, int K, int rows, int64_t Mb, const float *w,
-                                const float *dv, uint16_t *dz, hipStream_t s)
+                                const float *dv, uint16_t *dz, double *pw, double *pb, hipStream_t s)
 {
     // Mb is a multiple of 256: 8 samples per thread
     hipLaunchKernelGGL(head_backward_kernel, dim3((unsigned)((Mb / 8 + 255) / 256), (unsigned)rows),
-                       dim3(256), 0, s, h, K, Mb, w, dv, dz);
+                       dim3(256), 0, s, h, K, Mb, w, dv, dz, pw, pb);
     return hipGetLastError();
 }
 
