@@ -31,6 +31,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -96,6 +97,36 @@ def mlp_flops(dims, n_envs):
     return 2.0 * n_envs * sum(dims[i] * dims[i + 1] for i in range(len(dims) - 1))
 
 
+class _Roctx:
+    """roctx ranges around the step's calls (visible to rocprofv3 --marker-trace);
+    no-ops when the marker library is missing."""
+
+    def __init__(self):
+        self.lib = None
+        for name in ("librocprofiler-sdk-roctx.so.1", "libroctx64.so.4"):
+            try:
+                import ctypes
+                lib = ctypes.CDLL(os.path.join("/opt/rocm/lib", name))
+                lib.roctxRangePushA.argtypes = [ctypes.c_char_p]
+                lib.roctxRangePushA.restype = ctypes.c_int
+                lib.roctxRangePop.restype = ctypes.c_int
+                self.lib = lib
+                break
+            except OSError:
+                continue
+
+    def push(self, name):
+        if self.lib is not None:
+            self.lib.roctxRangePushA(name)
+
+    def pop(self):
+        if self.lib is not None:
+            self.lib.roctxRangePop()
+
+
+ROCTX = _Roctx()
+
+
 def run_gpu(wid, steps, warmup, graph=True, flush_mb=0):
     import torch
     from paper_2609_09821_amd import binding, synth
@@ -149,10 +180,14 @@ def run_gpu(wid, steps, warmup, graph=True, flush_mb=0):
             scratch.fill_(float(t))
         if ev is not None:
             ev[0].record(stream)
+        ROCTX.push(b"im_policy_act")
         ctx.policy_act(bufs.obs, bufs.env_n, N, mean, action, logp, stream=stream)
+        ROCTX.pop()
         if ev is not None:
             ev[1].record(stream)
+        ROCTX.push(b"im_env_step_fused")
         ctx.env_step_fused(bufs, stream=stream, with_ref_frame=False)
+        ROCTX.pop()
         if ev is not None:
             ev[2].record(stream)
 
@@ -377,6 +412,24 @@ def run_ppo_update(ctx, desc, ro, reps=2):
     }
 
 
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wid, target_s=16.0):
     """The oracle, as it stands, on a bounded sample of workload `wid`."""
     import oracle
@@ -416,6 +469,8 @@ def cpu_baseline(wid, target_s=16.0):
         "value": 1.0 / per_env,
         "unit": "env-steps/s",
         "cores": oracle.num_threads(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": "one step of the %d-env workload: oracle env step on %d envs (%.2f s), "
                   "oracle MLP+sampling on %d envs (%.2f s); per-env times summed"

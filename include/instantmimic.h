@@ -464,6 +464,41 @@ im_status im_ppo_grad(im_ctx *ctx, const im_ppo_batch *b, const im_ppo_params *p
  * weights (device float [n]). */
 im_status im_ppo_params_get(im_ctx *ctx, float *params, int64_t *n, void *stream);
 
+/*
+ * Buffers of the update's last minibatch (the one im_ppo_grad or
+ * im_ppo_update ran last), for checking its stages one at a time.  Columns
+ * are that minibatch's samples in gather order, padded to a multiple of 256
+ * (padding columns hold the zero-input forward and zero gradients); rows of a
+ * layer are its width padded to 128.
+ *   IM_PPO_BUF_INPUT          bf16 [D128][cols]  observation as the forward reads it
+ *   IM_PPO_BUF_ACTOR_HIDDEN   bf16 [W128][cols]  output of the actor's hidden layer `layer`
+ *                                                (bias, ReLU, rounded to bf16)
+ *   IM_PPO_BUF_CRITIC_HIDDEN  bf16 [W128][cols]  the same for the critic
+ *   IM_PPO_BUF_MEAN           float [A][cols]    policy mean
+ *   IM_PPO_BUF_VALUE          float [1][cols]    value
+ *   IM_PPO_BUF_DMEAN          bf16 [A128][cols]  gradient of the loss with respect to the
+ *                                                mean, as the backward reads it
+ *   IM_PPO_BUF_DVALUE         float [1][cols]    gradient of the loss with respect to the value
+ */
+enum {
+    IM_PPO_BUF_INPUT = 0,
+    IM_PPO_BUF_ACTOR_HIDDEN,
+    IM_PPO_BUF_CRITIC_HIDDEN,
+    IM_PPO_BUF_MEAN,
+    IM_PPO_BUF_VALUE,
+    IM_PPO_BUF_DMEAN,
+    IM_PPO_BUF_DVALUE,
+    IM_PPO_BUFFERS
+};
+
+/* Shape of buffer `buffer` (layer: hidden layer index, else 0) in *rows,
+ * *cols, *elem_bytes (any may be NULL) and, when dst != NULL, a device copy
+ * of it into dst (rows * cols * elem_bytes bytes, enqueued on the stream).
+ * Errors: no training state, no minibatch run yet, buffer or layer out of
+ * range. */
+im_status im_ppo_read(im_ctx *ctx, int32_t buffer, int32_t layer, void *dst, int64_t *rows,
+                      int64_t *cols, int64_t *elem_bytes, void *stream);
+
 const char *im_status_str(im_status s);
 const char *im_last_error(void);
 

@@ -10,7 +10,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# IM_ORACLE_LIB selects another build of oracle.c (e.g. the sanitizer build of
+# build.py --sanitize, run with the sanitizer runtime preloaded)
+_LIB_PATH = os.environ.get("IM_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")

@@ -93,6 +93,8 @@ class ImPpoBatch(C.Structure):
 
 # PPO update statistics (IM_PPO_* order)
 PPO_STATS = ("loss_pi", "loss_v", "kl", "clip_frac", "grad_norm", "minibatches", "lr")
+# im_ppo_read buffers (IM_PPO_BUF_*)
+PPO_BUFFERS = ("input", "actor_hidden", "critic_hidden", "mean", "value", "dmean", "dvalue")
 
 
 class ImInfo(C.Structure):
@@ -105,7 +107,7 @@ EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_p
             "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value",
             "im_policy_act_value", "im_gae",
             "im_ppo_setup", "im_ppo_update", "im_ppo_grad", "im_ppo_params_get",
-            "im_status_str", "im_last_error"]
+            "im_ppo_read", "im_status_str", "im_last_error"]
 
 _lib = None
 
@@ -155,6 +157,9 @@ def lib():
     L.im_ppo_grad.restype = st
     L.im_ppo_params_get.argtypes = [C.c_void_p, C.c_void_p, C.POINTER(C.c_int64), C.c_void_p]
     L.im_ppo_params_get.restype = st
+    L.im_ppo_read.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.POINTER(C.c_int64),
+                              C.POINTER(C.c_int64), C.POINTER(C.c_int64), C.c_void_p]
+    L.im_ppo_read.restype = st
     L.im_status_str.argtypes = [C.c_int]
     L.im_status_str.restype = C.c_char_p
     L.im_last_error.argtypes = []
@@ -246,6 +251,12 @@ def im_ppo_params_get(ctx, params_ptr=None, stream=None):
     n = C.c_int64()
     _check(lib().im_ppo_params_get(ctx, params_ptr, C.byref(n), stream))
     return n.value
+
+
+def im_ppo_read(ctx, buffer, layer, dst_ptr=None, stream=None):
+    r, c, e = C.c_int64(), C.c_int64(), C.c_int64()
+    _check(lib().im_ppo_read(ctx, buffer, layer, dst_ptr, C.byref(r), C.byref(c), C.byref(e), stream))
+    return r.value, c.value, e.value
 
 
 # ------------------------------------------------------------- conveniences
@@ -448,6 +459,17 @@ class Context:
         if out is None:
             return im_ppo_params_get(self.ptr)
         return im_ppo_params_get(self.ptr, _dptr(out), _stream(stream))
+
+    def ppo_read(self, name, layer=0, stream=None):
+        """A copy (device tensor [rows][cols]) of the update buffer `name`
+        (PPO_BUFFERS) of the last minibatch; bf16 buffers as torch.bfloat16."""
+        import torch
+        k = PPO_BUFFERS.index(name)
+        rows, cols, eb = im_ppo_read(self.ptr, k, layer)
+        out = torch.empty((rows, cols), dtype=torch.bfloat16 if eb == 2 else torch.float32,
+                          device="cuda")
+        im_ppo_read(self.ptr, k, layer, _dptr(out), _stream(stream))
+        return out
 
     def gae(self, ro, gamma, lam, summary=True, stream=None):
         """GAE (and, with summary, the rollout summaries) over a RolloutStorage."""

@@ -1170,6 +1170,7 @@ struct TrainState {
     double *head_part = nullptr;           // [head_K][blocks]: the critic head's weight gradient
     int norm_blocks = 0;
     float *log_std_old = nullptr;
+    int64_t last_Mbp = 0;                  // padded samples of the last minibatch run
     std::vector<void *> allocs;
     int64_t bytes = 0;
 };
@@ -1352,6 +1353,7 @@ im_status run_minibatch(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p
     mb_range(n_chunks, p->minibatches, mb, &first, &count);
     const int64_t Mb = count * 64;
     const int64_t Mbp = round_up(Mb, 256);
+    t->last_Mbp = Mbp;
     im::GatherArgs ga{};
     ga.obs = b->obs;
     ga.action = b->action;
@@ -1511,6 +1513,17 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     if (c->critic.L < 2) return fail(IM_ERR_INVALID_ARG, "the PPO update needs a critic with a hidden layer");
     if (max_minibatch < 64 || max_minibatch > ((int64_t)1 << 24))
         return fail(IM_ERR_INVALID_ARG, "max_minibatch must be in [64, 2^24]");
+    {
+        // The training GEMMs address their bf16 [rows][minibatch] operands with
+        // 32-bit byte extents and offsets: every such buffer (rows = a layer
+        // width padded to 128) must stay below 4 GiB.
+        int64_t rows = round_up(c->D, 128);
+        for (int l = 1; l <= c->L; ++l) rows = std::max(rows, round_up(c->dims[l], 128));
+        for (int l = 1; l <= c->critic.L; ++l) rows = std::max(rows, round_up(c->critic.dims[l], 128));
+        if ((uint64_t)rows * (uint64_t)round_up(max_minibatch, 256) * 2 >= ((uint64_t)1 << 32))
+            return fail(IM_ERR_UNSUPPORTED, "minibatch of " + std::to_string(max_minibatch) +
+                                                " samples: a training operand would reach 4 GiB");
+    }
     im_status s = check_device(c);
     if (s != IM_OK) return s;
     hipError_t e = hipDeviceSynchronize();
@@ -1700,6 +1713,44 @@ im_status im_ppo_grad(im_ctx *c, const im_ppo_batch *b, const im_ppo_params *p, 
     if (stats)
         IM_CHK(hipMemcpyAsync(stats, t->mb_stats, sizeof(double) * im::LOSS_STATS,
                               hipMemcpyDeviceToDevice, st));
+    return IM_OK;
+}
+
+im_status im_ppo_read(im_ctx *c, int32_t buffer, int32_t layer, void *dst, int64_t *rows,
+                      int64_t *cols, int64_t *elem_bytes, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    const TrainState *t = c->train;
+    if (!t) return fail(IM_ERR_INVALID_ARG, "no training state (im_ppo_setup)");
+    if (t->last_Mbp <= 0) return fail(IM_ERR_INVALID_ARG, "no minibatch has run yet");
+    if (buffer < 0 || buffer >= IM_PPO_BUFFERS) return fail(IM_ERR_INVALID_ARG, "unknown buffer");
+    const bool hidden = buffer == IM_PPO_BUF_ACTOR_HIDDEN || buffer == IM_PPO_BUF_CRITIC_HIDDEN;
+    if (!hidden && layer != 0) return fail(IM_ERR_INVALID_ARG, "layer must be 0 for this buffer");
+    const void *src = nullptr;
+    int64_t r = 0, eb = 2;
+    switch (buffer) {
+        case IM_PPO_BUF_INPUT: src = t->x0; r = t->Kp0; break;
+        case IM_PPO_BUF_ACTOR_HIDDEN:
+        case IM_PPO_BUF_CRITIC_HIDDEN: {
+            const auto &net = buffer == IM_PPO_BUF_ACTOR_HIDDEN ? t->actor : t->critic;
+            // the actor's last layer is its output, not a hidden layer
+            const int n_hidden = (int)net.size() - (buffer == IM_PPO_BUF_ACTOR_HIDDEN ? 1 : 0);
+            if (layer < 0 || layer >= n_hidden) return fail(IM_ERR_INVALID_ARG, "layer out of range");
+            src = net[layer].act;
+            r = net[layer].Mp;
+            break;
+        }
+        case IM_PPO_BUF_MEAN: src = t->mean_new; r = c->A; eb = 4; break;
+        case IM_PPO_BUF_VALUE: src = t->value_new; r = 1; eb = 4; break;
+        case IM_PPO_BUF_DMEAN: src = t->dmu; r = t->actor.back().Mp; break;
+        default: src = t->dv; r = 1; eb = 4; break;
+    }
+    if (rows) *rows = r;
+    if (cols) *cols = t->last_Mbp;
+    if (elem_bytes) *elem_bytes = eb;
+    if (dst)
+        IM_CHK(hipMemcpyAsync(dst, src, (size_t)(r * t->last_Mbp * eb), hipMemcpyDeviceToDevice,
+                              (hipStream_t)stream));
     return IM_OK;
 }
 

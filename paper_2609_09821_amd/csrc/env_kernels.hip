@@ -624,7 +624,12 @@ __global__ __launch_bounds__(512) void env_step_parts_kernel(EnvArgs a)
     float e_pos = 0.0f, e_ee = 0.0f, e_vel = 0.0f;
     f3 dc = mk3(0.0f, 0.0f, 0.0f);
     MulErr me;
+    // The root height is read before the barrier below: after it, the walk that
+    // owns the root may already be writing a reset root state, and every thread
+    // of the env must decide termination on the same (pre-reset) value.
+    float z_root = 0.0f;
     if (active) {
+        z_root = a.pos[2 * ld + e];
         k = safe_clip(a.env_clip[e], a.n_clips);
         const float phi = a.env_phase[e];
         t1 = a.env_t[e] + 1;
@@ -706,7 +711,6 @@ __global__ __launch_bounds__(512) void env_step_parts_kernel(EnvArgs a)
     }
     (void)nb;
     if (!active) return;
-    const float z_root = a.pos[2 * ld + e];
     const bool term = (t1 > a.grace) && ((z_root < a.h_term) || !(r >= a.r_min));
 
     // 4. masked reset (the same draw in every thread of the env)

@@ -56,11 +56,15 @@ __device__ __forceinline__ float lane_group_sum(float x)
 }
 
 // ---------------------------------------------------------------------------
-// GEMM: 128 x 128 tiles of 4 waves (2 x 2, each 64 x 64 = 2 x 2 MFMA
-// 32x32x16 tiles), K step 64, two LDS stages; loads of stage k+2 are in
-// flight while stage k runs.  k-contiguous operands sit in LDS rows of 72
-// bf16 (144 bytes: fragment reads free of bank conflicts).  A k-major B tile
-// is stored as it lies in memory, [64 k][128 n] in rows of 144 bf16, and its
+// GEMM: tiles of BM = 64 WM rows by BN columns (WM x 2 waves, each wave
+// 64 x BN/2 = 2 x BN/64 MFMA 32x32x16 tiles).  launch_tgemm picks WM = 4
+// (256 rows, 8 waves, 512 threads) when M is a multiple of 256, else WM = 2
+// (128 rows, 4 waves), and BN = 256 when N is a multiple of 256, else 128:
+// 256 x 256 tiles of 8 waves wherever the shape allows.  K step 64, two LDS
+// stages; loads of stage k+2 are in flight while stage k runs.  k-contiguous
+// operands sit in LDS rows of 72 bf16 (144 bytes: fragment reads free of bank
+// conflicts).  A k-major B tile is stored as it lies in memory, [64 k][BN n]
+// in rows of BN + 16 bf16, and its
 // MFMA fragments are read with the LDS transpose read: in every 16-lane
 // group, lane 4j+q addresses row k0+j, columns n0+4q..n0+4q+3, and lane l
 // receives rows k0..k0+3 of column n0+l (two reads give the 8 consecutive k

@@ -260,3 +260,34 @@ def test_policy_unaligned_leading_dimension(cfg):
     ctx.close()
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("cfg", [2, 4, 5, 6])
+def test_reference_sim_state_gives_reward_exactly_one(cfg):
+    # When the simulated state equals the reference, every error term is zero
+    # (or, from fp32 rounding, below 2^-25, where exp(-x) rounds to 1.0f): the
+    # reward is exactly 1 and no env terminates.  Two routes to such a state:
+    # the GPU's own stand-in without noise (the reference at each env's next
+    # phase), and the oracle's float64 reference state rounded to float32.
+    N = 1000
+    d, w, ctx, bufs = _setup(cfg, N)
+    ctx.reset_envs(bufs)
+    st = w.state(N)
+    w.reset_envs(st)
+    for step in range(3):
+        ctx.standin_physics(bufs, 0.0, 0.0)
+        ctx.env_step_fused(bufs)
+        g = H.download(bufs, N)
+        assert (g.reward == np.float32(1.0)).all(), (
+            "GPU stand-in step %d: reward %s" % (step, g.reward[g.reward != 1.0][:5]))
+        assert not g.terminated.any(), "GPU stand-in step %d" % step
+    for step in range(3):
+        w.standin(st, 0.0, 0.0)
+        H.upload_state(st, bufs)
+        ctx.env_step_fused(bufs)
+        w.env_step(st)
+        g = H.download(bufs, N)
+        assert (g.reward == np.float32(1.0)).all(), (
+            "oracle reference state step %d: reward %s" % (step, g.reward[g.reward != 1.0][:5]))
+        assert not g.terminated.any(), "oracle reference state step %d" % step
+        assert (st.reward.astype(np.float32) == np.float32(1.0)).all()

@@ -1,7 +1,8 @@
 """Pins of the tracking reward and the termination rule."""
+import math
+
 import numpy as np
 import pytest
-import torch
 
 import oracle
 from paper_2609_09821_amd import synth
@@ -83,28 +84,38 @@ def test_rigid_translation_moves_only_position_terms(world):
     assert r["e_com"] == pytest.approx(x, rel=1e-9)
 
 
-def test_without_ee_weight_equals_fig5_reward():
-    # The paper's printed tensor code (Fig. 5a), transcribed; with the EE weight at
-    # zero the oracle's reward is that three-term form.
+def test_without_ee_weight_is_the_three_term_reward():
+    # Sec. 4.1 / Fig. 5: the tracking reward is a weighted sum of three
+    # exponentiated errors -- the squared body-position differences summed over
+    # bodies and axes, the same for the body velocities, and the squared
+    # distance between the mass-weighted centres of the simulated and reference
+    # bodies -- with weights 0.60 / 0.25 / 0.15 and scales 4 / 0.25 / 8.  With
+    # the end-effector weight at zero the oracle's reward is that sum, written
+    # out here per body from the definition.
     d = synth.make_world(2, n_envs=1, w_ee=0.0)
+    cfg = d["config"]
+    assert (cfg["c_pose"], cfg["w_pos"], cfg["c_vel"], cfg["w_vel"], cfg["c_com"], cfg["w_com"]) == \
+        (np.float32(0.60), 4.0, np.float32(0.25), 0.25, np.float32(0.15), 8.0)
     w = oracle.World(d)
     P, V = _ref(w)
     m, M = _masses(d)
     for _ in range(10):
         Ps = P + RNG.normal(size=P.shape) * 0.05
         Vs = V + RNG.normal(size=V.shape) * 0.5
-        body_pos, ref_body_pos = torch.tensor(Ps)[None], torch.tensor(P)[None]
-        body_vel, ref_body_vel = torch.tensor(Vs)[None], torch.tensor(V)[None]
-        mt = torch.tensor(m)[:, None]
-        com_pos = (mt * body_pos[0]).sum(0, keepdim=True) / M
-        ref_com_pos = (mt * ref_body_pos[0]).sum(0, keepdim=True) / M
-        pose_err = (body_pos - ref_body_pos).square().sum(dim=(-1, -2))
-        vel_err = (body_vel - ref_body_vel).square().sum(dim=(-1, -2))
-        com_err = (com_pos - ref_com_pos).square().sum(dim=-1)
-        reward = (float(np.float32(0.60)) * torch.exp(-4.0 * pose_err)
-                  + 0.25 * torch.exp(-0.25 * vel_err)
-                  + float(np.float32(0.15)) * torch.exp(-8.0 * com_err))
-        assert w.reward(Ps, Vs, P, V)["r"] == pytest.approx(float(reward[0]), rel=1e-12)
+        pose = vel = 0.0
+        csim, cref = [0.0, 0.0, 0.0], [0.0, 0.0, 0.0]
+        for b in range(w.B):
+            for c in range(3):
+                pose += (float(Ps[b, c]) - float(P[b, c])) ** 2
+                vel += (float(Vs[b, c]) - float(V[b, c])) ** 2
+                csim[c] += float(m[b]) * float(Ps[b, c]) / M
+                cref[c] += float(m[b]) * float(P[b, c]) / M
+        com = sum((csim[c] - cref[c]) ** 2 for c in range(3))
+        # the weights and scales are float32 fields of the step configuration
+        f = lambda k: float(np.float32(cfg[k]))
+        expect = (f("c_pose") * math.exp(-f("w_pos") * pose) + f("c_vel") * math.exp(-f("w_vel") * vel)
+                  + f("c_com") * math.exp(-f("w_com") * com))
+        assert w.reward(Ps, Vs, P, V)["r"] == pytest.approx(expect, rel=1e-12)
 
 
 def test_termination_truth_table():
