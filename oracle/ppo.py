@@ -24,13 +24,19 @@ Gradients come from torch autograd in float64 on the CPU.  For bf16 networks
 the forward rounds the input, the hidden activations and the weights to bf16
 at the same points as the policy forward, and the gradient passes those
 roundings unchanged (straight-through: the float32 master weights are what
-is trained); the backward rounds the gradient with respect to each layer's
-pre-activation to bf16 (the actor's output layer included, the critic's
-scalar output not), which is where a bf16 backward stores it.  One Adam step per minibatch (bias-corrected; the gradient of
-all parameters clipped to a global norm first); with a KL threshold d the
-learning rate is first divided by 1.5 (not below lr_min) when the
-minibatch's KL exceeds 2d and multiplied by 1.5 (not above lr_max) when it is
-below d/2.
+is trained).  The backward itself is exact float64: how an implementation
+stores its intermediate gradients is not part of the method.  One Adam step
+per minibatch (bias-corrected; the gradient of all parameters clipped to a
+global norm first); with a KL threshold d the learning rate is first divided
+by 1.5 (not below lr_min) when the minibatch's KL exceeds 2d and multiplied
+by 1.5 (not above lr_max) when it is below d/2.
+
+Besides the whole minibatch, the stages of the gradient are available one by
+one, so that an implementation can be compared stage by stage on its own
+intermediate values: `layer_forward` (one layer's pre-activation),
+`output_grads` (the loss and its gradient with respect to the policy mean,
+the value and log_std, given a mean and a value) and `backward` (the chain
+rule of an MLP from the gradient at its output).
 """
 import numpy as np
 import torch
@@ -47,30 +53,14 @@ def _r16(x):
     return x + (_bf16(x) - x).detach()
 
 
-class _G16(torch.autograd.Function):
-    """Identity in value; the gradient passing back is rounded to bf16."""
-
-    @staticmethod
-    def forward(ctx, x):
-        return x.view_as(x)
-
-    @staticmethod
-    def backward(ctx, g):
-        return _bf16(g)
-
-
-def _mlp(x, Ws, bs, bf16, round_out_grad=True):
+def _mlp(x, Ws, bs, bf16):
     """bf16: the input, the weights and the hidden activations are rounded to
-    bf16 in the forward, and the gradient with respect to every layer's
-    pre-activation is rounded to bf16 in the backward (the output layer's only
-    with round_out_grad), where the GPU stores them as GEMM operands."""
+    bf16 in the forward (straight-through in the backward)."""
     r = _r16 if bf16 else (lambda t: t)
     h = r(x)
     L = len(Ws)
     for l in range(L):
         h = h @ r(Ws[l]).T + bs[l]
-        if bf16 and (l < L - 1 or round_out_grad):
-            h = _G16.apply(h)
         if l < L - 1:
             h = r(torch.relu(h))
     return h
@@ -105,6 +95,38 @@ def unflat(vec, actor, critic):
     return a, c
 
 
+def _t(a):
+    return torch.tensor(np.asarray(a, np.float64), dtype=torch.float64)
+
+
+def _loss(mu, V, ls, mb, p, adv_mean, adv_std):
+    """The loss terms of a minibatch from the policy mean mu [M][A], the value
+    V [M] and log_std [A] (float64 tensors)."""
+    act = _t(mb["action"])
+    sig = torch.exp(ls)
+    logp = -(((act - mu) ** 2) / (2.0 * sig ** 2) + ls + 0.5 * LOG_2PI).sum(dim=1)
+    ratio = torch.exp(logp - _t(mb["logp_old"]))
+    A = (_t(mb["adv"]) - adv_mean) / (adv_std + 1e-8)
+    eps = p["clip"]
+    l_pi = torch.maximum(-A * ratio, -A * torch.clamp(ratio, 1.0 - eps, 1.0 + eps)).mean()
+    R = _t(mb["ret"])
+    if p["clipped_value_loss"]:
+        Vo = _t(mb["value_old"])
+        Vc = Vo + torch.clamp(V - Vo, -eps, eps)
+        l_v = torch.maximum((V - R) ** 2, (Vc - R) ** 2).mean()
+    else:
+        l_v = ((V - R) ** 2).mean()
+    ent = (ls + 0.5 * (1.0 + LOG_2PI)).sum()
+    loss = l_pi + p["value_coef"] * l_v - p["entropy_coef"] * ent
+    with torch.no_grad():
+        so, sn = torch.exp(_t(mb["log_std_old"])), sig
+        kl = (ls - _t(mb["log_std_old"]) + (so ** 2 + (_t(mb["mean_old"]) - mu) ** 2) / (2.0 * sn ** 2)
+              - 0.5).sum(dim=1).mean()
+        clipfrac = ((ratio - 1.0).abs() > eps).double().mean()
+    return dict(loss=loss, l_pi=l_pi, l_v=l_v, entropy=ent, kl=kl, clipfrac=clipfrac, ratio=ratio,
+                logp=logp)
+
+
 def minibatch(actor, critic, mb, p, adv_mean, adv_std):
     """Loss terms and the float64 gradient (flat_params order) of one minibatch.
 
@@ -112,46 +134,68 @@ def minibatch(actor, critic, mb, p, adv_mean, adv_std):
     action, mean_old [M][A], logp_old, adv, ret, value_old [M]; log_std_old [A].
     p: dict clip, value_coef, entropy_coef, clipped_value_loss."""
     bf16 = bool(actor["bf16"])
-    t = lambda a: torch.tensor(np.asarray(a, np.float64), dtype=torch.float64)
-    aW = [t(W).requires_grad_() for W in actor["W"]]
-    ab = [t(b).requires_grad_() for b in actor["b"]]
-    ls = t(actor["log_std"]).requires_grad_()
-    cW = [t(W).requires_grad_() for W in critic["W"]]
-    cb = [t(b).requires_grad_() for b in critic["b"]]
-    obs = t(mb["obs"])
+    aW = [_t(W).requires_grad_() for W in actor["W"]]
+    ab = [_t(b).requires_grad_() for b in actor["b"]]
+    ls = _t(actor["log_std"]).requires_grad_()
+    cW = [_t(W).requires_grad_() for W in critic["W"]]
+    cb = [_t(b).requires_grad_() for b in critic["b"]]
+    obs = _t(mb["obs"])
     mu = _mlp(obs, aW, ab, bf16)
-    V = _mlp(obs, cW, cb, bf16, round_out_grad=False)[:, 0]
-    act = t(mb["action"])
-    sig = torch.exp(ls)
-    logp = -(((act - mu) ** 2) / (2.0 * sig ** 2) + ls + 0.5 * LOG_2PI).sum(dim=1)
-    ratio = torch.exp(logp - t(mb["logp_old"]))
-    A = (t(mb["adv"]) - adv_mean) / (adv_std + 1e-8)
-    eps = p["clip"]
-    l_pi = torch.maximum(-A * ratio, -A * torch.clamp(ratio, 1.0 - eps, 1.0 + eps)).mean()
-    R = t(mb["ret"])
-    if p["clipped_value_loss"]:
-        Vo = t(mb["value_old"])
-        Vc = Vo + torch.clamp(V - Vo, -eps, eps)
-        l_v = torch.maximum((V - R) ** 2, (Vc - R) ** 2).mean()
-    else:
-        l_v = ((V - R) ** 2).mean()
-    ent = (ls + 0.5 * (1.0 + LOG_2PI)).sum()
-    loss = l_pi + p["value_coef"] * l_v - p["entropy_coef"] * ent
-    loss.backward()
-    ls_old = t(mb["log_std_old"])
-    with torch.no_grad():
-        so, sn = torch.exp(ls_old), sig
-        kl = (ls - ls_old + (so ** 2 + (t(mb["mean_old"]) - mu) ** 2) / (2.0 * sn ** 2)
-              - 0.5).sum(dim=1).mean()
-        clipfrac = ((ratio - 1.0).abs() > eps).double().mean()
+    V = _mlp(obs, cW, cb, bf16)[:, 0]
+    r = _loss(mu, V, ls, mb, p, adv_mean, adv_std)
+    r["loss"].backward()
     g = []
     for W, b in zip(aW, ab):
         g += [W.grad.numpy().ravel(), b.grad.numpy().ravel()]
     g.append(ls.grad.numpy().ravel())
     for W, b in zip(cW, cb):
         g += [W.grad.numpy().ravel(), b.grad.numpy().ravel()]
-    return dict(loss=loss.item(), l_pi=l_pi.item(), l_v=l_v.item(), entropy=ent.item(),
-                kl=float(kl), clipfrac=float(clipfrac), grad=np.concatenate(g))
+    return dict(loss=r["loss"].item(), l_pi=r["l_pi"].item(), l_v=r["l_v"].item(),
+                entropy=r["entropy"].item(), kl=float(r["kl"]), clipfrac=float(r["clipfrac"]),
+                grad=np.concatenate(g))
+
+
+def layer_forward(W, b, x):
+    """Pre-activation z = x W^T + b of one layer in float64, from the values
+    given (for a bf16 network: the bf16 weights and the bf16 input)."""
+    return np.asarray(x, np.float64) @ np.asarray(W, np.float64).T + np.asarray(b, np.float64)
+
+
+def output_grads(mu, V, log_std, mb, p, adv_mean, adv_std):
+    """The loss of a minibatch and its float64 gradient with respect to the
+    policy mean mu [M][A], the value V [M] and log_std [A], given mu and V
+    (e.g. the forward of another implementation).  Also returns each sample's
+    ratio and the gradient with respect to each sample's log-likelihood
+    (through which the surrogate reaches the mean and log_std)."""
+    mu_t = _t(mu).requires_grad_()
+    V_t = _t(V).requires_grad_()
+    ls = _t(log_std).requires_grad_()
+    r = _loss(mu_t, V_t, ls, mb, p, adv_mean, adv_std)
+    r["logp"].retain_grad()
+    r["loss"].backward()
+    return dict(loss=r["loss"].item(), l_pi=r["l_pi"].item(), l_v=r["l_v"].item(),
+                kl=float(r["kl"]), clipfrac=float(r["clipfrac"]),
+                dmu=mu_t.grad.numpy(), dV=V_t.grad.numpy(), dlog_std=ls.grad.numpy(),
+                ratio=r["ratio"].detach().numpy(), dlogp=r["logp"].grad.numpy())
+
+
+def backward(layers, g_out):
+    """The chain rule through an MLP with ReLU hidden layers, in float64.
+
+    layers: [(W_l, x_l)] for l = 0..L-1, W_l [out][in] the weights the forward
+    used and x_l [M][in] the input of layer l (for l > 0 the ReLU output of
+    layer l - 1, so the ReLU passes the gradient where x_l > 0); g_out [M][out]:
+    the gradient of the loss with respect to the last layer's output.
+    Returns [(dW_l, db_l, g_l)] with g_l the gradient with respect to layer l's
+    pre-activation."""
+    out = [None] * len(layers)
+    g = np.asarray(g_out, np.float64)
+    for l in range(len(layers) - 1, -1, -1):
+        W, x = (np.asarray(a, np.float64) for a in layers[l])
+        out[l] = (g.T @ x, g.sum(axis=0), g)
+        if l > 0:
+            g = (g @ W) * (x > 0)
+    return out
 
 
 def adam_step(params, grad, m, v, step, lr, p):

@@ -248,13 +248,73 @@ def test_bf16_network_gradient_passes_the_roundings():
     assert not np.array_equal(r32["grad"], r16["grad"])
 
 
-def test_backward_rounds_the_pre_activation_gradient():
-    # the rounding of the gradient is identity in the forward and rounds in the backward
-    x = torch.tensor([1.0, -3.0], dtype=torch.float64, requires_grad=True)
-    y = ppo._G16.apply(x)
-    assert torch.equal(y, x)
-    y.backward(torch.tensor([1.0 + 2 ** -12, 0.3], dtype=torch.float64))
-    assert x.grad.tolist() == [1.0, float(torch.tensor(0.3).to(torch.bfloat16).double())]
+def _staged(actor, critic, mb, p, am, asd):
+    """The minibatch gradient composed from the staged oracle functions on the
+    oracle's own forward: layer_forward per layer (bf16 rounding points as the
+    policy forward), output_grads at the resulting mean and value, backward
+    through each network."""
+    bf16 = bool(actor["bf16"])
+    r16 = (lambda a: ppo._bf16(torch.tensor(np.asarray(a, np.float64))).numpy()) if bf16 else \
+        (lambda a: np.asarray(a, np.float64))
+
+    def forward(net):
+        x = r16(mb["obs"])
+        layers = []
+        for l, (W, b) in enumerate(zip(net["W"], net["b"])):
+            Wr = r16(W)
+            layers.append((Wr, x))
+            z = ppo.layer_forward(Wr, b, x)
+            x = r16(np.maximum(z, 0.0)) if l + 1 < len(net["W"]) else z
+        return layers, x
+
+    al, mu = forward(actor)
+    cl, V = forward(critic)
+    o = ppo.output_grads(mu, V[:, 0], actor["log_std"], mb, p, am, asd)
+    g = []
+    for dW, db, _ in ppo.backward(al, o["dmu"]):
+        g += [dW.ravel(), db]
+    g.append(o["dlog_std"])
+    for dW, db, _ in ppo.backward(cl, o["dV"][:, None]):
+        g += [dW.ravel(), db]
+    return np.concatenate(g), o, mu
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_staged_gradient_equals_the_minibatch_gradient(bf16):
+    # two routes to the same derivative: torch autograd through the whole
+    # minibatch, and the chain rule written out stage by stage (forward per
+    # layer, loss gradient at the output, backward through each network);
+    # bf16 networks: straight-through at every rounding point in both
+    actor, critic = _nets(D=24, H=(32, 16), A=5, bf16=bf16, seed=11)
+    mb = _mb(actor, M=64, seed=12)
+    p = dict(P, clipped_value_loss=True)
+    r = ppo.minibatch(actor, critic, mb, p, 0.1, 1.3)
+    g, o, mu = _staged(actor, critic, mb, p, 0.1, 1.3)
+    np.testing.assert_allclose(g, r["grad"], rtol=1e-10, atol=1e-13)
+    assert o["loss"] == pytest.approx(r["loss"], rel=1e-12)
+    # the surrogate reaches log_std through each sample's log-likelihood:
+    # d logp_s / d log_std_a = (a - mu)^2 / sigma^2 - 1, plus the entropy term
+    sig = np.exp(actor["log_std"].astype(np.float64))
+    dl = (o["dlogp"][:, None] * ((mb["action"] - mu) ** 2 / sig ** 2 - 1.0)).sum(axis=0)
+    np.testing.assert_allclose(dl - p["entropy_coef"], o["dlog_std"], rtol=1e-10, atol=1e-14)
+
+
+def test_backward_of_a_two_layer_network_by_hand():
+    # y = W1 relu(W0 x + b0) + b1 on two samples, the output gradient given:
+    # the gradients written out element by element
+    W0 = np.array([[1.0, -2.0], [0.5, 0.25], [-1.0, 1.0]])
+    W1 = np.array([[2.0, -1.0, 3.0]])
+    x = np.array([[1.0, 0.5], [-2.0, 1.0]])
+    b0 = np.array([0.1, 0.0, -0.2])
+    h = np.maximum(x @ W0.T + b0, 0.0)      # [[0.1, 0.625, 0.0], [0.0, 0.0, 2.8]]
+    g = np.array([[0.5], [-1.0]])
+    (dW0, db0, g0), (dW1, db1, g1) = ppo.backward([(W0, x), (W1, h)], g)
+    np.testing.assert_allclose(dW1, [[0.5 * 0.1, 0.5 * 0.625, -1.0 * 2.8]])
+    np.testing.assert_allclose(db1, [-0.5])
+    # layer-0 gradient: W1^T g where h > 0: sample 0 units 0, 1; sample 1 unit 2
+    np.testing.assert_allclose(g0, [[1.0, -0.5, 0.0], [0.0, 0.0, -3.0]])
+    np.testing.assert_allclose(dW0, [[1.0, 0.5], [-0.5, -0.25], [6.0, -3.0]])
+    np.testing.assert_allclose(db0, [1.0, -0.5, -3.0])
 
 
 @pytest.mark.parametrize("bf16", [False, True])
