@@ -375,6 +375,22 @@ typedef struct {
 im_status im_gae(im_ctx *ctx, const im_rollout *r, void *stream);
 
 /*
+ * im_gae for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * kernels and results, without a context.  The per-block summary sums go to
+ * a fixed array of the library on the current device (IM_GAE_NOALLOC_MAX_ENVS
+ * / 256 blocks x IM_SUMMARY_FIELDS doubles = 320 KiB, held until the process
+ * ends), whose address is looked up on the first call on each device (or at
+ * im_create on the context's device).  Every call on a device shares that
+ * array: calls that overlap on one GPU (different streams, no ordering) race
+ * and must be ordered by the caller.  The call allocates nothing.
+ * Errors: those of im_gae; n_envs above IM_GAE_NOALLOC_MAX_ENVS is
+ * IM_ERR_UNSUPPORTED.
+ */
+#define IM_GAE_NOALLOC_MAX_ENVS (1 << 20)
+im_status im_gae_noalloc(const im_rollout *r, void *stream);
+
+/*
  * PPO update (Fig. 3 update_policy; objective of Schulman et al. 2017, the
  * paper's configuration table gives its coefficients).  bf16 policies only.
  * Per minibatch: advantages normalised with the rollout's mean and unbiased

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libinstantmimic.so")
 
 IM_OK, IM_ERR_INVALID_ARG, IM_ERR_UNSUPPORTED, IM_ERR_OOM, IM_ERR_HIP = range(5)
 IM_DTYPE_F32, IM_DTYPE_BF16 = 0, 1
+IM_GAE_NOALLOC_MAX_ENVS = 1 << 20   # im_gae_noalloc scratch limit
 IM_JOINT_FREE, IM_JOINT_SPHERICAL, IM_JOINT_REVOLUTE, IM_JOINT_FIXED = range(4)
 IM_SPLIT_AUTO, IM_SPLIT_ONE, IM_SPLIT_HALVES, IM_SPLIT_PATHS = range(4)
 
@@ -105,7 +106,7 @@ class ImInfo(C.Structure):
 
 EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_policy_act",
             "im_reset_envs", "im_standin_physics", "im_set_critic", "im_value",
-            "im_policy_act_value", "im_gae",
+            "im_policy_act_value", "im_gae", "im_gae_noalloc",
             "im_ppo_setup", "im_ppo_update", "im_ppo_grad", "im_ppo_params_get",
             "im_ppo_read", "im_status_str", "im_last_error"]
 
@@ -148,6 +149,8 @@ def lib():
     L.im_policy_act_value.restype = st
     L.im_gae.argtypes = [C.c_void_p, C.POINTER(ImRollout), C.c_void_p]
     L.im_gae.restype = st
+    L.im_gae_noalloc.argtypes = [C.POINTER(ImRollout), C.c_void_p]
+    L.im_gae_noalloc.restype = st
     L.im_ppo_setup.argtypes = [C.c_void_p, C.c_int64]
     L.im_ppo_setup.restype = st
     L.im_ppo_update.argtypes = [C.c_void_p, C.POINTER(ImPpoBatch), C.POINTER(ImPpoParams), C.c_void_p]
@@ -232,6 +235,16 @@ def im_policy_act_value(ctx, obs_ptr, ld_obs, env_n_ptr, n_envs, mean_ptr, actio
 
 def im_gae(ctx, rollout, stream=None):
     _check(lib().im_gae(ctx, C.byref(rollout), stream))
+
+
+def im_gae_noalloc(rollout, stream=None):
+    _check(lib().im_gae_noalloc(C.byref(rollout), stream))
+
+
+def gae_noalloc(ro, gamma, lam, summary=True, stream=None):
+    """im_gae_noalloc over a RolloutStorage (no context; the library's fixed
+    scratch on the current device)."""
+    im_gae_noalloc(ro.struct(gamma, lam, summary), _stream(stream))
 
 
 def im_ppo_setup(ctx, max_minibatch):

@@ -680,6 +680,12 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
         if (pol->dtype == IM_DTYPE_BF16 && max_envs > SMALL_BATCH)
             IM_TRY_ALLOC(c->d_obs16, (size_t)max_envs * (size_t)c->K_pad[0] * 2);
     }
+    {
+        // set-up of im_gae_noalloc's scratch on this device (its address is
+        // looked up once per device, with the device current)
+        double *scratch = nullptr;
+        IM_TRY_HIP(im::gae_scratch_address(c->device, &scratch), "scratch address (hipGetSymbolAddress)");
+    }
 #undef IM_TRY_ALLOC
 #undef IM_TRY_HIP
     *out = c;
@@ -1089,13 +1095,17 @@ im_status im_policy_act_value(im_ctx *c, const float *obs, int64_t ld_obs, const
     return value_layers(c, obs, ld_obs, n_envs, value, st, staged);
 }
 
-im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
+}  // extern "C"
+
+namespace {
+
+// validation shared by im_gae and im_gae_noalloc; max_envs bounds n_envs
+im_status check_rollout(const im_rollout *r, int64_t max_envs, im_status too_many, const char *limit)
 {
-    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
     if (!r) return fail(IM_ERR_INVALID_ARG, "NULL rollout");
     if (r->T < 1) return fail(IM_ERR_INVALID_ARG, "T must be >= 1");
-    if (r->n_envs < 0 || r->n_envs > c->max_envs)
-        return fail(IM_ERR_INVALID_ARG, "n_envs must be in [0, max_envs]");
+    if (r->n_envs < 0) return fail(IM_ERR_INVALID_ARG, "n_envs must be >= 0");
+    if (r->n_envs > max_envs) return fail(too_many, std::string("n_envs above ") + limit);
     if (r->ld < r->n_envs || r->ld < 1) return fail(IM_ERR_INVALID_ARG, "ld must be >= n_envs and >= 1");
     if (!r->reward || !r->terminated || !r->truncated || !r->value || !r->advantage || !r->ret)
         return fail(IM_ERR_INVALID_ARG, "NULL rollout buffer");
@@ -1103,8 +1113,11 @@ im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
         return fail(IM_ERR_INVALID_ARG, "summaries need ep_return and ep_length");
     if (!(r->gamma >= 0.0f && r->gamma <= 1.0f) || !(r->lambda >= 0.0f && r->lambda <= 1.0f))
         return fail(IM_ERR_INVALID_ARG, "gamma and lambda must be in [0, 1]");
-    im_status s = check_device(c);
-    if (s != IM_OK) return s;
+    return IM_OK;
+}
+
+GaeArgs gae_args(const im_rollout *r, double *partial)
+{
     GaeArgs g{};
     g.T = r->T;
     g.n = r->n_envs;
@@ -1120,8 +1133,37 @@ im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
     g.ep_return = r->ep_return;
     g.ep_length = r->ep_length;
     g.summary = r->summary;
-    g.partial = c->d_partial;
-    hipError_t e = launch_gae(g, (hipStream_t)stream);
+    g.partial = partial;
+    return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+im_status im_gae(im_ctx *c, const im_rollout *r, void *stream)
+{
+    if (!c) return fail(IM_ERR_INVALID_ARG, "NULL context");
+    im_status s = check_rollout(r, c->max_envs, IM_ERR_INVALID_ARG, "max_envs");
+    if (s != IM_OK) return s;
+    s = check_device(c);
+    if (s != IM_OK) return s;
+    hipError_t e = launch_gae(gae_args(r, c->d_partial), (hipStream_t)stream);
+    return e == hipSuccess ? IM_OK : hip_fail(e, "gae launch");
+}
+
+im_status im_gae_noalloc(const im_rollout *r, void *stream)
+{
+    im_status s = check_rollout(r, IM_GAE_NOALLOC_MAX_ENVS, IM_ERR_UNSUPPORTED,
+                                "IM_GAE_NOALLOC_MAX_ENVS (the size of the call's scratch)");
+    if (s != IM_OK) return s;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    double *scratch = nullptr;
+    e = im::gae_scratch_address(dev, &scratch);
+    if (e != hipSuccess) return hip_fail(e, "scratch address (hipGetSymbolAddress)");
+    e = launch_gae(gae_args(r, scratch), (hipStream_t)stream);
     return e == hipSuccess ? IM_OK : hip_fail(e, "gae launch");
 }
 

@@ -63,6 +63,9 @@ hipError_t launch_value_head_rows(bool bf16, const void *x, int64_t ld_x, int K,
 hipError_t launch_value_head_obs(const float *obs, int64_t ld, int D, const float *w,
                                  const float *bias, bool bf16, int64_t N, float *value, hipStream_t s);
 hipError_t launch_gae(const GaeArgs &g, hipStream_t s);
+// Device address of im_gae_noalloc's scratch on `device`, which must be the
+// current device (looked up on the first call per device, then cached).
+hipError_t gae_scratch_address(int device, double **out);
 
 // PPO update (train_kernels.hip).
 enum { T_HIDDEN = 0, T_MASK = 1, T_LINEAR = 2, T_PARTIAL = 3 };

@@ -7,10 +7,43 @@
 // wavefront of 64 consecutive envs moves 256 contiguous bytes per step.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "device_math.h"
 #include "launch.h"
 
 namespace im {
+
+// ---------------------------------------------------------------------------
+// Scratch of im_gae_noalloc: the per-block summary sums ([blocks][fields]
+// float64, one block per 256 envs) in a fixed device array instead of the
+// context's buffer, so that the call allocates nothing.  Every device the
+// library runs on holds one copy (320 KiB) until the process ends; all calls
+// on a device share it.
+// ---------------------------------------------------------------------------
+constexpr int64_t GAE_SCRATCH_DOUBLES = (IM_GAE_NOALLOC_MAX_ENVS / 256) * IM_SUMMARY_FIELDS;
+static __device__ __align__(256) double gae_scratch[GAE_SCRATCH_DOUBLES];
+
+hipError_t gae_scratch_address(int device, double **out)
+{
+    // In host code `gae_scratch` only stands for the symbol: its device
+    // address (different on every device) comes from the runtime, once per
+    // device, with that device current.
+    constexpr int MAX_DEVICES = 64;
+    static std::mutex mu;
+    static double *addr[MAX_DEVICES] = {};
+    if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(gae_scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[device] = (double *)p;
+    }
+    *out = addr[device];
+    return hipSuccess;
+}
 
 // ---------------------------------------------------------------------------
 // Value head, last layer: value[e] = b[0] + sum_k w[k] x[e][k] over the last
