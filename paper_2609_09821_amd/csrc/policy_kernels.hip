@@ -581,8 +581,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
 
     if constexpr (!SAMPLE) {
         // bias, ReLU, bf16; the tile is staged env-major in LDS ([env][feature]
-        // rows of BM*2 bytes, 16-byte chunks XOR-swizzled by env) and written
-        // out in whole rows
+        // rows of BM*2 bytes) and written out in whole rows.  A lane's four
+        // features of one env are an 8-byte unit; units are XOR-swizzled by
+        // env % (units per row), so that the 8-byte writes of 32 consecutive
+        // envs hit distinct banks, and read back as 16-byte chunks (an odd
+        // swizzle swaps the chunk's two halves, undone in registers).
         constexpr int CPR = BM / 8;             // 16-byte chunks per staged row
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -599,8 +602,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
                     const float v3 = fmaxf(acc[i][j][4 * grp + 3] + bb.w, 0.0f);
                     const uint32_t lo = pack_bf16x2(v0, v1);
                     const uint32_t hi = pack_bf16x2(v2, v3);
-                    const int chunk = (ml >> 3) ^ (nl & (CPR - 1));
-                    *(uint2 *)(lds + nl * BM + chunk * 8 + 4 * (lane >> 5)) = make_uint2(lo, hi);
+                    const int unit = (ml >> 2) ^ (nl & (2 * CPR - 1));
+                    *(uint2 *)(lds + nl * BM + unit * 4) = make_uint2(lo, hi);
                 }
             }
         __syncthreads();
@@ -611,9 +614,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_kernel(GemmArgs g)
         for (int pass = 0; pass < BN / RPP; ++pass) {
             const int nl = pass * RPP + tid / CPR;
             const int64_t n = n0 + nl;
-            if (n < g.N)
-                *(uint4 *)(Y + n * g.ld_y + m0 + cl * 8) =
-                    *(const uint4 *)(lds + nl * BM + ((cl ^ (nl & (CPR - 1))) * 8));
+            const int sw = nl & (2 * CPR - 1);
+            uint4 v = *(const uint4 *)(lds + nl * BM + ((cl ^ (sw >> 1)) * 8));
+            if (sw & 1) v = make_uint4(v.z, v.w, v.x, v.y);
+            if (n < g.N) *(uint4 *)(Y + n * g.ld_y + m0 + cl * 8) = v;
         }
     } else {
         // every action of an env lies in one wave (WM == 1, m0 == 0)
@@ -737,8 +741,11 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
 
     // the 256 biases of tile ti into LDS buffer ti % 2, by one wave of group 1
     // (whose only other global memory operations are its tile stores)
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)g.bias, (short)0, (int)(g.M_blocks * 256 * 4), 0x00020000);
     auto stage_bias = [&](int ti) {
-        const f32x4_t v = *(const f32x4_t *)(g.bias + tile_m0(ti) + lane * 4);
+        const f32x4_t v = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+            br, (uint32_t)(lane * 16), (uint32_t)(tile_m0(ti) * 4), 0));
         *(f32x4_t *)(&bias_lds[ti & 1][lane * 4]) = v;
     };
 
@@ -786,42 +793,66 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
 
     // Writes this wave's 128x64 block of tile ti (bias from LDS, ReLU, bf16) in
     // four passes of 32 features through the 4 KB slot `ep`: [env][feature]
-    // rows of 64 bytes, 16-byte chunks XOR-swizzled by env % 4, copied out 16
-    // rows per wave instruction.  LDS operations of one wave complete in order,
-    // so the slot needs no barrier between its writes and reads.  Issues exactly
-    // 16 buffer stores (rows past the env count fall outside the buffer and are
-    // dropped, so no store is skipped).
+    // rows of 64 bytes, copied out 16 rows per wave instruction.  A lane's four
+    // features of one env are an 8-byte unit, stored at unit (unit ^ s(env)),
+    // s(env) = ((env >> 1) ^ (env >> 2)) % 8: the 8-byte writes of any 16 (and
+    // of any 32) consecutive envs then hit distinct banks, and the 16-byte
+    // reads of the copy-out stay conflict-free (an odd s swaps a chunk's two
+    // halves, undone in registers).  LDS operations of one wave complete in
+    // order, so the slot needs no barrier between its writes and reads.
+    // Issues exactly 16 buffer stores; rows past the env count get an offset
+    // past the buffer end, so their stores are dropped.
+    //
+    // The lane-dependent offsets are derived from an opaque copy of the lane
+    // id: hoisted out of the K loop they would hold registers the loop needs,
+    // and a spilled register's reload waits for every outstanding vector
+    // memory operation, the K step's operand loads included.
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
         g.y, (short)0, (int)g.y_bytes, 0x00020000);
     auto epilogue = [&](int ti, uint8_t *ep) {
-        const int64_t m0 = tile_m0(ti), n0 = tile_n0(ti);
-        const float *bias = bias_lds[ti & 1];
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const uint32_t m0 = (uint32_t)tile_m0(ti), n0 = (uint32_t)tile_n0(ti);
+        const uint32_t n_env = (uint32_t)g.N, ld_y = (uint32_t)g.ld_y;
+        const float *bias = bias_lds[ti & 1] + grp * 128 + 4 * (ln >> 5);
+        // the swizzle of env j*32 + ln%32 does not depend on j
+        const int e = ln & 31;
+        const int se = ((e >> 1) ^ (e >> 2)) & 7;
+        uint8_t *wbase = ep + e * 64;
+        const int rl = ln >> 2, c = ln & 3;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int nl = j * 32 + (lane & 31);
+                // a base of its own per j keeps the slot writes single 8-byte
+                // stores: merged into one two-address store they are made to
+                // wait for the outstanding global->LDS loads
+                int oj = j * 32 * 64;
+                asm volatile("" : "+v"(oj));
+                uint8_t *wj = wbase + oj;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int fl = 8 * q + 4 * (lane >> 5);
-                    const float4 bb = *(const float4 *)(bias + grp * 128 + i * 32 + fl);
+                    const float4 bb = *(const float4 *)(bias + i * 32 + 8 * q);
                     const float v0 = fmaxf(acc[i][j][4 * q + 0] + bb.x, 0.0f);
                     const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
                     const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
                     const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
                     const uint32_t lo = pack_bf16x2(v0, v1);
                     const uint32_t hi = pack_bf16x2(v2, v3);
-                    const int chunk = q ^ (nl & 3);
-                    *(uint2 *)(ep + nl * 64 + chunk * 16 + 8 * (lane >> 5)) = make_uint2(lo, hi);
+                    const int unit = (2 * q + (ln >> 5)) ^ se;
+                    *(uint2 *)(wj + unit * 8) = make_uint2(lo, hi);
                 }
             }
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                const int row = p * 16 + (lane >> 2), c = lane & 3;
-                const int64_t n = n0 + wi * 64 + row;
-                const u32x4_t v = *(const u32x4_t *)(ep + row * 64 + ((c ^ (row & 3)) * 16));
-                __builtin_amdgcn_raw_buffer_store_b128(
-                    v, yr, (uint32_t)((n * g.ld_y + m0 + grp * 128 + i * 32 + c * 8) * 2), 0, 0);
+                const int row = p * 16 + rl;
+                const int sw = ((row >> 1) ^ (row >> 2)) & 7;
+                u32x4_t v = *(const u32x4_t *)(ep + row * 64 + ((c ^ (sw >> 1)) * 16));
+                if (sw & 1) v = u32x4_t{v[2], v[3], v[0], v[1]};
+                const uint32_t n = n0 + (uint32_t)(wi * 64 + row);
+                const uint32_t off = n < n_env
+                    ? (n * ld_y + m0 + (uint32_t)(grp * 128 + i * 32 + c * 8)) * 2u : 0xFFFFFFF0u;
+                __builtin_amdgcn_raw_buffer_store_b128(v, yr, off, 0, 0);
             }
         }
     };
@@ -842,6 +873,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     for (int st = 0; st < S; ++st) {
         const int buf = st & 1;
         const int kt = st % nk, ti = st / nk;
+        // A finished tile is written first: its writes to the LDS slot would
+        // otherwise be held back (by the compiler's ordering of LDS stores
+        // after direct-to-LDS loads) until the loads issued below had landed.
+        const bool flush = st > 0 && kt == 0;
+        if (flush) {
+            epilogue(ti - 1, my_ep);
+            zero_acc();
+        }
         // group 0: loads of K step st+1 into the other buffer (last read in the two
         // phases before this one).  Group 1, halfway through a tile: the next
         // tile's biases (both groups wrote the previous tile in the tile's first
@@ -851,23 +890,11 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
         } else if (wi == 0 && kt == nk / 2 && ti + 1 < n_tiles) {
             stage_bias(ti + 1);
         }
-        // a finished tile is written after those loads, so that waiting for the
-        // loads below can leave its 16 stores in flight
-        const bool flush = st > 0 && kt == 0;
-        if (flush) {
-            epilogue(ti - 1, my_ep);
-            zero_acc();
-        }
         read_frags(buf);
         wg_barrier();
         mfma_step();
-        // group 0: K step st+1 has landed in LDS.  Vector memory operations of a
-        // wave complete in issue order, so allowing the 16 later stores to be
-        // outstanding still covers every load.
-        if (grp == 0) {
-            if (flush) __builtin_amdgcn_s_waitcnt(0x4F70);   // vmcnt(16)
-            else wait_vmcnt0();
-        }
+        // group 0: K step st+1 has landed in LDS
+        if (grp == 0) wait_vmcnt0();
         wg_barrier();
     }
     if (grp == 0) wg_barrier();

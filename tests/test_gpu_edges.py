@@ -291,3 +291,36 @@ def test_reference_sim_state_gives_reward_exactly_one(cfg):
             "oracle reference state step %d: reward %s" % (step, g.reward[g.reward != 1.0][:5]))
         assert not g.terminated.any(), "oracle reference state step %d" % step
         assert (st.reward.astype(np.float32) == np.float32(1.0)).all()
+
+
+def test_policy_rows_past_the_env_count_near_4_gib():
+    # A 1280-wide hidden layer at 1677721 envs is just under the 4 GiB extent
+    # the policy accepts; the last 256-env tile reaches past 2^32 bytes, where a
+    # store offset taken modulo 2^32 would land in the first env's row.  The
+    # first envs' outputs must equal those of a 65536-env call, which runs the
+    # same kernel on the same first tile.
+    d = synth.make_world(3, n_envs=1)
+    D, A = d["spec"]["mlp"][0], d["spec"]["mlp"][-1]
+    d["policy"] = synth.make_policy(np.random.default_rng(7), [D, 1280, 256, A], True)
+    N_big, N_small, n_cmp = 1677721, 65536, 256
+    assert N_big * 1280 * 2 <= 0xFFFFFFF0 < ((N_big + 255) // 256 * 256) * 1280 * 2
+    g = torch.Generator().manual_seed(11)
+    head = torch.randn((D, N_small), generator=g).cuda()
+    outs = []
+    for N in (N_small, N_big):
+        ctx = binding.Context(d, max_envs=N, critic=False)
+        obs = torch.zeros((D, N), device="cuda")
+        obs[:, :N_small] = head
+        env_n = torch.arange(N, dtype=torch.int32, device="cuda")
+        mean = torch.zeros((N, A), device="cuda")
+        act = torch.zeros((N, A), device="cuda")
+        logp = torch.zeros(N, device="cuda")
+        ctx.policy_act(obs, env_n, N, mean, act, logp)
+        torch.cuda.synchronize()
+        outs.append((mean[:n_cmp].cpu(), act[:n_cmp].cpu(), logp[:n_cmp].cpu()))
+        assert bool(torch.isfinite(act).all())
+        ctx.close()
+        del obs, env_n, mean, act, logp
+        torch.cuda.empty_cache()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
