@@ -644,27 +644,69 @@ static hipError_t launch_bf16(GemmArgs g, int M_pad, hipStream_t s)
 // wave w env columns [64w, 64w+64): 4x2 MFMA tiles of 32x32 each.  The groups
 // alternate between two phases separated by workgroup barriers: while one
 // group runs the 32 MFMAs of a K step from fragments already in its
-// registers, the other reads its fragments of the K step from LDS (group 0
-// also issues the global->LDS loads of the next K step), so each SIMD's MFMA
-// pipe is fed by one wave while the other waits on memory.  Operands move
-// global->LDS without passing through registers (buffer loads with the LDS
-// flag, 16 bytes per lane; past the buffer end they return zero, which pads
-// the env tail).  A 128-byte LDS row holds its eight 16-byte chunks
+// registers, the other reads its fragments of the K step from LDS, so each
+// SIMD's MFMA pipe is fed by one wave while the other waits on memory.
+// Operands move global->LDS without passing through registers (buffer loads
+// with the LDS flag, 16 bytes per lane; past the buffer end they return zero,
+// which pads the env tail).  Issuing them holds up the issuing wave while the
+// CU's memory pipeline drains (about 50 bytes per clock), so a K step's loads
+// are split over its two phases: the reading group issues the activations
+// (group 0) or its weight rows (group 1), and group 0 also issues its weight
+// rows between its MFMAs.  A 128-byte LDS row holds its eight 16-byte chunks
 // XOR-swizzled by (row/2)%8, so that fragment reads of 16 consecutive rows
 // hit distinct banks.  Two LDS stages of 64 KB.
 //
 // One workgroup per CU walks a list of tiles, and the K steps of consecutive
 // tiles form one pipeline: the next tile's first K step is loaded while the
-// current one finishes, and each wave writes out a finished tile (bias, ReLU,
-// bf16) at the start of its next read phase, through an 8 KB LDS slot of its
-// SIMD (the SIMD's two waves use it in different phases), in 128-byte rows.
-// Tiles are ordered so that the workgroups of one XCD (workgroups are dealt
-// to the 8 XCDs round-robin) share env blocks, whose activations then come
-// from that XCD's L2.
+// current one finishes.  A finished tile is written out (bias, ReLU, bf16) by
+// both groups in the same phase, through a 2 KB LDS slot per wave, in
+// 32-byte rows.  Tiles are ordered so that the workgroups of one XCD
+// (workgroups are dealt to the 8 XCDs round-robin) share env blocks, whose
+// activations then come from that XCD's L2.
 // ---------------------------------------------------------------------------
 #define IM_LDS_AS __attribute__((address_space(3)))
 
-__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt immediate that waits until at most n vector memory operations are
+// outstanding (expcnt and lgkmcnt at their maxima)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+static_assert(vmcnt_imm(0) == 0x0F70 && vmcnt_imm(16) == 0x4F70, "s_waitcnt encoding");
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); }
+
+// Global->LDS load of 16 bytes per lane, to LDS byte address lds + 16 * lane
+// (lds wave-uniform), issued through inline assembly: the compiler then does
+// not know that the instruction writes LDS, so it makes no later LDS access
+// wait for it (it cannot tell the buffers apart, and would wait for every
+// such load in flight); the kernel orders these loads itself with vmcnt waits
+// and workgroup barriers.  m0, the instruction's LDS base, is restored.
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds, uint32_t voff,
+                                           uint32_t soff)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %1\n\t"
+                 "buffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(lds), "v"(voff), "s"(rsrc), "s"(soff)
+                 : "memory");
+}
+
+// ReLU of a packed bf16 pair: a bf16 whose sign bit is set is a negative
+// 16-bit integer, so a packed integer max with zero clears exactly the
+// negative values (and -0).
+typedef short im_s16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t relu_bf16x2(uint32_t p)
+{
+    const im_s16x2_t v = __builtin_bit_cast(im_s16x2_t, p);
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(v, (im_s16x2_t){0, 0}));
+}
+
+// LDS byte address of a __shared__ array
+#define IM_LDS_ADDR(arr) ((uint32_t)(size_t)(IM_LDS_AS const void *)(arr))
+__device__ __forceinline__ uint32_t uniform(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
 __device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 __device__ __forceinline__ void wg_barrier()
 {
@@ -679,12 +721,10 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     constexpr int ROWB = BK * 2;                // bytes per LDS row
     constexpr int TILE_B = 256 * ROWB;          // one 256-row operand tile
     constexpr int STAGE_B = 2 * TILE_B;         // weight tile, then activation tile
-    constexpr int EPI_B = 64 * 64;              // epilogue slot: 64 envs x 32 features bf16
+    constexpr int EPI_B = 64 * 32;              // epilogue slot per wave: 64 envs x 16 features bf16
     constexpr int TM = 4, TN = 2, NS = BK / 16;
-    // separate arrays, so that the compiler sees that the global->LDS loads into
-    // the stages never write the epilogue slots or the biases
     __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE_B];
-    __shared__ __attribute__((aligned(16))) uint8_t epi_lds[4 * EPI_B];
+    __shared__ __attribute__((aligned(16))) uint8_t epi_lds[8 * EPI_B];
     __shared__ __attribute__((aligned(16))) float bias_lds[2][256];
 
     const int tid = threadIdx.x;
@@ -711,42 +751,44 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.x, (short)0, (int)g.x_bytes, 0x00020000);
 
-    // Loads (group 0): thread t fills 16-byte slot 256c + t of a stage, c = 0..15;
-    // slots 0..2047 are the weight tile, 2048.. the activation tile.  Slot s of a
-    // tile: row s/8, physical chunk s%8 = t%8, holding logical chunk
-    // (t%8) ^ ((row/2)%8); the row is 32c' + t/8, so the swizzle depends on t only.
+    // Loads: thread t of a group (t = tid % 256) fills 16-byte slot 256c + t of a
+    // tile, c = 0..7: row 32c + t/8, physical chunk t%8, holding logical chunk
+    // (t%8) ^ ((row/2)%8); the swizzle depends on t only.  The weight tile's rows
+    // 0..127 (c = 0..3) are read only by group 0 and rows 128..255 (c = 4..7)
+    // only by group 1, the activation tile by both.
     const int lrow = (tid & 255) >> 3;
     const int lq = (tid & 7) ^ ((lrow >> 1) & 7);
     const uint32_t a_voff = (uint32_t)((lrow * g.K_pad + lq * 8) * 2);
     const uint32_t b_voff = (uint32_t)((lrow * g.ld_x + lq * 8) * 2);
+    const uint32_t lbase = IM_LDS_ADDR(lds) + (uint32_t)(((tid & 255) & ~63) * 16);
     // Activation row offsets stay in the per-lane offset (the part the buffer
     // range check sees), so rows past the env count read as zero; weight rows
     // are always in range.
-    auto issue = [&](int st, int buf) {
+    auto issue_x = [&](int st, int buf) {
         const int ti = st / nk, kt = st - ti * nk;
-        const int64_t m0 = tile_m0(ti), n0 = tile_n0(ti);
-        uint8_t *base = lds + buf * STAGE_B + (tid & ~63) * 16;
-        const uint32_t k2 = (uint32_t)(kt * BK * 2);
+        const int64_t n0 = tile_n0(ti);
+        const uint32_t base = lbase + (uint32_t)(buf * STAGE_B + TILE_B);
+        const uint32_t k2 = uniform((uint32_t)(kt * BK * 2));
 #pragma unroll
         for (int c = 0; c < 8; ++c)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                wr, (IM_LDS_AS void *)(base + c * 256 * 16), 16, a_voff,
-                (uint32_t)(((m0 + 32 * c) * g.K_pad) * 2) + k2, 0, 0);
-#pragma unroll
-        for (int c = 0; c < 8; ++c)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                xr, (IM_LDS_AS void *)(base + TILE_B + c * 256 * 16), 16,
-                b_voff + (uint32_t)(((n0 + 32 * c) * g.ld_x) * 2), k2, 0, 0);
+            lds_load16(xr, uniform(base + c * 256 * 16),
+                       b_voff + (uint32_t)(((n0 + 32 * c) * g.ld_x) * 2), k2);
     };
+    // LDS address and buffer offset of the 32-row group c of the weight tile of
+    // K step st (wave-uniform)
+    auto w_lds = [&](int buf, int c) { return uniform(lbase + (uint32_t)(buf * STAGE_B + c * 256 * 16)); };
+    auto w_off = [&](int st, int c) {
+        const int ti = st / nk, kt = st - ti * nk;
+        return uniform((uint32_t)(((tile_m0(ti) + 32 * c) * g.K_pad) * 2) + (uint32_t)(kt * BK * 2));
+    };
+    auto issue_w = [&](int st, int buf, int c) { lds_load16(wr, w_lds(buf, c), a_voff, w_off(st, c)); };
 
     // the 256 biases of tile ti into LDS buffer ti % 2, by one wave of group 1
-    // (whose only other global memory operations are its tile stores)
     const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g.bias, (short)0, (int)(g.M_blocks * 256 * 4), 0x00020000);
     auto stage_bias = [&](int ti) {
-        const f32x4_t v = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-            br, (uint32_t)(lane * 16), (uint32_t)(tile_m0(ti) * 4), 0));
-        *(f32x4_t *)(&bias_lds[ti & 1][lane * 4]) = v;
+        lds_load16(br, uniform(IM_LDS_ADDR(bias_lds) + (uint32_t)((ti & 1) * 1024)), (uint32_t)(lane * 16),
+                   uniform((uint32_t)(tile_m0(ti) * 4)));
     };
 
     bf16x8_t fa[NS][TM], fb[NS][TN];
@@ -771,42 +813,68 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     };
 
     f32x16_t acc[TM][TN];
-    auto zero_acc = [&]() {
+    // A tile's accumulators start at the bias of their feature (row
+    // 8 (r / 4) + 4 (lane / 32) + r % 4 of MFMA tile i holds feature
+    // grp*128 + 32 i + that row), so the epilogue adds nothing.
+    auto init_acc = [&](int ti) {
+        const float *bias = bias_lds[ti & 1] + grp * 128 + 4 * (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const f32x4_t b = *(const f32x4_t *)(bias + i * 32 + 8 * q);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[i][j][4 * q + r] = b[r];
+            }
+    };
+    auto mfma_sub = [&](int s) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
     };
-    auto mfma_step = [&]() {
+    // The MFMAs of a K step.  With stw >= 0 (group 0), weight rows 0..127 of K
+    // step stw are issued one 32-row group after each substep (addresses formed
+    // before the first MFMA), so that the loads trickle into the memory pipeline
+    // instead of holding up the MFMAs behind a queue of other loads.  One MFMA
+    // sequence with wave-uniform branches: two copies of it exhaust the registers.
+    auto mfma_step = [&](int stw, int bufw) {
+        const bool ld = stw >= 0;
+        uint32_t la[4] = {0, 0, 0, 0}, so[4] = {0, 0, 0, 0};
+        if (ld) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                la[c] = w_lds(bufw, c);
+                so[c] = w_off(stw, c);
+            }
+        }
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+        for (int s = 0; s < NS; ++s) {
+            mfma_sub(s);
+            if (ld) lds_load16(wr, la[s], a_voff, so[s]);
+        }
         __builtin_amdgcn_s_setprio(0);
     };
 
-    // Writes this wave's 128x64 block of tile ti (bias from LDS, ReLU, bf16) in
-    // four passes of 32 features through the 4 KB slot `ep`: [env][feature]
-    // rows of 64 bytes, copied out 16 rows per wave instruction.  A lane's four
+    // Writes this wave's 128x64 block of tile ti (ReLU, bf16; the accumulators
+    // started at the bias) in eight passes of 16 features through its 2 KB slot
+    // `ep`: [env][feature]
+    // rows of 32 bytes, copied out 32 rows per wave instruction.  A lane's four
     // features of one env are an 8-byte unit, stored at unit (unit ^ s(env)),
-    // s(env) = ((env >> 1) ^ (env >> 2)) % 8: the 8-byte writes of any 16 (and
-    // of any 32) consecutive envs then hit distinct banks, and the 16-byte
-    // reads of the copy-out stay conflict-free (an odd s swaps a chunk's two
-    // halves, undone in registers).  LDS operations of one wave complete in
+    // s(env) = ((env >> 2) ^ (env >> 3)) % 4: the 8-byte writes of any 16 (and
+    // of any 32) consecutive envs then hit distinct banks, and so do the 8-byte
+    // reads of the copy-out (two per 16-byte store, since an odd s swaps a
+    // chunk's two halves).  LDS operations of one wave complete in
     // order, so the slot needs no barrier between its writes and reads.
     // Issues exactly 16 buffer stores; rows past the env count get an offset
     // past the buffer end, so their stores are dropped.
     //
     // The lane-dependent offsets are derived from an opaque copy of the lane
-    // id: hoisted out of the K loop they would hold registers the loop needs,
-    // and a spilled register's reload waits for every outstanding vector
-    // memory operation, the K step's operand loads included.
+    // id: hoisted out of the K loop they would hold registers the loop needs.
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
         g.y, (short)0, (int)g.y_bytes, 0x00020000);
     auto epilogue = [&](int ti, uint8_t *ep) {
@@ -814,92 +882,118 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
         asm volatile("" : "+v"(ln));
         const uint32_t m0 = (uint32_t)tile_m0(ti), n0 = (uint32_t)tile_n0(ti);
         const uint32_t n_env = (uint32_t)g.N, ld_y = (uint32_t)g.ld_y;
-        const float *bias = bias_lds[ti & 1] + grp * 128 + 4 * (ln >> 5);
         // the swizzle of env j*32 + ln%32 does not depend on j
         const int e = ln & 31;
-        const int se = ((e >> 1) ^ (e >> 2)) & 7;
-        uint8_t *wbase = ep + e * 64;
-        const int rl = ln >> 2, c = ln & 3;
+        const int se = ((e >> 2) ^ (e >> 3)) & 3;
+        uint8_t *wbase = ep + e * 32;
+        const int rl = ln >> 1, c = ln & 1;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                // a base of its own per j keeps the slot writes single 8-byte
-                // stores: merged into one two-address store they are made to
-                // wait for the outstanding global->LDS loads
-                int oj = j * 32 * 64;
-                asm volatile("" : "+v"(oj));
-                uint8_t *wj = wbase + oj;
+            for (int hq = 0; hq < 2; ++hq) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float4 bb = *(const float4 *)(bias + i * 32 + 8 * q);
-                    const float v0 = fmaxf(acc[i][j][4 * q + 0] + bb.x, 0.0f);
-                    const float v1 = fmaxf(acc[i][j][4 * q + 1] + bb.y, 0.0f);
-                    const float v2 = fmaxf(acc[i][j][4 * q + 2] + bb.z, 0.0f);
-                    const float v3 = fmaxf(acc[i][j][4 * q + 3] + bb.w, 0.0f);
-                    const uint32_t lo = pack_bf16x2(v0, v1);
-                    const uint32_t hi = pack_bf16x2(v2, v3);
-                    const int unit = (2 * q + (ln >> 5)) ^ se;
-                    *(uint2 *)(wj + unit * 8) = make_uint2(lo, hi);
+                for (int j = 0; j < TN; ++j) {
+                    // a base of its own per j keeps the slot writes single 8-byte
+                    // stores (the compiler would otherwise pair them)
+                    int oj = j * 32 * 32;
+                    asm volatile("" : "+v"(oj));
+                    uint8_t *wj = wbase + oj;
+#pragma unroll
+                    for (int q2 = 0; q2 < 2; ++q2) {
+                        const int q = 2 * hq + q2;
+                        const uint32_t lo = relu_bf16x2(pack_bf16x2(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]));
+                        const uint32_t hi = relu_bf16x2(pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+                        const int unit = (2 * q2 + (ln >> 5)) ^ se;
+                        *(uint2 *)(wj + unit * 8) = make_uint2(lo, hi);
+                    }
                 }
-            }
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const int row = p * 16 + rl;
-                const int sw = ((row >> 1) ^ (row >> 2)) & 7;
-                u32x4_t v = *(const u32x4_t *)(ep + row * 64 + ((c ^ (sw >> 1)) * 16));
-                if (sw & 1) v = u32x4_t{v[2], v[3], v[0], v[1]};
-                const uint32_t n = n0 + (uint32_t)(wi * 64 + row);
-                const uint32_t off = n < n_env
-                    ? (n * ld_y + m0 + (uint32_t)(grp * 128 + i * 32 + c * 8)) * 2u : 0xFFFFFFF0u;
-                __builtin_amdgcn_raw_buffer_store_b128(v, yr, off, 0, 0);
+                for (int p = 0; p < 2; ++p) {
+                    // features 8c..8c+7 of the row: logical units 2c and 2c+1, at
+                    // physical units (2c) ^ s and (2c+1) ^ s
+                    const int row = p * 32 + rl;
+                    const int sw = ((row >> 2) ^ (row >> 3)) & 3;
+                    const uint8_t *rp = ep + row * 32 + ((c ^ (sw >> 1)) * 16);
+                    const uint2 a = *(const uint2 *)(rp + (sw & 1) * 8);
+                    const uint2 b = *(const uint2 *)(rp + ((sw & 1) ^ 1) * 8);
+                    const u32x4_t v = {a.x, a.y, b.x, b.y};
+                    const uint32_t n = n0 + (uint32_t)(wi * 64 + row);
+                    const uint32_t off = n < n_env
+                        ? (n * ld_y + m0 + (uint32_t)(grp * 128 + i * 32 + hq * 16 + c * 8)) * 2u
+                        : 0xFFFFFFF0u;
+                    __builtin_amdgcn_raw_buffer_store_b128(v, yr, off, 0, 0);
+                }
             }
         }
     };
 
-    // Both groups run the same pipeline (read K step st; barrier; MFMAs of st;
-    // barrier), group 1 one phase behind group 0: it passes one extra barrier
-    // first, and group 0 one extra barrier at the end so that the counts match.
-    zero_acc();
+    // Phase 2st: group 0 reads K step st and loads the activations of st+1 into
+    // the other buffer (last read by group 1 in phase 2st-1).  Phase 2st+1: group
+    // 0 runs the MFMAs of st and, between them, loads weight rows 0..127 of st+2
+    // into the buffer it has just read (only group 0 reads those rows); group 1
+    // reads st and loads weight rows 128..255 of st+1 (its own rows, last read
+    // in phase 2st-1).  Each phase thus carries half a K step's operand bytes,
+    // and every load has two phases or more to land.  Loads of a wave complete
+    // in issue order: group 0 waits at the end of phase 2st+1 for all but the 4
+    // loads of st+2, group 1 at the end of phase 2st+2 for all of its loads.
     if (grp == 0) {
-        issue(0, 0);
+        issue_x(0, 0);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) issue_w(0, 0, c);
+        if (S > 1) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) issue_w(1, 1, c);
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));
+        } else {
+            wait_vmcnt0();
+        }
+    } else {
+        if (wi == 0) stage_bias(0);
+#pragma unroll
+        for (int c = 4; c < 8; ++c) issue_w(0, 0, c);
         wait_vmcnt0();
-    } else if (wi == 0) {
-        stage_bias(0);
     }
     wg_barrier();
+    init_acc(0);
     if (grp == 1) wg_barrier();
-    uint8_t *my_ep = epi_lds + (wave & 3) * EPI_B;
+    uint8_t *my_ep = epi_lds + wave * EPI_B;
     for (int st = 0; st < S; ++st) {
         const int buf = st & 1;
         const int kt = st % nk, ti = st / nk;
-        // A finished tile is written first: its writes to the LDS slot would
-        // otherwise be held back (by the compiler's ordering of LDS stores
-        // after direct-to-LDS loads) until the loads issued below had landed.
-        const bool flush = st > 0 && kt == 0;
-        if (flush) {
+        // Group 0 writes a finished tile at the start of the tile's next read
+        // phase, group 1 right after the tile's last MFMAs: the same phase, so
+        // that the MFMA pipes stand idle through one epilogue per tile, not two.
+        if (grp == 0 && st > 0 && kt == 0) {
             epilogue(ti - 1, my_ep);
-            zero_acc();
+            init_acc(ti);
         }
-        // group 0: loads of K step st+1 into the other buffer (last read in the two
-        // phases before this one).  Group 1, halfway through a tile: the next
-        // tile's biases (both groups wrote the previous tile in the tile's first
-        // K step, and those stores have long completed).
+        // group 1, in a tile's first K step: the next tile's biases (the
+        // buffer's previous biases were read when the tile before started)
         if (grp == 0) {
-            if (st + 1 < S) issue(st + 1, buf ^ 1);
-        } else if (wi == 0 && kt == nk / 2 && ti + 1 < n_tiles) {
-            stage_bias(ti + 1);
+            if (st + 1 < S) issue_x(st + 1, buf ^ 1);
+        } else {
+            if (wi == 0 && kt == 0 && ti + 1 < n_tiles) stage_bias(ti + 1);
+            if (st + 1 < S) {
+#pragma unroll
+                for (int c = 4; c < 8; ++c) issue_w(st + 1, buf ^ 1, c);
+            }
         }
         read_frags(buf);
         wg_barrier();
-        mfma_step();
-        // group 0: K step st+1 has landed in LDS
-        if (grp == 0) wait_vmcnt0();
+        const bool wt = grp == 0 && st + 2 < S;
+        mfma_step(wt ? st + 2 : -1, buf);
+        if (wt) __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));
+        else wait_vmcnt0();
+        if (grp == 1 && kt == nk - 1) {
+            epilogue(ti, my_ep);
+            if (ti + 1 < n_tiles) init_acc(ti + 1);
+        }
         wg_barrier();
     }
-    if (grp == 0) wg_barrier();
-    // the last tile: every LDS stage is free now, one slot per wave
-    epilogue(n_tiles - 1, lds + wave * EPI_B);
+    if (grp == 0) {
+        wg_barrier();
+        epilogue(n_tiles - 1, my_ep);
+    }
 }
 
 static hipError_t launch_bf16_pp(GemmArgs g, int M_pad, hipStream_t s)
