@@ -47,7 +47,7 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # Measured HBM traffic per launch: rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE passes
 # over this bench (KiB per dispatch, mean over the dispatches of each kernel), each scaled
 # by what the same counter reads over a plain 512 MiB device copy (bench.py
-# --calibrate-copy 512): FETCH_SIZE reported 262167 KiB for 524288 KiB read, WRITE_SIZE
+# --calibrate-copy 512): FETCH_SIZE reported 262166 KiB for 524288 KiB read, WRITE_SIZE
 # 524288 KiB for 524288 KiB written, so the factors are 2.0 and 1.0.  Each entry is keyed
 # by a hash of the kernel's source file and the device headers it includes; once one of
 # them changes the figure no longer describes the kernel and the bench reports null.
@@ -57,11 +57,11 @@ SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act, in order (observation
     # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "d43ba3290b195f2e", "workloads": {
-        4: {"fetch": [46224.5, 36439.5, 99053.6, 74205.0, 33469.5],
-            "write": [49152.1, 136046.8, 133602.5, 68081.7, 35584.0]}}},
-    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "e4c8c3753f5872ec", "workloads": {
-        4: {"fetch": [61791.3], "write": [169487.7]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "7cff8cbbe9e2a1ed", "workloads": {
+        4: {"fetch": [46216.5, 36056.0, 98786.1, 73906.0, 33463.0],
+            "write": [49152.2, 133367.1, 132204.4, 66056.7, 35584.0]}}},
+    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "4a67f5f7314807d4", "workloads": {
+        4: {"fetch": [61794.2], "write": [169487.7]}}},
 }
 
 
@@ -412,6 +412,81 @@ def run_ppo_update(ctx, desc, ro, reps=2):
     }
 
 
+def calibrate_probes():
+    """Measurement probes of the GPU itself (include/instantmimic_calib.h) and
+    of the vendor GEMM on the policy's layer shapes: what the chip sustains for
+    the instruction mixes the step's kernels use.  One JSON line; each figure
+    is the best of 5 timed launches (HIP events on the launch stream)."""
+    import torch
+    import torch.nn.functional as F
+    from paper_2609_09821_amd import binding
+
+    props = torch.cuda.get_device_properties(torch.cuda.current_device())
+    n_cu = props.multi_processor_count
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    def best_ms(launch, reps=5):
+        launch()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return min(ts)
+
+    res = {"n_cu": n_cu, "clock_for_per_clock_figures_ghz": 2.4}
+    blocks = 2 * n_cu               # two wavefronts per SIMD
+    out = torch.empty(256 * blocks, device="cuda")
+    for kind, name, flop, iters in ((binding.IM_CALIB_MFMA_BF16, "mfma_bf16_32x32x16", 32768, 20000),
+                                    (binding.IM_CALIB_MFMA_F32, "mfma_f32_32x32x2", 4096, 10000)):
+        ms = best_ms(lambda: binding.im_calib_mfma(kind, iters, blocks, out.data_ptr(), sp))
+        res[name + "_tflops"] = 4 * blocks * iters * 8 * flop / (ms * 1e-3) / 1e12
+    lds = {}
+    outl = torch.empty(64 * 16 * n_cu, dtype=torch.int32, device="cuda")
+    for width in (16, 8):
+        for waves in (1, 2, 4, 8, 12, 16):
+            iters = 2000
+            ms = best_ms(lambda: binding.im_calib_lds(width, waves, iters, n_cu, outl.data_ptr(), sp))
+            per_cu = waves * 64 * width * 16 * iters / (ms * 1e-3)
+            lds["b%d_w%d" % (8 * width, waves)] = {"gbs_per_cu": per_cu / 1e9,
+                                                  "bytes_per_clk_per_cu": per_cu / 2.4e9}
+    res["lds_read"] = lds
+    rd = {}
+    outr = torch.empty(256 * 8 * n_cu, dtype=torch.int32, device="cuda")
+    for label, mib, passes in (("hbm_1gib", 1024, 1), ("mall_128mib", 128, 8), ("l2_2mib", 2, 256)):
+        buf = torch.ones((mib << 20) // 4, device="cuda")
+        ms = best_ms(lambda: binding.im_calib_read(buf.data_ptr(), mib << 20, passes, 8 * n_cu,
+                                                   outr.data_ptr(), sp))
+        rd[label + "_tbs"] = passes * (mib << 20) / (ms * 1e-3) / 1e12
+        del buf
+    src = torch.ones(128 << 20, device="cuda")      # 512 MiB
+    dst = torch.empty_like(src)
+    ms = best_ms(lambda: dst.copy_(src))
+    rd["copy_512mib_tbs"] = 2 * src.numel() * 4 / (ms * 1e-3) / 1e12
+    del src, dst
+    res["global_read"] = rd
+    blas = {}
+    N = 65536
+    for K, M in ((384, 1024), (1024, 1024), (1024, 512), (512, 96)):
+        x = torch.randn(N, K, device="cuda", dtype=torch.bfloat16)
+        w = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(M, device="cuda", dtype=torch.bfloat16)
+        for label, f in (("linear", lambda: F.linear(x, w)),
+                         ("linear_bias_relu", lambda: torch.relu(F.linear(x, w, b)))):
+            ms = best_ms(f)
+            blas["%s_%dx%dx%d" % (label, N, K, M)] = {"us": ms * 1e3,
+                                                       "tflops": 2 * N * K * M / (ms * 1e-3) / 1e12}
+        del x, w, b
+    res["vendor_gemm_bf16"] = blas
+    print(json.dumps({"calibration": res}), flush=True)
+
+
 def cpu_model():
     """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
     try:
@@ -495,6 +570,9 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                     help="only run a plain device copy of MB mebibytes (profiler calibration "
                          "of the HBM byte counters) and exit")
+    ap.add_argument("--calibrate-probes", action="store_true",
+                    help="only run the GPU measurement probes (MFMA, LDS, global reads, copy, "
+                         "vendor GEMM on the policy's layer shapes), print them and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the env-plus-policy step shards over envs with no "
@@ -505,6 +583,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_probes:
+        calibrate_probes()
+        return
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         src = torch.ones(n, device="cuda")

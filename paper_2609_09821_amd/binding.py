@@ -109,6 +109,9 @@ EXPORTED = ["im_create", "im_destroy", "im_get_info", "im_env_step_fused", "im_p
             "im_policy_act_value", "im_gae", "im_gae_noalloc",
             "im_ppo_setup", "im_ppo_update", "im_ppo_grad", "im_ppo_params_get",
             "im_ppo_read", "im_status_str", "im_last_error"]
+# measurement probes of the GPU (include/instantmimic_calib.h), not the method
+CALIB_EXPORTED = ["im_calib_mfma", "im_calib_lds", "im_calib_read"]
+IM_CALIB_MFMA_BF16, IM_CALIB_MFMA_F32 = 0, 1
 
 _lib = None
 
@@ -167,6 +170,12 @@ def lib():
     L.im_status_str.restype = C.c_char_p
     L.im_last_error.argtypes = []
     L.im_last_error.restype = C.c_char_p
+    L.im_calib_mfma.argtypes = [C.c_int, C.c_int64, C.c_int, C.c_void_p, C.c_void_p]
+    L.im_calib_mfma.restype = st
+    L.im_calib_lds.argtypes = [C.c_int, C.c_int, C.c_int64, C.c_int, C.c_void_p, C.c_void_p]
+    L.im_calib_lds.restype = st
+    L.im_calib_read.argtypes = [C.c_void_p, C.c_int64, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+    L.im_calib_read.restype = st
     _lib = L
     return L
 
@@ -245,6 +254,18 @@ def gae_noalloc(ro, gamma, lam, summary=True, stream=None):
     """im_gae_noalloc over a RolloutStorage (no context; the library's fixed
     scratch on the current device)."""
     im_gae_noalloc(ro.struct(gamma, lam, summary), _stream(stream))
+
+
+def im_calib_mfma(kind, iters, blocks, out_ptr, stream=None):
+    _check(lib().im_calib_mfma(int(kind), int(iters), int(blocks), out_ptr, stream))
+
+
+def im_calib_lds(width, waves, iters, blocks, out_ptr, stream=None):
+    _check(lib().im_calib_lds(int(width), int(waves), int(iters), int(blocks), out_ptr, stream))
+
+
+def im_calib_read(src_ptr, nbytes, passes, blocks, out_ptr, stream=None):
+    _check(lib().im_calib_read(src_ptr, int(nbytes), int(passes), int(blocks), out_ptr, stream))
 
 
 def im_ppo_setup(ctx, max_minibatch):

@@ -3,7 +3,8 @@
     python -m paper_2609_09821_amd.build [-v]
 
 Each .hip source is compiled to an object in parallel, then linked into
-paper_2609_09821_amd/libinstantmimic.so (the C ABI of include/instantmimic.h).
+paper_2609_09821_amd/libinstantmimic.so (the C ABI of include/instantmimic.h,
+and the measurement probes of include/instantmimic_calib.h).
 """
 import concurrent.futures as cf
 import os
@@ -16,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libinstantmimic.so")
 SOURCES = ["api.hip", "env_kernels.hip", "policy_kernels.hip", "rollout_kernels.hip",
-           "train_kernels.hip"]
+           "train_kernels.hip", "calib_kernels.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

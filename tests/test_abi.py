@@ -23,8 +23,11 @@ def lib():
     return binding.lib()
 
 
-def _declared():
-    text = open(HEADER).read()
+CALIB_HEADER = os.path.join(ROOT, "include", "instantmimic_calib.h")
+
+
+def _declared(path=HEADER):
+    text = open(path).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     text = re.sub(r"//[^\n]*", "", text)
     return sorted(set(re.findall(r"\b(im_[a-z_]+)\s*\(", text)))
@@ -275,3 +278,28 @@ def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         binding.lib()
+
+
+def test_calibration_probes_exported_and_argument_checks(lib):
+    # the measurement probes' header: every declared function is exported, and
+    # bad arguments are refused before anything is launched (no GPU here)
+    names = _declared(CALIB_HEADER)
+    assert sorted(binding.CALIB_EXPORTED) == names
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    assert not [n for n in names if n not in exported]
+    buf = C.c_void_p(256)
+    bad = 1   # IM_ERR_INVALID_ARG
+    assert lib.im_calib_mfma(2, 10, 1, buf, None) == bad
+    assert lib.im_calib_mfma(binding.IM_CALIB_MFMA_BF16, 0, 1, buf, None) == bad
+    assert lib.im_calib_mfma(binding.IM_CALIB_MFMA_F32, 10, 0, buf, None) == bad
+    assert lib.im_calib_mfma(binding.IM_CALIB_MFMA_F32, 10, 1, None, None) == bad
+    assert lib.im_calib_lds(12, 4, 10, 1, buf, None) == bad
+    assert lib.im_calib_lds(16, 0, 10, 1, buf, None) == bad
+    assert lib.im_calib_lds(16, 17, 10, 1, buf, None) == bad
+    assert lib.im_calib_lds(8, 4, 0, 1, buf, None) == bad
+    assert lib.im_calib_read(buf, 24, 1, 1, buf, None) == bad        # not a multiple of 16
+    assert lib.im_calib_read(C.c_void_p(264), 32, 1, 1, buf, None) == bad   # unaligned
+    assert lib.im_calib_read(None, 32, 1, 1, buf, None) == bad
+    assert lib.im_calib_read(buf, 32, 0, 1, buf, None) == bad
