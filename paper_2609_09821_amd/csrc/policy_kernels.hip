@@ -677,13 +677,16 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(vmcnt
 // not know that the instruction writes LDS, so it makes no later LDS access
 // wait for it (it cannot tell the buffers apart, and would wait for every
 // such load in flight); the kernel orders these loads itself with vmcnt waits
-// and workgroup barriers.  m0, the instruction's LDS base, is restored.
+// and workgroup barriers.  m0, the instruction's LDS base, is restored; an
+// SALU write of m0 needs one wait state before an LDS-DMA instruction reads
+// it, which the compiler's hazard checks do not supply inside inline assembly.
 __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rsrc, uint32_t lds, uint32_t voff,
                                            uint32_t soff)
 {
     uint32_t saved;
     asm volatile("s_mov_b32 %0, m0\n\t"
                  "s_mov_b32 m0, %1\n\t"
+                 "s_nop 0\n\t"
                  "buffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
                  "s_mov_b32 m0, %0"
                  : "=&s"(saved)
