@@ -199,7 +199,8 @@ class World:
         self.D = int(lib().or_obs_dim(self.ptr))
 
     def __del__(self):
-        if getattr(self, "ptr", None):
+        # at interpreter shutdown the module's globals may already be gone
+        if getattr(self, "ptr", None) and lib is not None:
             lib().or_world_destroy(self.ptr)
             self.ptr = None
 
