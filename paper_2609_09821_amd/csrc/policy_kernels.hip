@@ -61,15 +61,23 @@ __device__ __forceinline__ void sample_epilogue(const GemmArgs &g, float *so, in
 {
     const int lane = tid & 63;
     const int A = g.A;
-    // per action sigma = exp(log_std), and the noise-free part of -logp,
-    // sum over actions of (log_std + log(2 pi) / 2), once per block
+    // Once per block, in LDS: the biases and sigma = exp(log_std) of every
+    // action (each lane's values then add an LDS read, not a global load in
+    // its own divergent branch), and the noise-free part of -logp, the sum over
+    // actions of log_std + log(2 pi) / 2, by wave 0 in a fixed butterfly.
     __shared__ float sig[TM * 32];
+    __shared__ float sbias[TM * 32];
     __shared__ float lp0;
-    for (int m = tid; m < A; m += NTHR) sig[m] = expf(g.log_std[m]);
-    if (tid == 0) {
+    for (int m = tid; m < A; m += NTHR) {
+        sig[m] = expf(g.log_std[m]);
+        sbias[m] = g.bias[m];
+    }
+    if (tid < 64) {
         float c = 0.0f;
-        for (int m = 0; m < A; ++m) c += g.log_std[m] + HALF_LOG_2PI;
-        lp0 = c;
+        for (int m = tid; m < A; m += 64) c += g.log_std[m] + HALF_LOG_2PI;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+        if (tid == 0) lp0 = c;
     }
     __syncthreads();
 #pragma unroll
@@ -91,7 +99,7 @@ __device__ __forceinline__ void sample_epilogue(const GemmArgs &g, float *so, in
                 for (int q = 0; q < 4; ++q) {
                     const int m = mb + q;
                     if (m < A) {
-                        const float mu = acc[i][j][4 * grp + q] + g.bias[m];
+                        const float mu = acc[i][j][4 * grp + q] + sbias[m];
                         so[nl * A + m] = mu;
                         acc[i][j][4 * grp + q] = mu + sig[m] * z[q];
                         lp += 0.5f * z[q] * z[q];
