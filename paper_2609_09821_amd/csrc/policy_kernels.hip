@@ -882,7 +882,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
     // chunk's two halves).  LDS operations of one wave complete in
     // order, so the slot needs no barrier between its writes and reads.
     // Issues exactly 16 buffer stores; rows past the env count get an offset
-    // past the buffer end, so their stores are dropped.
+    // past the buffer end (the buffer range check drops such stores).
     //
     // The lane-dependent offsets are derived from an opaque copy of the lane
     // id: hoisted out of the K loop they would hold registers the loop needs.
@@ -904,11 +904,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
             for (int hq = 0; hq < 2; ++hq) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    // a base of its own per j keeps the slot writes single 8-byte
-                    // stores (the compiler would otherwise pair them)
-                    int oj = j * 32 * 32;
-                    asm volatile("" : "+v"(oj));
-                    uint8_t *wj = wbase + oj;
+                    uint8_t *wj = wbase + j * 32 * 32;
 #pragma unroll
                     for (int q2 = 0; q2 < 2; ++q2) {
                         const int q = 2 * hq + q2;
@@ -928,10 +924,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(GemmArgs g)
                     const uint2 a = *(const uint2 *)(rp + (sw & 1) * 8);
                     const uint2 b = *(const uint2 *)(rp + ((sw & 1) ^ 1) * 8);
                     const u32x4_t v = {a.x, a.y, b.x, b.y};
+                    // a row past the env count gets offset 0xFFFFFFF0 (all ones
+                    // ORed in, no branch; offsets are multiples of 16), past every
+                    // buffer the library accepts, with no dword of the store
+                    // wrapping around 2^32
                     const uint32_t n = n0 + (uint32_t)(wi * 64 + row);
-                    const uint32_t off = n < n_env
-                        ? (n * ld_y + m0 + (uint32_t)(grp * 128 + i * 32 + hq * 16 + c * 8)) * 2u
-                        : 0xFFFFFFF0u;
+                    const uint32_t off =
+                        (((n * ld_y + m0 + (uint32_t)(grp * 128 + i * 32 + hq * 16 + c * 8)) * 2u) |
+                         (0u - (uint32_t)(n >= n_env))) & 0xFFFFFFF0u;
                     __builtin_amdgcn_raw_buffer_store_b128(v, yr, off, 0, 0);
                 }
             }
