@@ -57,11 +57,11 @@ SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act, in order (observation
     # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "7cff8cbbe9e2a1ed", "workloads": {
-        4: {"fetch": [46216.5, 36056.0, 98786.1, 73906.0, 33463.0],
-            "write": [49152.2, 133367.1, 132204.4, 66056.7, 35584.0]}}},
-    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "4a67f5f7314807d4", "workloads": {
-        4: {"fetch": [61794.2], "write": [169487.7]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "e2db6d6939c049eb", "workloads": {
+        4: {"fetch": [46224.5, 36279.3, 98713.8, 73901.1, 33455.5],
+            "write": [49152.0, 132820.0, 131625.8, 65841.9, 35584.0]}}},
+    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "227c1405eaae8b00", "workloads": {
+        4: {"fetch": [61792.6], "write": [169487.7]}}},
 }
 
 
