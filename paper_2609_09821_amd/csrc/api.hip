@@ -40,6 +40,9 @@ struct im_ctx {
     std::vector<int> dims, M_pad, K_pad;
     std::vector<void *> d_w;
     std::vector<float *> d_b;
+    // bf16 policies that the one-launch small-batch kernel holds: each layer's
+    // weights again, in MFMA fragment order (empty otherwise)
+    std::vector<uint16_t *> d_wf;
     float *d_log_std = nullptr;
     void *d_ws[2] = {nullptr, nullptr};
     void *d_obs16 = nullptr;   // bf16 [max_envs][K_pad[0]] staging of the observation
@@ -78,6 +81,16 @@ im_status hip_fail(hipError_t e, const char *what)
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// A bf16 policy whose widths the one-launch small-batch kernel holds.
+bool fused_policy_fits(const im_ctx *c)
+{
+    if (c->L > FUSED_MAX_LAYERS || c->K_pad[0] > FUSED_MAX_WIDTH || c->M_pad[c->L - 1] > 128)
+        return false;
+    for (int l = 0; l + 1 < c->L; ++l)
+        if (c->M_pad[l] > FUSED_MAX_WIDTH) return false;
+    return true;
+}
+
 bool finite_f(float x) { return std::isfinite(x); }
 
 bool unit_quat(const float *q, double tol)
@@ -112,6 +125,7 @@ void free_ctx(im_ctx *c)
     hipFree(c->d_seg);
     for (void *p : c->d_w) hipFree(p);
     for (float *p : c->d_b) hipFree(p);
+    for (uint16_t *p : c->d_wf) hipFree(p);
     hipFree(c->d_log_std);
     hipFree(c->d_ws[0]);
     hipFree(c->d_ws[1]);
@@ -663,6 +677,20 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
         IM_TRY_HIP(hipMemcpy(db, bbuf.data(), sizeof(float) * bbuf.size(), hipMemcpyHostToDevice),
                    "upload biases");
     }
+    if (pol->dtype == IM_DTYPE_BF16 && fused_policy_fits(c)) {
+        for (int l = 0; l < c->L; ++l) {
+            const int M = c->dims[l + 1], K = c->dims[l], nks = c->K_pad[l] / 64;
+            std::vector<uint16_t> fbuf((size_t)c->M_pad[l] * c->K_pad[l], 0);
+            const uint16_t *src = (const uint16_t *)pol->weight[l];
+            for (int m = 0; m < M; ++m)
+                for (int k = 0; k < K; ++k) fbuf[im::frag_index(m, k, nks)] = src[(size_t)m * K + k];
+            uint16_t *dwf = nullptr;
+            IM_TRY_ALLOC(dwf, fbuf.size() * 2);
+            c->d_wf.push_back(dwf);
+            IM_TRY_HIP(hipMemcpy(dwf, fbuf.data(), fbuf.size() * 2, hipMemcpyHostToDevice),
+                       "upload weights (fragment order)");
+        }
+    }
     IM_TRY_ALLOC(c->d_log_std, sizeof(float) * c->A);
     IM_TRY_HIP(hipMemcpy(c->d_log_std, pol->log_std, sizeof(float) * c->A, hipMemcpyHostToDevice),
                "upload log_std");
@@ -809,6 +837,34 @@ im_status policy_layers(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
 {
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
     const uint64_t esz = bf16 ? 2 : 4;
+    if (bf16 && n_envs <= SMALL_BATCH && !c->d_wf.empty()) {
+        FusedMlpArgs f{};
+        f.obs = obs;
+        f.ld_obs = ld_obs;
+        f.obs_bytes = (uint32_t)((uint64_t)c->D * (uint64_t)ld_obs * 4);
+        f.D = c->D;
+        f.L = c->L;
+        for (int l = 0; l < c->L; ++l) {
+            f.w[l] = c->d_wf[l];
+            f.bias[l] = c->d_b[l];
+            f.w_bytes[l] = (uint32_t)((uint64_t)c->M_pad[l] * (uint64_t)c->K_pad[l] * 2);
+            f.M_pad[l] = c->M_pad[l];
+            f.K_pad[l] = c->K_pad[l];
+        }
+        GemmArgs &g = f.out;
+        g.N = n_envs;
+        g.bias = c->d_b[c->L - 1];
+        g.mean = mean;
+        g.action = action;
+        g.logp = logp;
+        g.env_n = env_n;
+        g.log_std = c->d_log_std;
+        g.A = c->A;
+        g.seed = c->cfg.seed;
+        hipError_t e = launch_policy_fused(f, stream);
+        if (e != hipSuccess) return hip_fail(e, "fused policy launch");
+        return IM_OK;
+    }
     for (int l = 0; l < c->L; ++l) {
         GemmArgs g{};
         const bool last = l == c->L - 1;
@@ -1184,6 +1240,7 @@ struct TrainLayer {
     uint4 *mbits = nullptr;                // its ReLU mask as bits, tile-major (Mp % 256 == 0)
     void *roll = nullptr;                  // the rollout's packed copy [.][roll_K]
     int roll_K = 0;
+    uint16_t *rollf = nullptr;             // the rollout's fragment-order copy, or null
     float *roll_bias = nullptr;
 };
 
@@ -1493,6 +1550,7 @@ im_status repack_all(im_ctx *c, hipStream_t st)
             r.Kp = L.Kp;
             r.roll = L.roll;
             r.roll_K = L.roll_K;
+            r.rollf = L.rollf;
             r.roll_bf16 = 1;
             r.bias_train = L.bias;
             r.bias_roll = L.roll_bias;
@@ -1659,6 +1717,7 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     for (size_t l = 0; l < t->actor.size(); ++l) {
         t->actor[l].roll = c->d_w[l];
         t->actor[l].roll_K = c->K_pad[l];
+        t->actor[l].rollf = c->d_wf.empty() ? nullptr : c->d_wf[l];
         t->actor[l].roll_bias = c->d_b[l];
     }
     for (size_t l = 0; l < t->critic.size(); ++l) {

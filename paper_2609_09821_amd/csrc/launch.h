@@ -43,6 +43,39 @@ struct GemmArgs {
                          // earlier layer of the same call), the staging pass is skipped
 };
 
+// The whole bf16 policy in one launch for small batches (policy_kernels.hip):
+// hidden widths M_pad[l] multiples of 256 up to FUSED_MAX_WIDTH, observation
+// width K_pad[0] up to FUSED_MAX_WIDTH, at most 128 padded actions.
+constexpr int FUSED_MAX_LAYERS = 8;
+constexpr int FUSED_MAX_WIDTH = 1024;
+
+// Index of weight (o, i) of a bf16 [M_pad][K_pad] layer (K_pad = 64 nks) in
+// MFMA fragment order: 1 KB blocks, one per (32-row tile t, K step ks of 64,
+// substep s of 16), block b = (t nks + ks) 4 + s holding, for lane
+// l = 32 h + r, the eight weights k = 64 ks + 16 s + 8 h .. +7 of row 32 t + r.
+// A wavefront then loads the A operand of one MFMA as 1 KB of consecutive
+// bytes, 16 per lane.
+__host__ __device__ inline int64_t frag_index(int o, int i, int nks)
+{
+    const int t = o >> 5, r = o & 31, ks = i >> 6, s = (i >> 4) & 3, h = (i >> 3) & 1;
+    return ((((int64_t)t * nks + ks) * 4 + s) * 64 + 32 * h + r) * 8 + (i & 7);
+}
+
+struct FusedMlpArgs {
+    const float *obs;    // [D][ld_obs] fp32, env fastest
+    int64_t ld_obs;
+    uint32_t obs_bytes;  // D * ld_obs * 4
+    int D;
+    int L;
+    const uint16_t *w[FUSED_MAX_LAYERS];   // M_pad x K_pad bf16 in fragment order (frag_index)
+    const float *bias[FUSED_MAX_LAYERS];   // [M_pad]
+    uint32_t w_bytes[FUSED_MAX_LAYERS];
+    int M_pad[FUSED_MAX_LAYERS], K_pad[FUSED_MAX_LAYERS];
+    GemmArgs out;        // sampling epilogue: N, bias (last layer), mean, action, logp,
+                         // env_n, log_std, A, seed
+};
+hipError_t launch_policy_fused(const FusedMlpArgs &f, hipStream_t s);
+
 // Rollout end (rollout_kernels.hip).
 struct GaeArgs {
     int T;
@@ -160,6 +193,8 @@ struct RepackArgs {
     int Mp, Kp;
     void *roll;            // rollout copy [.][roll_K] or null
     int roll_K, roll_bf16; // 1: bf16, 2: fp32 of the bf16-rounded value, 0: fp32
+    uint16_t *rollf;       // bf16 rollout copy in fragment order (frag_index, K_pad =
+                           // roll_K) or null
     float *bias_train, *bias_roll;
 };
 

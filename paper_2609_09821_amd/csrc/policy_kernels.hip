@@ -1076,6 +1076,254 @@ __global__ __launch_bounds__(256) void stage_obs_bf16_kernel(const float *__rest
     }
 }
 
+// ---------------------------------------------------------------------------
+// The whole bf16 policy in one kernel for small batches.  One workgroup of 8
+// waves per 64 envs runs every layer; between layers the activations stay in
+// LDS as [64 envs][K] bf16 rows whose 16-byte chunks (8 features) are
+// XOR-swizzled by env % 16, so that the fragment reads and the output writes
+// of 16 consecutive envs hit distinct banks.  At 16384 envs that is one
+// workgroup per CU, and no activation goes through memory.
+//
+// Hidden layer of width M: wave w owns output features [w M/8, (w+1) M/8),
+// M/256 MFMA tiles of 32 rows, for all 64 envs (2 tiles of 32).  Its weight
+// fragments (A operand) come from global memory straight into registers,
+// loaded one K step (64) ahead: every workgroup reads the same weights, which
+// stay in the L2.  The env fragments (B operand) are read from LDS.  The
+// accumulators start at the bias; once every wave has read the layer's input
+// (workgroup barrier) they are written over it: ReLU, bf16, and the two half
+// waves trade four-feature groups so that each lane stores whole 16-byte
+// chunks.  The last layer runs on waves 0 and 1 (32 envs each, every action),
+// then all waves take part in the sampling epilogue.
+// ---------------------------------------------------------------------------
+constexpr int FUSED_BN = 64;                      // envs per workgroup
+constexpr int FUSED_ROW = FUSED_MAX_WIDTH * 2;    // LDS bytes per env
+
+// LDS byte offset of 16-byte chunk c of env e in rows of rs bytes
+__device__ __forceinline__ uint32_t fused_off(int e, int c, int rs)
+{
+    return (uint32_t)(e * rs + ((c ^ (e & 15)) << 4));
+}
+
+// acc[TM][TN] += W[rows][K] X[envs][K]^T: rows w_row0 + 32 mt + lane % 32 of
+// the weights (w in fragment order, frag_index), envs e0 + 32 nt + lane % 32
+// of the LDS rows (rs bytes each).  MFMA substep s of K step ks takes
+// k = 64 ks + 16 s + 8 (lane / 32) .. +7 for both operands; its weight
+// fragment is one 1 KB block, 16 consecutive bytes per lane (in the weights'
+// row-major layout a wavefront's 16-byte pieces would lie in 32 rows, and the
+// vector L1 serves such a load at a fraction of the rate of whole lines).
+// The weight loads of K step ks + 1 are issued right after the MFMAs of the
+// same substep of step ks (held there by scheduling barriers: the compiler
+// would otherwise gather them at the end of the step); in the last step they
+// go through a descriptor of extent zero, which makes them return zero
+// without a memory access (a branch around them would make the compiler copy
+// the fragments).  The env fragments of the next substep are read from LDS
+// before the MFMAs of the current one.
+template <int TM, int TN>
+__device__ __forceinline__ void fused_mma(const uint16_t *w, uint32_t w_bytes, int w_row0, int K,
+                                          const uint8_t *act, int rs, int e0, int lane,
+                                          f32x16_t (&acc)[TM][TN])
+{
+    const int r = lane & 31, h = lane >> 5;
+    const int nks = K / 64;
+    const __amdgpu_buffer_rsrc_t wr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, (int)w_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t wr0 = __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, 0, 0x00020000);
+    uint32_t vo[TM];
+#pragma unroll
+    for (int mt = 0; mt < TM; ++mt) vo[mt] = (uint32_t)((w_row0 / 32 + mt) * nks * 4096 + 16 * lane);
+    // the caller's loads (the biases the accumulators start from) complete
+    // here, so that no wait for them lands inside the loop
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_sched_barrier(0);
+    // in the order of the loop's own loads, which its waits count on
+    u32x4_t wa[TM][4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int mt = 0; mt < TM; ++mt)
+            wa[mt][s] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                        wr, vo[mt] + 1024 * s, 0, 0));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    bf16x8_t bn[TN];
+#pragma unroll
+    for (int nt = 0; nt < TN; ++nt) bn[nt] = *(const bf16x8_t *)(act + fused_off(e0 + 32 * nt + r, h, rs));
+    for (int ks = 0; ks < nks; ++ks) {
+        const bool more = ks + 1 < nks;
+        const __amdgpu_buffer_rsrc_t wk = more ? wr : wr0;
+        const int kn = more ? (ks + 1) * 4096 : 0;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            bf16x8_t b[TN];
+#pragma unroll
+            for (int nt = 0; nt < TN; ++nt) b[nt] = bn[nt];
+            // next substep's chunk (the last step re-reads its own chunk 0)
+            const int cn = s < 3 ? 8 * ks + 2 * (s + 1) + h : (more ? 8 * (ks + 1) + h : 8 * ks + h);
+#pragma unroll
+            for (int nt = 0; nt < TN; ++nt)
+                bn[nt] = *(const bf16x8_t *)(act + fused_off(e0 + 32 * nt + r, cn, rs));
+#pragma unroll
+            for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < TN; ++nt)
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8_t, wa[mt][s]), b[nt], acc[mt][nt], 0, 0, 0);
+#pragma unroll
+            for (int mt = 0; mt < TM; ++mt)
+                wa[mt][s] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                                            wk, vo[mt] + 1024 * s, kn, 0));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// Hidden layer l of width M = 256 TM: LDS rows of rs bytes in, M * 2 out.
+template <int TM>
+__device__ __forceinline__ void fused_hidden(const FusedMlpArgs &f, int l, uint8_t *act, int rs,
+                                             int wave, int lane)
+{
+    const int K = f.K_pad[l], h = lane >> 5, r = lane & 31;
+    const int fm = wave * TM * 32;
+    f32x16_t acc[TM][2];
+#pragma unroll
+    for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+            const float4 bb = *(const float4 *)(f.bias[l] + fm + mt * 32 + 8 * grp + 4 * h);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                acc[mt][nt][4 * grp + 0] = bb.x;
+                acc[mt][nt][4 * grp + 1] = bb.y;
+                acc[mt][nt][4 * grp + 2] = bb.z;
+                acc[mt][nt][4 * grp + 3] = bb.w;
+            }
+        }
+    fused_mma<TM, 2>(f.w[l], f.w_bytes[l], fm, K, act, rs, 0, lane, acc);
+    __syncthreads();
+    const int rso = 2 * TM * 256;
+#pragma unroll
+    for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            uint32_t p[4][2];
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                p[grp][0] = relu_bf16x2(pack_bf16x2(acc[mt][nt][4 * grp + 0], acc[mt][nt][4 * grp + 1]));
+                p[grp][1] = relu_bf16x2(pack_bf16x2(acc[mt][nt][4 * grp + 2], acc[mt][nt][4 * grp + 3]));
+            }
+            // 16-byte chunk j (features 8j .. 8j+7 of the tile) is group j of
+            // both half waves: lanes of half 0 keep chunks 0 and 2, half 1
+            // chunks 1 and 3, and each sends the other the groups it keeps
+            const uint32_t ra0 = __shfl_xor(h ? p[0][0] : p[1][0], 32);
+            const uint32_t ra1 = __shfl_xor(h ? p[0][1] : p[1][1], 32);
+            const uint32_t rb0 = __shfl_xor(h ? p[2][0] : p[3][0], 32);
+            const uint32_t rb1 = __shfl_xor(h ? p[2][1] : p[3][1], 32);
+            const u32x4_t ca = h ? u32x4_t{ra0, ra1, p[1][0], p[1][1]} : u32x4_t{p[0][0], p[0][1], ra0, ra1};
+            const u32x4_t cb = h ? u32x4_t{rb0, rb1, p[3][0], p[3][1]} : u32x4_t{p[2][0], p[2][1], rb0, rb1};
+            const int e = 32 * nt + r, c = (fm + 32 * mt) / 8 + h;
+            *(u32x4_t *)(act + fused_off(e, c, rso)) = ca;
+            *(u32x4_t *)(act + fused_off(e, c + 2, rso)) = cb;
+        }
+    __syncthreads();
+}
+
+// Last layer (32 MT padded actions) on waves 0 and 1, then sampling.
+template <int MT>
+__device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, int rs, int64_t n0,
+                                           int64_t nv, int wave, int tid)
+{
+    const int l = f.L - 1, K = f.K_pad[l];
+    f32x16_t acc[MT][1];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[mt][0][q] = 0.0f;
+    if (wave < 2) fused_mma<MT, 1>(f.w[l], f.w_bytes[l], 0, K, act, rs, 32 * wave, tid & 63, acc);
+    __syncthreads();
+    sample_epilogue<512, MT, 1>(f.out, (float *)act, n0, nv, wave < 2 ? 32 * wave : (1 << 20), tid, acc);
+}
+
+// Observation [D][ld] fp32 -> bf16 LDS rows: lane = env, wave w takes chunks
+// w, w + 8, ..., CPW at a time with every load of the batch issued before the
+// first is used (each load instruction reads 64 consecutive envs of one
+// feature); features >= D and envs past the batch are zero.
+template <int CPW>
+__device__ __forceinline__ void fused_stage_obs(const FusedMlpArgs &f, uint8_t *act, int rs, int64_t n0,
+                                                int64_t nv, int wave, int lane)
+{
+    const __amdgpu_buffer_rsrc_t orr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, (int)f.obs_bytes, 0x00020000);
+    const int64_t n = n0 + lane;
+    const bool nvalid = lane < nv;
+    const int C = f.K_pad[0] / 8;
+    for (int c0 = wave; c0 < C; c0 += 8 * CPW) {
+        float v[CPW][8];
+#pragma unroll
+        for (int j = 0; j < CPW; ++j)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int k = 8 * (c0 + 8 * j) + i;
+                const bool ok = nvalid && k < f.D;
+                const uint32_t off = ok ? (uint32_t)(((int64_t)k * f.ld_obs + n) * 4) : 0u;
+                const float x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(orr, off, 0, 0));
+                v[j][i] = ok ? x : 0.0f;
+            }
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) {
+            const int c = c0 + 8 * j;
+            if (c < C)
+                *(u32x4_t *)(act + fused_off(lane, c, rs)) =
+                    u32x4_t{pack_bf16x2(v[j][0], v[j][1]), pack_bf16x2(v[j][2], v[j][3]),
+                            pack_bf16x2(v[j][4], v[j][5]), pack_bf16x2(v[j][6], v[j][7])};
+        }
+    }
+}
+
+__global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t act[FUSED_BN * FUSED_ROW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t n0 = (int64_t)blockIdx.x * FUSED_BN;
+    const int64_t nv = f.out.N - n0 < FUSED_BN ? f.out.N - n0 : FUSED_BN;
+
+    // observation [D][ld] fp32 -> bf16 rows of 16-byte chunks (8 features)
+    int rs = ((f.K_pad[0] + 127) & ~127) * 2;
+    if (f.K_pad[0] <= 256) fused_stage_obs<4>(f, act, rs, n0, nv, wave, lane);
+    else fused_stage_obs<8>(f, act, rs, n0, nv, wave, lane);
+    __syncthreads();
+    for (int l = 0; l + 1 < f.L; ++l) {
+        switch (f.M_pad[l] >> 8) {
+            case 1: fused_hidden<1>(f, l, act, rs, wave, lane); break;
+            case 2: fused_hidden<2>(f, l, act, rs, wave, lane); break;
+            case 3: fused_hidden<3>(f, l, act, rs, wave, lane); break;
+            default: fused_hidden<4>(f, l, act, rs, wave, lane); break;
+        }
+        rs = 2 * f.M_pad[l];
+    }
+    switch (f.M_pad[f.L - 1] >> 5) {
+        case 1: fused_last<1>(f, act, rs, n0, nv, wave, tid); break;
+        case 2: fused_last<2>(f, act, rs, n0, nv, wave, tid); break;
+        case 3: fused_last<3>(f, act, rs, n0, nv, wave, tid); break;
+        default: fused_last<4>(f, act, rs, n0, nv, wave, tid); break;
+    }
+}
+
+hipError_t launch_policy_fused(const FusedMlpArgs &f, hipStream_t s)
+{
+    if (f.out.N <= 0) return hipSuccess;
+    if (f.L < 1 || f.L > FUSED_MAX_LAYERS || f.K_pad[0] > FUSED_MAX_WIDTH || (f.K_pad[0] & 63) ||
+        f.M_pad[f.L - 1] > 128 || (f.M_pad[f.L - 1] & 31) || f.out.A > f.M_pad[f.L - 1])
+        return hipErrorInvalidValue;
+    for (int l = 0; l < f.L; ++l) {
+        if (l > 0 && f.K_pad[l] != f.M_pad[l - 1]) return hipErrorInvalidValue;
+        if (l + 1 < f.L && (f.M_pad[l] > FUSED_MAX_WIDTH || (f.M_pad[l] & 255) || f.M_pad[l] <= 0))
+            return hipErrorInvalidValue;
+    }
+    hipLaunchKernelGGL(policy_fused_bf16_kernel, dim3((unsigned)((f.out.N + FUSED_BN - 1) / FUSED_BN)),
+                       dim3(512), 0, s, f);
+    return hipGetLastError();
+}
+
 template <bool IN_OBS, int BN, int WN>
 static hipError_t launch_bf16_sample_t(const GemmArgs &g, int M_pad, hipStream_t s)
 {

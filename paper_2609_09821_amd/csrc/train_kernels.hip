@@ -785,6 +785,7 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackArgs r)
         else if (r.roll_bf16 == 2) ((float *)r.roll)[(int64_t)o * r.roll_K + i] = bf16_to_f32(h);
         else ((float *)r.roll)[(int64_t)o * r.roll_K + i] = w;
     }
+    if (r.rollf) r.rollf[frag_index(o, i, r.roll_K / 64)] = h;
     if (i == 0) {
         if (r.bias_train) r.bias_train[o] = r.b[o];
         if (r.bias_roll) r.bias_roll[o] = r.b[o];
