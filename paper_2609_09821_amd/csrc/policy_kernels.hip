@@ -1104,6 +1104,39 @@ __device__ __forceinline__ uint32_t fused_off(int e, int c, int rs)
     return (uint32_t)(e * rs + ((c ^ (e & 15)) << 4));
 }
 
+// The observation [D][ld] fp32 into the first layer's LDS rows as bf16, by
+// K step (64 features, eight 16-byte chunks: one per wave); lane = env, so
+// that each load instruction reads 64 consecutive envs of one feature.  The
+// feature's row offset is wave-uniform (a scalar offset); features past D go
+// through a descriptor of extent zero and read as zero; envs past the block
+// are zeroed by store().
+struct ObsStream {
+    __amdgpu_buffer_rsrc_t r, r0;
+    int64_t ld;
+    uint32_t nb;     // this lane's env, in bytes
+    int D, wave, lane, rs;
+    bool nvalid;
+    __device__ __forceinline__ void load(int ks, float (&v)[8]) const
+    {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int k = 64 * ks + 8 * wave + i;
+            const bool in = k < D;
+            v[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                 in ? r : r0, nb, in ? (int)((int64_t)k * ld * 4) : 0, 0));
+        }
+    }
+    __device__ __forceinline__ void store(uint8_t *act, int ks, const float (&v)[8]) const
+    {
+        float x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = nvalid ? v[i] : 0.0f;
+        *(u32x4_t *)(act + fused_off(lane, 8 * ks + wave, rs)) =
+            u32x4_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                    pack_bf16x2(x[6], x[7])};
+    }
+};
+
 // acc[TM][TN] += W[rows][K] X[envs][K]^T: rows w_row0 + 32 mt + lane % 32 of
 // the weights (w in fragment order, frag_index), envs e0 + 32 nt + lane % 32
 // of the LDS rows (rs bytes each).  MFMA substep s of K step ks takes
@@ -1118,22 +1151,25 @@ __device__ __forceinline__ uint32_t fused_off(int e, int c, int rs)
 // without a memory access (a branch around them would make the compiler copy
 // the fragments).  The env fragments of the next substep are read from LDS
 // before the MFMAs of the current one.
-template <int TM, int TN>
-__device__ __forceinline__ void fused_mma(const uint16_t *w, uint32_t w_bytes, int w_row0, int K,
-                                          const uint8_t *act, int rs, int e0, int lane,
-                                          f32x16_t (&acc)[TM][TN])
+template <int TM, int TN, bool DRAIN>
+__device__ __forceinline__ void fused_mma(const uint16_t *w, uint32_t w_bytes, int w_row0, int nks,
+                                          int ks0, int ks1, const uint8_t *act, int rs, int e0,
+                                          int lane, f32x16_t (&acc)[TM][TN])
 {
     const int r = lane & 31, h = lane >> 5;
-    const int nks = K / 64;
+    if (ks0 >= ks1) return;
     const __amdgpu_buffer_rsrc_t wr =
         __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, (int)w_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t wr0 = __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, 0, 0x00020000);
-    uint32_t vo[TM];
+    // byte offset of this lane's 16 bytes in a fragment block (a vector
+    // offset) and of tile mt's K step ks (a scalar offset)
+    const uint32_t vo = (uint32_t)(16 * lane);
+    int so[TM];
 #pragma unroll
-    for (int mt = 0; mt < TM; ++mt) vo[mt] = (uint32_t)((w_row0 / 32 + mt) * nks * 4096 + 16 * lane);
-    // the caller's loads (the biases the accumulators start from) complete
-    // here, so that no wait for them lands inside the loop
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    for (int mt = 0; mt < TM; ++mt) so[mt] = (w_row0 / 32 + mt) * nks * 4096;
+    // the caller's loads that the loop uses (the biases the accumulators
+    // start from) complete here, so that no wait for them lands inside it
+    if (DRAIN) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __builtin_amdgcn_sched_barrier(0);
     // in the order of the loop's own loads, which its waits count on
     u32x4_t wa[TM][4];
@@ -1142,16 +1178,17 @@ __device__ __forceinline__ void fused_mma(const uint16_t *w, uint32_t w_bytes, i
 #pragma unroll
         for (int mt = 0; mt < TM; ++mt)
             wa[mt][s] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                        wr, vo[mt] + 1024 * s, 0, 0));
+                                                        wr, vo + 1024 * s, so[mt] + ks0 * 4096, 0));
         __builtin_amdgcn_sched_barrier(0);
     }
     bf16x8_t bn[TN];
 #pragma unroll
-    for (int nt = 0; nt < TN; ++nt) bn[nt] = *(const bf16x8_t *)(act + fused_off(e0 + 32 * nt + r, h, rs));
-    for (int ks = 0; ks < nks; ++ks) {
-        const bool more = ks + 1 < nks;
+    for (int nt = 0; nt < TN; ++nt)
+        bn[nt] = *(const bf16x8_t *)(act + fused_off(e0 + 32 * nt + r, 8 * ks0 + h, rs));
+    for (int ks = ks0; ks < ks1; ++ks) {
+        const bool more = ks + 1 < ks1;
         const __amdgpu_buffer_rsrc_t wk = more ? wr : wr0;
-        const int kn = more ? (ks + 1) * 4096 : 0;
+        const int kn = (ks + 1) * 4096;
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             bf16x8_t b[TN];
@@ -1171,7 +1208,7 @@ __device__ __forceinline__ void fused_mma(const uint16_t *w, uint32_t w_bytes, i
 #pragma unroll
             for (int mt = 0; mt < TM; ++mt)
                 wa[mt][s] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                            wk, vo[mt] + 1024 * s, kn, 0));
+                                                            wk, vo + 1024 * s, so[mt] + kn, 0));
             __builtin_amdgcn_sched_barrier(0);
         }
     }
@@ -1198,7 +1235,7 @@ __device__ __forceinline__ void fused_hidden(const FusedMlpArgs &f, int l, uint8
                 acc[mt][nt][4 * grp + 3] = bb.w;
             }
         }
-    fused_mma<TM, 2>(f.w[l], f.w_bytes[l], fm, K, act, rs, 0, lane, acc);
+    fused_mma<TM, 2, true>(f.w[l], f.w_bytes[l], fm, K / 64, 0, K / 64, act, rs, 0, lane, acc);
     __syncthreads();
     const int rso = 2 * TM * 256;
 #pragma unroll
@@ -1213,13 +1250,16 @@ __device__ __forceinline__ void fused_hidden(const FusedMlpArgs &f, int l, uint8
             }
             // 16-byte chunk j (features 8j .. 8j+7 of the tile) is group j of
             // both half waves: lanes of half 0 keep chunks 0 and 2, half 1
-            // chunks 1 and 3, and each sends the other the groups it keeps
-            const uint32_t ra0 = __shfl_xor(h ? p[0][0] : p[1][0], 32);
-            const uint32_t ra1 = __shfl_xor(h ? p[0][1] : p[1][1], 32);
-            const uint32_t rb0 = __shfl_xor(h ? p[2][0] : p[3][0], 32);
-            const uint32_t rb1 = __shfl_xor(h ? p[2][1] : p[3][1], 32);
-            const u32x4_t ca = h ? u32x4_t{ra0, ra1, p[1][0], p[1][1]} : u32x4_t{p[0][0], p[0][1], ra0, ra1};
-            const u32x4_t cb = h ? u32x4_t{rb0, rb1, p[3][0], p[3][1]} : u32x4_t{p[2][0], p[2][1], rb0, rb1};
+            // chunks 1 and 3.  v_permlane32_swap exchanges the upper half-wave
+            // of its first operand with the lower half of its second, so
+            // after swapping (group 0, group 1) every lane holds its chunk
+            // as (first, second), likewise (group 2, group 3)
+            const auto a0 = __builtin_amdgcn_permlane32_swap(p[0][0], p[1][0], false, false);
+            const auto a1 = __builtin_amdgcn_permlane32_swap(p[0][1], p[1][1], false, false);
+            const auto b0 = __builtin_amdgcn_permlane32_swap(p[2][0], p[3][0], false, false);
+            const auto b1 = __builtin_amdgcn_permlane32_swap(p[2][1], p[3][1], false, false);
+            const u32x4_t ca = u32x4_t{a0[0], a1[0], a0[1], a1[1]};
+            const u32x4_t cb = u32x4_t{b0[0], b1[0], b0[1], b1[1]};
             const int e = 32 * nt + r, c = (fm + 32 * mt) / 8 + h;
             *(u32x4_t *)(act + fused_off(e, c, rso)) = ca;
             *(u32x4_t *)(act + fused_off(e, c + 2, rso)) = cb;
@@ -1227,69 +1267,151 @@ __device__ __forceinline__ void fused_hidden(const FusedMlpArgs &f, int l, uint8
     __syncthreads();
 }
 
-// Last layer (32 MT padded actions) on waves 0 and 1, then sampling.
+// Last layer and sampling.  The 32 MT padded actions of the 64 envs are 2 MT
+// MFMA tiles of 32 x 32, each computed over KS = 4 / MT slices of K (one at
+// MT = 3), so that every wave but two at MT = 3 takes one (tile, env half,
+// K slice).  The partial tiles go to LDS and all 512 threads then take one
+// (env, block of four actions) at a time: the mean is the bias plus the
+// partials in slice order, the noise comes from Philox, action = mean +
+// sigma z, and each env's logp adds its blocks' sums in block order.  log
+// sigma, the biases and the envs' step counters are loaded before the
+// layer's MFMAs and staged in LDS after them.
 template <int MT>
 __device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, int rs, int64_t n0,
                                            int64_t nv, int wave, int tid)
 {
-    const int l = f.L - 1, K = f.K_pad[l];
-    f32x16_t acc[MT][1];
+    constexpr int KS = MT == 3 ? 1 : 4 / MT;
+    constexpr int MP = 32 * MT;
+    const GemmArgs &g = f.out;
+    const int l = f.L - 1, nks = f.K_pad[l] / 64, lane = tid & 63, A = g.A;
+    __shared__ float sig[128], sbias[128], slp0;
+    __shared__ uint32_t senv[FUSED_BN];
+    float p0 = 0.0f, p1 = 0.0f;
+    uint32_t en = 0;
+    if (wave == 0) {
+        if (lane < A) p0 = g.log_std[lane];
+        if (lane + 64 < A) p1 = g.log_std[lane + 64];
+    } else if (wave == 1) {
+        if (lane < A) p0 = g.bias[lane];
+        if (lane + 64 < A) p1 = g.bias[lane + 64];
+    } else if (wave == 2 && lane < nv) {
+        en = g.env_n[n0 + lane];
+    }
+    f32x16_t acc[1][1];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) acc[mt][0][q] = 0.0f;
-    if (wave < 2) fused_mma<MT, 1>(f.w[l], f.w_bytes[l], 0, K, act, rs, 32 * wave, tid & 63, acc);
+    for (int q = 0; q < 16; ++q) acc[0][0][q] = 0.0f;
+    const int nt = wave & 1, mt = (wave >> 1) % MT, ksl = (wave >> 1) / MT;
+    const bool active = wave < 2 * MT * KS;
+    if (active)
+        fused_mma<1, 1, false>(f.w[l], f.w_bytes[l], 32 * mt, nks, ksl * nks / KS, (ksl + 1) * nks / KS,
+                               act, rs, 32 * nt, lane, acc);
     __syncthreads();
-    sample_epilogue<512, MT, 1>(f.out, (float *)act, n0, nv, wave < 2 ? 32 * wave : (1 << 20), tid, acc);
-}
-
-// Observation [D][ld] fp32 -> bf16 LDS rows: lane = env, wave w takes chunks
-// w, w + 8, ..., CPW at a time with every load of the batch issued before the
-// first is used (each load instruction reads 64 consecutive envs of one
-// feature); features >= D and envs past the batch are zero.
-template <int CPW>
-__device__ __forceinline__ void fused_stage_obs(const FusedMlpArgs &f, uint8_t *act, int rs, int64_t n0,
-                                                int64_t nv, int wave, int lane)
-{
-    const __amdgpu_buffer_rsrc_t orr =
-        __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, (int)f.obs_bytes, 0x00020000);
-    const int64_t n = n0 + lane;
-    const bool nvalid = lane < nv;
-    const int C = f.K_pad[0] / 8;
-    for (int c0 = wave; c0 < C; c0 += 8 * CPW) {
-        float v[CPW][8];
+    // the layer input is read: partial tiles [KS][64 envs][MP] fp32 (16-byte
+    // units XOR-swizzled by env % 8), mean and action rows [64][A], and the
+    // per-block sums of z^2 / 2 [64][33] take its place
+    float *part = (float *)act;
+    float *smean = part + KS * FUSED_BN * MP;
+    float *sact = smean + FUSED_BN * A;
+    float *slp = sact + FUSED_BN * A;
+    if (active) {
+        const int e = 32 * nt + (lane & 31), h = lane >> 5;
 #pragma unroll
-        for (int j = 0; j < CPW; ++j)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int k = 8 * (c0 + 8 * j) + i;
-                const bool ok = nvalid && k < f.D;
-                const uint32_t off = ok ? (uint32_t)(((int64_t)k * f.ld_obs + n) * 4) : 0u;
-                const float x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(orr, off, 0, 0));
-                v[j][i] = ok ? x : 0.0f;
-            }
-#pragma unroll
-        for (int j = 0; j < CPW; ++j) {
-            const int c = c0 + 8 * j;
-            if (c < C)
-                *(u32x4_t *)(act + fused_off(lane, c, rs)) =
-                    u32x4_t{pack_bf16x2(v[j][0], v[j][1]), pack_bf16x2(v[j][2], v[j][3]),
-                            pack_bf16x2(v[j][4], v[j][5]), pack_bf16x2(v[j][6], v[j][7])};
+        for (int grp = 0; grp < 4; ++grp) {
+            const int unit = (8 * mt + 2 * grp + h) ^ (e & 7);
+            *(f32x4_t *)(part + (ksl * FUSED_BN + e) * MP + 4 * unit) =
+                f32x4_t{acc[0][0][4 * grp], acc[0][0][4 * grp + 1], acc[0][0][4 * grp + 2],
+                        acc[0][0][4 * grp + 3]};
         }
     }
+    if (wave == 0) {
+        if (lane < A) sig[lane] = expf(p0);
+        if (lane + 64 < A) sig[lane + 64] = expf(p1);
+        float c = (lane < A ? p0 + HALF_LOG_2PI : 0.0f) + (lane + 64 < A ? p1 + HALF_LOG_2PI : 0.0f);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+        if (lane == 0) slp0 = c;
+    } else if (wave == 1) {
+        if (lane < A) sbias[lane] = p0;
+        if (lane + 64 < A) sbias[lane + 64] = p1;
+    } else if (wave == 2) {
+        senv[lane] = en;
+    }
+    __syncthreads();
+    const int G = (A + 3) / 4;
+    for (int it = tid; it < FUSED_BN * G; it += 512) {
+        const int e = it & (FUSED_BN - 1), j = it / FUSED_BN;
+        if (e >= nv) continue;
+        float mu[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mu[q] = 4 * j + q < A ? sbias[4 * j + q] : 0.0f;
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+            const f32x4_t v = *(const f32x4_t *)(part + (k * FUSED_BN + e) * MP + 4 * (j ^ (e & 7)));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) mu[q] += v[q];
+        }
+        float z[4];
+        normals4(g.seed, (uint32_t)(n0 + e), senv[e], (uint32_t)j, 0u, z);
+        float lp = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int m = 4 * j + q;
+            if (m < A) {
+                smean[e * A + m] = mu[q];
+                sact[e * A + m] = mu[q] + sig[m] * z[q];
+                lp += 0.5f * z[q] * z[q];
+            }
+        }
+        slp[e * 33 + j] = lp;
+    }
+    __syncthreads();
+    if (tid < nv && g.logp) {
+        float sum = 0.0f;
+        for (int j = 0; j < G; ++j) sum += slp[tid * 33 + j];
+        g.logp[n0 + tid] = -(sum + slp0);
+    }
+    copy_rows_out<512>(g.mean + n0 * A, smean, nv * A, tid);
+    copy_rows_out<512>(g.action + n0 * A, sact, nv * A, tid);
+}
+
+// The whole observation of the block staged before the first layer: every
+// load (up to S K steps, one chunk each per wave) is issued before the first
+// is written, one memory latency in all.
+template <int S>
+__device__ __forceinline__ void fused_stage_obs(const ObsStream &os, uint8_t *act, int nks)
+{
+    float v[S][8];
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+        if (j < nks) os.load(j, v[j]);
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+        if (j < nks) os.store(act, j, v[j]);
 }
 
 __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
 {
     __shared__ __attribute__((aligned(16))) uint8_t act[FUSED_BN * FUSED_ROW];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = (int)uniform((uint32_t)tid >> 6);
     const int64_t n0 = (int64_t)blockIdx.x * FUSED_BN;
     const int64_t nv = f.out.N - n0 < FUSED_BN ? f.out.N - n0 : FUSED_BN;
 
     // observation [D][ld] fp32 -> bf16 rows of 16-byte chunks (8 features)
     int rs = ((f.K_pad[0] + 127) & ~127) * 2;
-    if (f.K_pad[0] <= 256) fused_stage_obs<4>(f, act, rs, n0, nv, wave, lane);
-    else fused_stage_obs<8>(f, act, rs, n0, nv, wave, lane);
+    ObsStream os;
+    os.r = __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, (int)f.obs_bytes, 0x00020000);
+    os.r0 = __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, 0, 0x00020000);
+    os.ld = f.ld_obs;
+    os.nb = (uint32_t)((n0 + lane) * 4);
+    os.D = f.D;
+    os.wave = wave;
+    os.lane = lane;
+    os.rs = rs;
+    os.nvalid = lane < nv;
+    const int nks0 = f.K_pad[0] / 64;
+    if (nks0 <= 4) fused_stage_obs<4>(os, act, nks0);
+    else if (nks0 <= 8) fused_stage_obs<8>(os, act, nks0);
+    else fused_stage_obs<16>(os, act, nks0);
     __syncthreads();
     for (int l = 0; l + 1 < f.L; ++l) {
         switch (f.M_pad[l] >> 8) {
