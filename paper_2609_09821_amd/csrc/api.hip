@@ -40,7 +40,7 @@ struct im_ctx {
     std::vector<int> dims, M_pad, K_pad;
     std::vector<void *> d_w;
     std::vector<float *> d_b;
-    // bf16 policies that the one-launch small-batch kernel holds: each layer's
+    // bf16 policies that the one-launch policy kernel holds: each layer's
     // weights again, in MFMA fragment order (empty otherwise)
     std::vector<uint16_t *> d_wf;
     float *d_log_std = nullptr;
@@ -81,7 +81,7 @@ im_status hip_fail(hipError_t e, const char *what)
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-// A bf16 policy whose widths the one-launch small-batch kernel holds.
+// A bf16 policy whose widths the one-launch policy kernel holds.
 bool fused_policy_fits(const im_ctx *c)
 {
     if (c->L > FUSED_MAX_LAYERS || c->K_pad[0] > FUSED_MAX_WIDTH || c->M_pad[c->L - 1] > 128)
@@ -704,8 +704,9 @@ im_status im_create(const im_config *cfg, const im_skeleton *sk, const im_clip *
             IM_TRY_ALLOC(c->d_ws[1], wsb);
             c->ws_bytes[1] = wsb;
         }
-        // large bf16 batches stage the observation as bf16 rows for the first layer
-        if (pol->dtype == IM_DTYPE_BF16 && max_envs > SMALL_BATCH)
+        // large bf16 batches of the per-layer kernels stage the observation as
+        // bf16 rows for the first layer (the one-launch kernel stages it in LDS)
+        if (pol->dtype == IM_DTYPE_BF16 && max_envs > SMALL_BATCH && c->d_wf.empty())
             IM_TRY_ALLOC(c->d_obs16, (size_t)max_envs * (size_t)c->K_pad[0] * 2);
     }
     {
@@ -837,7 +838,7 @@ im_status policy_layers(im_ctx *c, const float *obs, int64_t ld_obs, const uint3
 {
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
     const uint64_t esz = bf16 ? 2 : 4;
-    if (bf16 && n_envs <= SMALL_BATCH && !c->d_wf.empty()) {
+    if (bf16 && !c->d_wf.empty()) {
         FusedMlpArgs f{};
         f.obs = obs;
         f.ld_obs = ld_obs;

@@ -43,9 +43,9 @@ struct GemmArgs {
                          // earlier layer of the same call), the staging pass is skipped
 };
 
-// The whole bf16 policy in one launch for small batches (policy_kernels.hip):
-// hidden widths M_pad[l] multiples of 256 up to FUSED_MAX_WIDTH, observation
-// width K_pad[0] up to FUSED_MAX_WIDTH, at most 128 padded actions.
+// The whole bf16 policy in one launch (policy_kernels.hip): hidden widths
+// M_pad[l] multiples of 256 up to FUSED_MAX_WIDTH, observation width K_pad[0]
+// up to FUSED_MAX_WIDTH, at most 128 padded actions.
 constexpr int FUSED_MAX_LAYERS = 8;
 constexpr int FUSED_MAX_WIDTH = 1024;
 

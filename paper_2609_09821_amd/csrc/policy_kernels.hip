@@ -1077,23 +1077,25 @@ __global__ __launch_bounds__(256) void stage_obs_bf16_kernel(const float *__rest
 }
 
 // ---------------------------------------------------------------------------
-// The whole bf16 policy in one kernel for small batches.  One workgroup of 8
-// waves per 64 envs runs every layer; between layers the activations stay in
-// LDS as [64 envs][K] bf16 rows whose 16-byte chunks (8 features) are
-// XOR-swizzled by env % 16, so that the fragment reads and the output writes
-// of 16 consecutive envs hit distinct banks.  At 16384 envs that is one
-// workgroup per CU, and no activation goes through memory.
+// The whole bf16 policy in one kernel.  One workgroup of 8 waves per 64 envs
+// runs every layer; between layers the activations stay in LDS as [64 envs][K]
+// bf16 rows whose 16-byte chunks (8 features) are XOR-swizzled by env % 16,
+// so that the fragment reads and the output writes of 16 consecutive envs
+// hit distinct banks.  No activation goes through memory; the LDS (about
+// 136 KB) holds one workgroup per CU, and a batch larger than 64 envs per CU
+// runs in successive rounds of workgroups.
 //
 // Hidden layer of width M: wave w owns output features [w M/8, (w+1) M/8),
 // M/256 MFMA tiles of 32 rows, for all 64 envs (2 tiles of 32).  Its weight
 // fragments (A operand) come from global memory straight into registers,
-// loaded one K step (64) ahead: every workgroup reads the same weights, which
-// stay in the L2.  The env fragments (B operand) are read from LDS.  The
-// accumulators start at the bias; once every wave has read the layer's input
-// (workgroup barrier) they are written over it: ReLU, bf16, and the two half
-// waves trade four-feature groups so that each lane stores whole 16-byte
-// chunks.  The last layer runs on waves 0 and 1 (32 envs each, every action),
-// then all waves take part in the sampling epilogue.
+// loaded one K step (64) ahead: every workgroup reads the same weights (a
+// copy in MFMA fragment order), which stay in the L2, so each weight byte
+// from the L2 serves 64 envs (128 flop).  The env fragments (B operand) are
+// read from LDS.  The accumulators start at the bias; once every wave has
+// read the layer's input (workgroup barrier) they are written over it: ReLU,
+// bf16, and the two half waves trade four-feature groups so that each lane
+// stores whole 16-byte chunks.  The last layer and the sampling use every
+// wave (fused_last).
 // ---------------------------------------------------------------------------
 constexpr int FUSED_BN = 64;                      // envs per workgroup
 constexpr int FUSED_ROW = FUSED_MAX_WIDTH * 2;    // LDS bytes per env

@@ -1,5 +1,6 @@
 """The persistent bf16 GEMM of large batches at the edges of its schedule,
-against the oracle on every env.
+against the oracle on every env, through the critic's hidden layers (the
+policy of the same shape runs in the one-launch policy kernel, checked too).
 
 A six-body chain has a 91-wide observation, whose first layer then runs two K
 steps per tile (the shortest pipeline: the next tile's loads and biases are
@@ -26,6 +27,7 @@ def _chain_world(dims):
                      [clip_from_arrays(np.zeros((2, 3)), np.tile([1, 0, 0, 0], (2, 1)),
                                        np.tile([1, 0, 0, 0], (2, B - 1, 1)))])
     d["policy"] = synth.make_policy(np.random.default_rng(3), dims, True)
+    d["critic"] = synth.make_policy(np.random.default_rng(4), dims[:-1] + [1], True)
     return d
 
 
@@ -37,7 +39,7 @@ def test_persistent_gemm_schedule_edges(hidden, N):
     d = _chain_world(dims)
     d["n_envs"] = N
     print("gemm shapes %s at %d envs" % (dims, N), flush=True)
-    ctx = binding.Context(d, max_envs=N, critic=False)
+    ctx = binding.Context(d, max_envs=N)
     assert ctx.info.obs_dim == D
     rng = np.random.default_rng(N)
     obs = rng.normal(size=(D, N)).astype(np.float32)
@@ -47,9 +49,18 @@ def test_persistent_gemm_schedule_edges(hidden, N):
     logp = torch.empty(N, device="cuda")
     ctx.policy_act(torch.from_numpy(obs).cuda(), torch.from_numpy(n.view(np.int32)).cuda(), N,
                    mean, act, logp)
+    v = torch.empty(N, device="cuda")
+    ctx.value(torch.from_numpy(obs).cuda(), N, v)
     torch.cuda.synchronize()
     gm, ga, gl = mean.cpu().numpy(), act.cpu().numpy(), logp.cpu().numpy()
+    gv = v.cpu().numpy()
     ctx.close()
+
+    ov = oracle.value(d["critic"], obs)
+    sv = np.sqrt(np.mean(ov.astype(np.float64) ** 2))
+    verr = np.abs(gv - ov) / np.maximum(np.abs(ov), sv)
+    assert verr.max() <= 2e-2, "value: worst %.3e at env %d" % (verr.max(), int(np.argmax(verr)))
+    print("value (all %d envs): max rel err %.2e" % (N, verr.max()))
 
     pol = d["policy"]
     om, oa, olp = oracle.policy(pol, d["config"]["seed"], obs, n)
