@@ -55,11 +55,9 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 CSRC = os.path.join(ROOT, "paper_2609_09821_amd", "csrc")
 SHARED_SOURCES = []
 TRAFFIC_KIB = {
-    # policy: one entry per launch of im_policy_act, in order (observation
-    # staging, the four layers)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h"], "sha": "e2db6d6939c049eb", "workloads": {
-        4: {"fetch": [46224.5, 36279.3, 98713.8, 73901.1, 33455.5],
-            "write": [49152.0, 132820.0, 131625.8, 65841.9, 35584.0]}}},
+    # policy: one entry per launch of im_policy_act (a bf16 policy is one launch)
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h", "launch.h"], "sha": "20ca46e30de90da0", "workloads": {
+        4: {"fetch": [109658.0], "write": [35584.0]}}},
     "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "227c1405eaae8b00", "workloads": {
         4: {"fetch": [61792.6], "write": [169487.7]}}},
 }
@@ -640,7 +638,9 @@ def main():
             "note": "same timed steps captured as one HIP graph and replayed; results "
                     "checked equal to the eager run"},
         "roofline": {
-            "kernel": "policy MLP (im_policy_act: one MFMA GEMM per layer)",
+            "kernel": ("policy MLP (im_policy_act: policy_fused_bf16_kernel, every layer and "
+                       "the sampling in one launch)" if r["prec"] == "bf16" else
+                       "policy MLP (im_policy_act: one MFMA GEMM per layer)"),
             "bound": "mfma", "achieved": mlp_tflops, "peak": peak, "unit": "TFLOP/s",
             "frac": mlp_tflops / peak, "traffic": tr_pol and tr_pol[0],
             "traffic_unit": "HBM bytes per launch",

@@ -56,6 +56,8 @@ struct im_ctx {
         std::vector<int> dims, M_pad, K_pad;
         std::vector<void *> d_w;
         std::vector<float *> d_b;
+        std::vector<uint16_t *> d_wf;   // bf16 critics the one-launch kernel holds: the hidden
+                                        // layers' weights in MFMA fragment order (else empty)
         float *d_head = nullptr;   // [K_head + 1]: last-layer weights (zero-padded), then its bias
         int K_head = 0;            // D for a one-layer critic, else M_pad[L-2]
         int64_t bytes = 0;         // device memory of the above
@@ -105,9 +107,11 @@ void free_critic(im_ctx *c)
     auto &k = c->critic;
     for (void *p : k.d_w) hipFree(p);
     for (float *p : k.d_b) hipFree(p);
+    for (uint16_t *p : k.d_wf) hipFree(p);
     hipFree(k.d_head);
     k.d_w.clear();
     k.d_b.clear();
+    k.d_wf.clear();
     k.d_head = nullptr;
     k.L = 0;
     c->device_bytes -= k.bytes;
@@ -1035,6 +1039,22 @@ im_status im_set_critic(im_ctx *c, const im_policy *k)
             hipSuccess)
             return upload_fail(e, "upload critic biases");
     }
+    // hidden layers of a bf16 critic that the one-launch kernel holds, again in
+    // MFMA fragment order
+    bool fits = bf16 && L >= 2 && L - 1 <= FUSED_MAX_LAYERS && cr.K_pad[0] <= FUSED_MAX_WIDTH;
+    for (int l = 0; l < L - 1; ++l) fits = fits && cr.M_pad[l] <= FUSED_MAX_WIDTH;
+    for (int l = 0; fits && l < L - 1; ++l) {
+        const int M = cr.dims[l + 1], K = cr.dims[l], nks = cr.K_pad[l] / 64;
+        std::vector<uint16_t> fbuf((size_t)cr.M_pad[l] * cr.K_pad[l], 0);
+        const uint16_t *src = (const uint16_t *)k->weight[l];
+        for (int m = 0; m < M; ++m)
+            for (int i = 0; i < K; ++i) fbuf[im::frag_index(m, i, nks)] = src[(size_t)m * K + i];
+        uint16_t *dwf = nullptr;
+        if (!alloc(&dwf, fbuf.size() * 2)) return oom("critic weights (fragment order)");
+        cr.d_wf.push_back(dwf);
+        if ((e = hipMemcpy(dwf, fbuf.data(), fbuf.size() * 2, hipMemcpyHostToDevice)) != hipSuccess)
+            return upload_fail(e, "upload critic weights (fragment order)");
+    }
     // last layer as an fp32 vector (bf16 weights convert exactly)
     cr.K_head = L == 1 ? c->D : cr.M_pad[L - 2];
     std::vector<float> head(cr.K_head + 1, 0.0f);
@@ -1061,7 +1081,7 @@ im_status im_set_critic(im_ctx *c, const im_policy *k)
             free_critic(c);
             return s;
         }
-        if (bf16 && c->max_envs > SMALL_BATCH && !c->d_obs16 &&
+        if (bf16 && c->max_envs > SMALL_BATCH && !c->d_obs16 && cr.d_wf.empty() &&
             dev_alloc(c, &c->d_obs16, (size_t)c->max_envs * (size_t)round_up(c->D, 64) * 2) !=
                 hipSuccess)
             return oom("observation staging");
@@ -1106,6 +1126,26 @@ im_status value_layers(im_ctx *c, const float *obs, int64_t ld_obs, int64_t n_en
     const auto &cr = c->critic;
     const bool bf16 = c->dtype == IM_DTYPE_BF16;
     hipError_t e;
+    if (!cr.d_wf.empty()) {
+        FusedMlpArgs f{};
+        f.obs = obs;
+        f.ld_obs = ld_obs;
+        f.obs_bytes = (uint32_t)((uint64_t)c->D * (uint64_t)ld_obs * 4);
+        f.D = c->D;
+        f.L = cr.L - 1;
+        for (int l = 0; l < f.L; ++l) {
+            f.w[l] = cr.d_wf[l];
+            f.bias[l] = cr.d_b[l];
+            f.w_bytes[l] = (uint32_t)((uint64_t)cr.M_pad[l] * (uint64_t)cr.K_pad[l] * 2);
+            f.M_pad[l] = cr.M_pad[l];
+            f.K_pad[l] = cr.K_pad[l];
+        }
+        f.out.N = n_envs;
+        f.head = cr.d_head;
+        f.value = value;
+        e = launch_value_fused(f, st);
+        return e == hipSuccess ? IM_OK : hip_fail(e, "fused value launch");
+    }
     if (cr.L == 1) {
         e = launch_value_head_obs(obs, ld_obs, c->D, cr.d_head, cr.d_head + cr.K_head, bf16, n_envs,
                                   value, st);
@@ -1724,6 +1764,7 @@ im_status im_ppo_setup(im_ctx *c, int64_t max_minibatch)
     for (size_t l = 0; l < t->critic.size(); ++l) {
         t->critic[l].roll = cr.d_w[l];
         t->critic[l].roll_K = cr.K_pad[l];
+        t->critic[l].rollf = cr.d_wf.empty() ? nullptr : cr.d_wf[l];
         t->critic[l].roll_bias = cr.d_b[l];
     }
     // float32 masters from the current weights (bf16 values convert exactly)

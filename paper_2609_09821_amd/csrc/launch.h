@@ -72,9 +72,14 @@ struct FusedMlpArgs {
     uint32_t w_bytes[FUSED_MAX_LAYERS];
     int M_pad[FUSED_MAX_LAYERS], K_pad[FUSED_MAX_LAYERS];
     GemmArgs out;        // sampling epilogue: N, bias (last layer), mean, action, logp,
-                         // env_n, log_std, A, seed
+                         // env_n, log_std, A, seed (a critic: N only)
+    // a critic (launch_value_fused): the L layers are all hidden, then the value
+    // v = head[0..M_pad[L-1]) . h + head[M_pad[L-1]] (fp32, zero past the width)
+    const float *head;
+    float *value;        // [N]
 };
 hipError_t launch_policy_fused(const FusedMlpArgs &f, hipStream_t s);
+hipError_t launch_value_fused(const FusedMlpArgs &f, hipStream_t s);
 
 // Rollout end (rollout_kernels.hip).
 struct GaeArgs {

@@ -1376,6 +1376,36 @@ __device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, 
     copy_rows_out<512>(g.action + n0 * A, sact, nv * A, tid);
 }
 
+// The critic's output: v = head . h + bias over the last hidden layer's
+// activations h (bf16 in LDS, rows of rs bytes) with the fp32 head.  Wave w
+// sums chunks [w C/8, (w+1) C/8) of every env (lane), the eight partial sums
+// are added in wave order.
+__device__ __forceinline__ void fused_value_head(const FusedMlpArgs &f, const uint8_t *act, int rs,
+                                                 int64_t n0, int64_t nv, int wave, int tid)
+{
+    __shared__ float spart[8][FUSED_BN];
+    const int K = f.M_pad[f.L - 1], per = K / 64, e = tid & (FUSED_BN - 1);
+    float acc = 0.0f;
+    for (int j = 0; j < per; ++j) {
+        const int c = wave * per + j;
+        const u32x4_t v = *(const u32x4_t *)(act + fused_off(e, c, rs));
+        const float *w = f.head + 8 * c;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc += w[2 * q] * __uint_as_float(v[q] << 16);
+            acc += w[2 * q + 1] * __uint_as_float(v[q] & 0xFFFF0000u);
+        }
+    }
+    spart[wave][e] = acc;
+    __syncthreads();
+    if (tid < nv) {
+        float sum = f.head[K];
+#pragma unroll
+        for (int p = 0; p < 8; ++p) sum += spart[p][tid];
+        f.value[n0 + tid] = sum;
+    }
+}
+
 // The whole observation of the block staged before the first layer: every
 // load (up to S K steps, one chunk each per wave) is issued before the first
 // is written, one memory latency in all.
@@ -1391,6 +1421,8 @@ __device__ __forceinline__ void fused_stage_obs(const ObsStream &os, uint8_t *ac
         if (j < nks) os.store(act, j, v[j]);
 }
 
+// VALUE: a critic (every layer hidden, then the value head).
+template <bool VALUE>
 __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
 {
     __shared__ __attribute__((aligned(16))) uint8_t act[FUSED_BN * FUSED_ROW];
@@ -1415,7 +1447,7 @@ __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
     else if (nks0 <= 8) fused_stage_obs<8>(os, act, nks0);
     else fused_stage_obs<16>(os, act, nks0);
     __syncthreads();
-    for (int l = 0; l + 1 < f.L; ++l) {
+    for (int l = 0; l + (VALUE ? 0 : 1) < f.L; ++l) {
         switch (f.M_pad[l] >> 8) {
             case 1: fused_hidden<1>(f, l, act, rs, wave, lane); break;
             case 2: fused_hidden<2>(f, l, act, rs, wave, lane); break;
@@ -1423,6 +1455,10 @@ __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
             default: fused_hidden<4>(f, l, act, rs, wave, lane); break;
         }
         rs = 2 * f.M_pad[l];
+    }
+    if constexpr (VALUE) {
+        fused_value_head(f, act, rs, n0, nv, wave, tid);
+        return;
     }
     switch (f.M_pad[f.L - 1] >> 5) {
         case 1: fused_last<1>(f, act, rs, n0, nv, wave, tid); break;
@@ -1432,19 +1468,37 @@ __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
     }
 }
 
+// Shapes the kernel assumes; n_hidden: the layers that are hidden.
+static bool fused_shapes_ok(const FusedMlpArgs &f, int n_hidden)
+{
+    if (f.L < 1 || f.L > FUSED_MAX_LAYERS || f.K_pad[0] > FUSED_MAX_WIDTH || (f.K_pad[0] & 63) ||
+        f.K_pad[0] <= 0)
+        return false;
+    for (int l = 0; l < f.L; ++l) {
+        if (l > 0 && f.K_pad[l] != f.M_pad[l - 1]) return false;
+        if (l < n_hidden && (f.M_pad[l] > FUSED_MAX_WIDTH || (f.M_pad[l] & 255) || f.M_pad[l] <= 0))
+            return false;
+    }
+    return true;
+}
+
 hipError_t launch_policy_fused(const FusedMlpArgs &f, hipStream_t s)
 {
     if (f.out.N <= 0) return hipSuccess;
-    if (f.L < 1 || f.L > FUSED_MAX_LAYERS || f.K_pad[0] > FUSED_MAX_WIDTH || (f.K_pad[0] & 63) ||
-        f.M_pad[f.L - 1] > 128 || (f.M_pad[f.L - 1] & 31) || f.out.A > f.M_pad[f.L - 1])
+    if (!fused_shapes_ok(f, f.L - 1) || f.M_pad[f.L - 1] > 128 || (f.M_pad[f.L - 1] & 31) ||
+        f.M_pad[f.L - 1] <= 0 || f.out.A > f.M_pad[f.L - 1])
         return hipErrorInvalidValue;
-    for (int l = 0; l < f.L; ++l) {
-        if (l > 0 && f.K_pad[l] != f.M_pad[l - 1]) return hipErrorInvalidValue;
-        if (l + 1 < f.L && (f.M_pad[l] > FUSED_MAX_WIDTH || (f.M_pad[l] & 255) || f.M_pad[l] <= 0))
-            return hipErrorInvalidValue;
-    }
-    hipLaunchKernelGGL(policy_fused_bf16_kernel, dim3((unsigned)((f.out.N + FUSED_BN - 1) / FUSED_BN)),
-                       dim3(512), 0, s, f);
+    hipLaunchKernelGGL(policy_fused_bf16_kernel<false>,
+                       dim3((unsigned)((f.out.N + FUSED_BN - 1) / FUSED_BN)), dim3(512), 0, s, f);
+    return hipGetLastError();
+}
+
+hipError_t launch_value_fused(const FusedMlpArgs &f, hipStream_t s)
+{
+    if (f.out.N <= 0) return hipSuccess;
+    if (!fused_shapes_ok(f, f.L) || !f.head || !f.value) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(policy_fused_bf16_kernel<true>,
+                       dim3((unsigned)((f.out.N + FUSED_BN - 1) / FUSED_BN)), dim3(512), 0, s, f);
     return hipGetLastError();
 }
 

@@ -1,13 +1,14 @@
 """The persistent bf16 GEMM of large batches at the edges of its schedule,
-against the oracle on every env, through the critic's hidden layers (the
-policy of the same shape runs in the one-launch policy kernel, checked too).
+against the oracle on every env, through the hidden layers of a critic whose
+1280-wide first layer the one-launch kernel does not hold (the policy with
+the other two widths runs in the one-launch kernel, checked too).
 
 A six-body chain has a 91-wide observation, whose first layer then runs two K
 steps per tile (the shortest pipeline: the next tile's loads and biases are
 staged while the current tile is one step from done).  The hidden widths give
-one, two and three feature blocks per env block; the env counts leave ragged
-last tiles and, at 16684 envs, fewer tiles than compute units (one tile per
-workgroup).  Tolerances as in the full-size parity test.
+one, two, three and five feature blocks per env block; the env counts leave
+ragged last tiles and, at 16684 envs, fewer tiles than compute units (one
+tile per workgroup).  Tolerances as in the full-size parity test.
 """
 import numpy as np
 import pytest
@@ -27,7 +28,7 @@ def _chain_world(dims):
                      [clip_from_arrays(np.zeros((2, 3)), np.tile([1, 0, 0, 0], (2, 1)),
                                        np.tile([1, 0, 0, 0], (2, B - 1, 1)))])
     d["policy"] = synth.make_policy(np.random.default_rng(3), dims, True)
-    d["critic"] = synth.make_policy(np.random.default_rng(4), dims[:-1] + [1], True)
+    d["critic"] = synth.make_policy(np.random.default_rng(4), [dims[0], 1280] + dims[1:-1] + [1], True)
     return d
 
 

@@ -1,4 +1,4 @@
-"""The one-launch bf16 policy of small batches (every layer in one kernel, the
+"""The one-launch bf16 policy and critic (every layer in one kernel, the
 activations held in LDS between layers, weights read in MFMA fragment order)
 against the oracle on every env.
 
@@ -8,7 +8,9 @@ padded actions, one layer (no hidden layer) up to eight, an observation 961
 wide (1024 padded: the widest LDS row), a single env, ragged last blocks of
 64 envs and a full grid of 16384 envs.  Policies it does not hold (a
 1280-wide hidden layer, nine layers) take the per-layer kernels, checked the
-same way.  Tolerances as in the full-size parity test.
+same way.  The critic variant (hidden layers, then the fp32 value head)
+runs over the same widths and depths.  Tolerances as in the full-size parity
+test.
 """
 import numpy as np
 import pytest
@@ -25,13 +27,16 @@ CHAIN6 = list(range(-1, 5))                  # observation 91 wide
 COMB64 = [-1] + [0 if j == 0 else 9 * b + j for b in range(7) for j in range(9)]
 
 
-def _world(parent, hidden, A, seed):
+def _world(parent, hidden, A, seed, critic_hidden=None):
     B = len(parent)
     d = custom_world(parent, [0] + [1] * (B - 1), [[0, 0, 0]] + [[0.1, 0, 0]] * (B - 1), [1.0] * B,
                      [clip_from_arrays(np.zeros((2, 3)), np.tile([1, 0, 0, 0], (2, 1)),
                                        np.tile([1, 0, 0, 0], (2, B - 1, 1)))])
     D = 15 * B + 1
     d["policy"] = synth.make_policy(np.random.default_rng(seed), [D] + list(hidden) + [A], True)
+    if critic_hidden is not None:
+        d["critic"] = synth.make_policy(np.random.default_rng(seed + 1), [D] + list(critic_hidden) + [1],
+                                        True)
     return d
 
 
@@ -81,3 +86,36 @@ def test_fused_policy_shapes(parent, hidden, A, N):
                          ids=["hidden-1280", "nine-layers"])
 def test_policies_outside_the_fused_kernel(hidden, N):
     check_policy(_world(CHAIN6, hidden, 8, 6), N)
+
+
+def check_value(d, N):
+    """value on N envs of random observations against the oracle."""
+    crit = d["critic"]
+    D = crit["dims"][0]
+    d["n_envs"] = N
+    print("critic %s at %d envs" % (crit["dims"], N), flush=True)
+    ctx = binding.Context(d, max_envs=N)
+    obs = np.random.default_rng(N + 7).normal(size=(D, N)).astype(np.float32)
+    v = torch.empty(N, device="cuda")
+    ctx.value(torch.from_numpy(obs).cuda(), N, v)
+    torch.cuda.synchronize()
+    gv = v.cpu().numpy()
+    ctx.close()
+    ov = oracle.value(crit, obs)
+    s = np.sqrt(np.mean(ov.astype(np.float64) ** 2))
+    err = np.abs(gv - ov) / np.maximum(np.abs(ov), s)
+    assert err.max() <= 2e-2, "value: worst %.3e at env %d" % (err.max(), int(np.argmax(err)))
+    print("value (all %d envs): max rel err %.2e" % (N, err.max()))
+    assert np.all(np.isfinite(gv))
+
+
+@pytest.mark.parametrize("parent,hidden,N", [
+    (CHAIN6, [256, 768], 1300),
+    (CHAIN6, [1024, 512], 16384),
+    (CHAIN6, [512], 1),
+    (CHAIN6, [256] * 8, 130),             # eight hidden layers
+    (COMB64, [1024, 256], 333),           # 1024-wide padded observation
+    (CHAIN6, [1280], 700),                # too wide: per-layer kernels
+], ids=["256-768", "1024-512-full-grid", "one-env", "eight-hidden", "obs-961", "hidden-1280"])
+def test_fused_critic_shapes(parent, hidden, N):
+    check_value(_world(parent, [256], 8, 9, critic_hidden=hidden), N)
