@@ -56,8 +56,8 @@ CSRC = os.path.join(ROOT, "paper_2609_09821_amd", "csrc")
 SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act (a bf16 policy is one launch)
-    "policy": {"sources": ["policy_kernels.hip", "device_math.h", "launch.h"], "sha": "e3c23d6fc3d5f131", "workloads": {
-        4: {"fetch": [109672.5], "write": [35584.0]}}},
+    "policy": {"sources": ["policy_kernels.hip", "device_math.h", "launch.h"], "sha": "8d96ff129a595a70", "workloads": {
+        4: {"fetch": [109671.5], "write": [35584.0]}}},
     "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "227c1405eaae8b00", "workloads": {
         4: {"fetch": [61792.6], "write": [169487.7]}}},
 }

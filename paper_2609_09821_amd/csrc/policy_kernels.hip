@@ -1110,12 +1110,13 @@ __device__ __forceinline__ uint32_t fused_off(int e, int c, int rs)
 // K step (64 features, eight 16-byte chunks: one per wave); lane = env, so
 // that each load instruction reads 64 consecutive envs of one feature.  The
 // feature's row offset is wave-uniform (a scalar offset); features past D go
-// through a descriptor of extent zero and read as zero; envs past the block
-// are zeroed by store().
+// through a descriptor of extent zero and read as zero; lanes past the last
+// env read env 0 (every address stays inside the buffer, whether or not the
+// descriptor's range check counts the scalar offset) and are zeroed by store().
 struct ObsStream {
     __amdgpu_buffer_rsrc_t r, r0;
     int64_t ld;
-    uint32_t nb;     // this lane's env, in bytes
+    uint32_t nb;     // this lane's env, in bytes (0 past the last env)
     int D, wave, lane, rs;
     bool nvalid;
     __device__ __forceinline__ void load(int ks, float (&v)[8]) const
@@ -1436,7 +1437,7 @@ __global__ __launch_bounds__(512) void policy_fused_bf16_kernel(FusedMlpArgs f)
     os.r = __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, (int)f.obs_bytes, 0x00020000);
     os.r0 = __builtin_amdgcn_make_buffer_rsrc((void *)f.obs, (short)0, 0, 0x00020000);
     os.ld = f.ld_obs;
-    os.nb = (uint32_t)((n0 + lane) * 4);
+    os.nb = lane < nv ? (uint32_t)((n0 + lane) * 4) : 0u;
     os.D = f.D;
     os.wave = wave;
     os.lane = lane;
