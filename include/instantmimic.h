@@ -304,9 +304,12 @@ im_status im_value(im_ctx *ctx, const float *obs, int64_t ld_obs, int64_t n_envs
  * im_policy_act followed by im_value on the same observation, as one rollout
  * step needs them (Fig. 3: action, logp and value of every observation go to
  * the storage).  Arguments as in the two calls; the outputs equal theirs bit
- * for bit.  A large bf16 batch rounds and transposes the observation into the
- * staging buffer once for both networks instead of once per call.  Needs
- * im_set_critic.  Errors: those of the two calls, before any launch.
+ * for bit.  A bf16 network of at most 8 layers, hidden widths and input up to
+ * 1024 and an output up to 128 runs as one kernel that reads the float
+ * observation itself; when both networks are beyond that, a large batch rounds
+ * and transposes the observation into the staging buffer once for both
+ * instead of once per call.  Needs im_set_critic.  Errors: those of the two
+ * calls, before any launch.
  */
 im_status im_policy_act_value(im_ctx *ctx, const float *obs, int64_t ld_obs,
                               const uint32_t *env_n, int64_t n_envs, float *mean, float *action,

@@ -345,6 +345,50 @@ def test_policy_act_value_equals_separate_calls(cfg, N):
     assert not torch.equal(ref1[3], ref2[3])
 
 
+@pytest.mark.parametrize("wide", ["both", "critic"])
+def test_policy_act_value_per_layer_networks(wide):
+    """Networks beyond the one-launch kernel (a 1280-wide first hidden layer)
+    at a large bf16 batch: with both per-layer, the critic's first layer reads
+    the observation the policy staged; with the policy in one launch the critic
+    stages its own.  Either way the bits of the two separate calls."""
+    N = 16384 + 700
+    print("policy_act_value per-layer %s N %d" % (wide, N), flush=True)
+    d = synth.make_world(4, n_envs=N)
+    D, A = d["policy"]["dims"][0], d["policy"]["dims"][-1]
+    if wide == "both":
+        d["policy"] = synth.make_policy(np.random.default_rng(11), [D, 1280, 512, A], True)
+    d["critic"] = synth.make_policy(np.random.default_rng(12), [D, 1280, 512, 1], True)
+    ctx = binding.Context(d, max_envs=N)
+    obs1, n1 = _gpu_obs(ctx, d, N, 1)
+    obs2, n2 = _gpu_obs(ctx, d, N, 2)
+    res = {}
+    for key, obs, n, comb in (("s1", obs1, n1, False), ("c2", obs2, n2, True),
+                              ("s2", obs2, n2, False), ("c1", obs1, n1, True)):
+        m = torch.full((N, A), -9.0, device="cuda")
+        a = torch.full((N, A), -9.0, device="cuda")
+        lp = torch.full((N,), -9.0, device="cuda")
+        v = torch.full((N,), -9.0, device="cuda")
+        if comb:
+            ctx.policy_act_value(obs, n, N, m, a, lp, v)
+        else:
+            ctx.policy_act(obs, n, N, m, a, lp)
+            ctx.value(obs, N, v)
+        res[key] = (m, a, lp, v)
+    torch.cuda.synchronize()
+    for c, s_ in (("c1", "s1"), ("c2", "s2")):
+        for name, g, r in zip(("mean", "action", "logp", "value"), res[c], res[s_]):
+            assert torch.equal(g, r), "%s differs from the separate calls" % name
+    assert not torch.equal(res["s1"][3], res["s2"][3])
+    # and the value is the critic's, against the oracle on sampled envs
+    idx = np.random.default_rng(5).choice(N, 64, replace=False)
+    ob = obs1.cpu().numpy()[:, idx].astype(np.float32)
+    ov = oracle.value(d["critic"], ob)
+    gv = res["c1"][3].cpu().numpy()[idx]
+    sv = np.sqrt(np.mean(ov.astype(np.float64) ** 2))
+    assert np.max(np.abs(gv - ov) / np.maximum(np.abs(ov), sv)) <= 2e-2
+    ctx.close()
+
+
 def test_policy_act_value_errors_before_any_launch():
     """Without a critic, or with a null value buffer, the combined call fails
     with the two calls' errors and writes nothing."""
