@@ -77,7 +77,10 @@ def check_policy(d, N):
     (CHAIN6, [], 64, 200),                # no hidden layer
     (CHAIN6, [256] * 7, 8, 130),          # eight layers
     (COMB64, [1024], 69, 333),            # 1024-wide padded observation, three action tiles
-], ids=["256-768", "1024-512-full-grid", "one-env", "one-layer", "eight-layers", "obs-961"])
+    (CHAIN6, [512], 96, 777),             # three full action tiles
+    (CHAIN6, [256], 128, 300),            # the widest action set: four full tiles
+], ids=["256-768", "1024-512-full-grid", "one-env", "one-layer", "eight-layers", "obs-961",
+        "96-actions", "128-actions"])
 def test_fused_policy_shapes(parent, hidden, A, N):
     check_policy(_world(parent, hidden, A, 5), N)
 
