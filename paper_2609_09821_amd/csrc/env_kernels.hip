@@ -114,69 +114,78 @@ __device__ __forceinline__ Frame child_frame(const Frame &p, const float4 *rec, 
     return f;
 }
 
-// Forward kinematics of one reference segment record in preorder;
-// visit(i, body, frame, anchor, data, q_joint, w_joint) is called for every
-// position i (q_joint, w_joint: the reference joint rotation and joint angular
-// velocity in the parent frame; the root's world values).  A
-// depth-2 software prefetch keeps the segment record and the per-body data
-// returned by load(body) for positions i+1 and i+2 in flight while body i is
-// processed, so the memory latency of one body overlaps the arithmetic of
-// the previous ones.
+// Forward kinematics of one reference segment record in preorder, over a walk
+// table T (the whole skeleton, or one part of it): visit(i, body, own, frame,
+// anchor, data, q_joint, w_joint) is called for every position i (q_joint, w_joint:
+// the reference joint rotation and joint angular velocity in the parent frame;
+// the root's world values).  A ring of R slots keeps the segment record and
+// the per-body data returned by load(body) of the next R - 1 positions in
+// flight while one position is processed: position i takes slot (i - 1) % R,
+// which is then refilled with position i + R.  The loop is unrolled by R so
+// that each slot stays in fixed registers; a rotating buffer (next -> current)
+// would copy registers whose loads are still in flight, and each copy waits
+// for them, which costs a whole memory latency per position.  Positions past
+// the end refetch the walk's last body, so that every load is unconditional
+// and inside the tables.
 struct NoData {
 };
 
-template <class D, class Load, class Visit>
-__device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, const float4 *rec,
-                                              float alpha, Load &&load, Visit &&visit)
+using PartWalk = SkelTab::PartWalk;
+
+// The walk tables: the whole skeleton (position p's segment record is p) or
+// one part walk (its record is rec[p]); both have body, pslot, bslot, jtype
+// and offset per position.  The walk reads them through the constant address
+// space: they are written only when a context is created, and so their reads
+// stay scalar loads (counted apart from the vector memory operations) also
+// where the walk itself stores (reset walks); read as ordinary global memory
+// next to those stores they became vector loads, each waiting for every
+// store and load issued before it.
+#define IM_CONST_AS __attribute__((address_space(4)))
+__device__ __forceinline__ int walk_len(const IM_CONST_AS SkelTab *t) { return t->B; }
+__device__ __forceinline__ int walk_len(const IM_CONST_AS PartWalk *t) { return t->n; }
+__device__ __forceinline__ int walk_rec(const IM_CONST_AS SkelTab *, int p) { return p; }
+__device__ __forceinline__ int walk_rec(const IM_CONST_AS PartWalk *t, int p) { return t->rec[p]; }
+__device__ __forceinline__ bool walk_own(const IM_CONST_AS SkelTab *, int) { return true; }
+__device__ __forceinline__ bool walk_own(const IM_CONST_AS PartWalk *t, int p) { return t->own[p] != 0; }
+
+template <int R, class D, class T, class Load, class Visit>
+__device__ __forceinline__ void walk_ring(const T *tg, const float4 *rec, float alpha, Load &&load,
+                                          Visit &&visit)
 {
+    const IM_CONST_AS T *t = (const IM_CONST_AS T *)tg;
     const LdsStack<13> st{im_lds + threadIdx.x, (int)blockDim.x};
     float buf[13];
-    const int B = sk->B;
+    const int n = walk_len(t);
     const float4 *jr = rec + 6;
-    // position 0 (root) and prefetch of positions 1, 2
-    D d0 = load(0);
-    D d1{}, d2{};
-    float4 a1{}, u1{}, w1{}, a2{}, u2{}, w2{};
-    if (B > 1) {
-        d1 = load(sk->body[1]);
-        a1 = jr[0];
-        u1 = jr[1];
-        w1 = jr[2];
-    }
-    if (B > 2) {
-        d2 = load(sk->body[2]);
-        a2 = jr[3];
-        u2 = jr[4];
-        w2 = jr[5];
-    }
+    struct Slot {
+        D d;
+        float4 a, u, w;
+    };
+    auto fetch = [&](int p, Slot &s) {
+        const int q = p < n ? p : n - 1;
+        s.d = load(t->body[q]);
+        const float4 *r = jr + 3 * (walk_rec(t, q) - 1);
+        s.a = r[0];
+        s.u = r[1];
+        s.w = r[2];
+    };
+    const D d0 = load(0);
+    Slot sl[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) fetch(1 + j, sl[j]);
     f3 A;
     Frame cur = root_frame(rec, alpha, &A);
-    // visit also gets the body's reference joint rotation and joint angular
-    // velocity in the parent frame (the root's world values)
-    visit(0, 0, cur, A, d0, cur.Q, cur.W);
-    if (sk->bslot[0] >= 0) {
+    visit(0, t->body[0], walk_own(t, 0), cur, A, d0, cur.Q, cur.W);
+    if (t->bslot[0] >= 0) {
         pack_frame(cur, buf);
-        st.put(sk->bslot[0], buf);
+        st.put(t->bslot[0], buf);
     }
-    for (int i = 1; i < B; ++i) {
-        const D d = d1;
-        const float4 ra = a1, ru = u1, rw = w1;
-        d1 = d2;
-        a1 = a2;
-        u1 = u2;
-        w1 = w2;
-        if (i + 2 < B) {
-            d2 = load(sk->body[i + 2]);
-            const float4 *p = jr + 3 * (i + 1);
-            a2 = p[0];
-            u2 = p[1];
-            w2 = p[2];
-        }
-        if (sk->pslot[i] >= 0) {
-            st.get(sk->pslot[i], buf);
+    auto step = [&](int i, const Slot &s) {
+        if (t->pslot[i] >= 0) {
+            st.get(t->pslot[i], buf);
             cur = unpack_frame(buf);
         }
-        const f3 off = mk3(sk->offset[i][0], sk->offset[i][1], sk->offset[i][2]);
+        const f3 off = mk3(t->offset[i][0], t->offset[i][1], t->offset[i][2]);
         // child frame from the prefetched record (same arithmetic as child_frame)
         Frame c;
         const f3 r = qrot(cur.Q, off);
@@ -184,22 +193,47 @@ __device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, co
         c.V = cur.V + cross3(cur.W, r);
         q4 ql = q4{1.0f, 0.0f, 0.0f, 0.0f};
         f3 wl = mk3(0.0f, 0.0f, 0.0f);
-        if (sk->jtype[i] == IM_JOINT_FIXED) {
+        if (t->jtype[i] == IM_JOINT_FIXED) {
             c.Q = cur.Q;
             c.W = cur.W;
         } else {
-            ql = slerp_basis(ra, ru, alpha * rw.w);
-            wl = mk3(rw.x, rw.y, rw.z);
+            ql = slerp_basis(s.a, s.u, alpha * s.w.w);
+            wl = mk3(s.w.x, s.w.y, s.w.z);
             c.Q = qmul(cur.Q, ql);
             c.W = cur.W + qrot(cur.Q, wl);
         }
         cur = c;
-        visit(i, sk->body[i], cur, A, d, ql, wl);
-        if (sk->bslot[i] >= 0) {
+        visit(i, t->body[i], walk_own(t, i), cur, A, s.d, ql, wl);
+        if (t->bslot[i] >= 0) {
             pack_frame(cur, buf);
-            st.put(sk->bslot[i], buf);
+            st.put(t->bslot[i], buf);
+        }
+    };
+    int i = 1;
+    for (; i + R <= n; i += R) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            step(i + j, sl[j]);
+            fetch(i + j + R, sl[j]);
         }
     }
+#pragma unroll
+    for (int j = 0; j < R - 1; ++j)
+        if (i + j < n) step(i + j, sl[j]);
+}
+
+constexpr int WALK_RING = 3;
+
+// visit(i, body, frame, anchor, data, q_joint, w_joint) for every preorder
+// position i of the skeleton.
+template <class D, class Load, class Visit>
+__device__ __forceinline__ void walk_prefetch(const SkelTab *__restrict__ sk, const float4 *rec,
+                                              float alpha, Load &&load, Visit &&visit)
+{
+    walk_ring<WALK_RING, D>(sk, rec, alpha, load,
+                            [&](int i, int b, bool, const Frame &f, f3 A, const D &d, q4 ql, f3 wl) {
+                                visit(i, b, f, A, d, ql, wl);
+                            });
 }
 
 // Discrete phase -> (i0, alpha), fp32 without contraction.  phi_ev is
@@ -350,7 +384,8 @@ __device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, f
 {
     const int64_t ld = a.ld;
     const SkelTab *__restrict__ sk = a.sk;
-    const int rows_f = 9 * (1 + sk->n_ee);
+    const IM_CONST_AS SkelTab *skc = (const IM_CONST_AS SkelTab *)sk;  // scalar reads next to stores
+    const int rows_f = 9 * (1 + skc->n_ee);
     const ClipTab ci = a.clips[k];
     float phj = ph;
     for (int j = 0; j < a.obs_future; ++j) {
@@ -366,7 +401,7 @@ __device__ __forceinline__ void obs_extras(const EnvArgs &a, int64_t e, int k, f
         const int base = a.obs_base + j * rows_f;
         walk_prefetch<NoData>(sk, rec, al, [](int) { return NoData{}; },
                               [&](int i, int, const Frame &f, f3 A, const NoData &, q4, f3) {
-            const int slot = sk->ee_slot[i];
+            const int slot = skc->ee_slot[i];
             if (slot >= 0) write_frame9(a.obs, ld, e, base + 9 * slot, h, A + f.P, f.Q);
         });
     }
@@ -406,85 +441,16 @@ struct SimPV {
     f3 P, V;
 };
 
-using PartWalk = SkelTab::PartWalk;
-
-// Forward kinematics over one part walk (root first, preorder), with the same
-// depth-2 prefetch as walk_prefetch; load(body) is called for owned bodies
-// only, and visit(i, body, own, frame, anchor, data, joint rotation, joint
-// angular velocity) for every position.
+// Forward kinematics over one part walk: visit(i, body, own, frame, anchor,
+// data, joint rotation, joint angular velocity) for every position.  load(body)
+// is called for every position, owned or not (an ancestor's data is what its
+// owner's walk reads too, so it comes from the cache), so that the ring's
+// loads stay unconditional; visit uses it for owned bodies only.
 template <class D, class Load, class Visit>
 __device__ __forceinline__ void walk_part(const PartWalk *__restrict__ w, const float4 *rec,
                                           float alpha, Load &&load, Visit &&visit)
 {
-    const LdsStack<13> st{im_lds + threadIdx.x, (int)blockDim.x};
-    float buf[13];
-    const int n = w->n;
-    const float4 *jr = rec + 6;
-    D d0 = w->own[0] ? load(0) : D{};
-    D d1{}, d2{};
-    float4 a1{}, u1{}, w1{}, a2{}, u2{}, w2{};
-    if (n > 1) {
-        d1 = w->own[1] ? load(w->body[1]) : D{};
-        const float4 *p = jr + 3 * (w->rec[1] - 1);
-        a1 = p[0];
-        u1 = p[1];
-        w1 = p[2];
-    }
-    if (n > 2) {
-        d2 = w->own[2] ? load(w->body[2]) : D{};
-        const float4 *p = jr + 3 * (w->rec[2] - 1);
-        a2 = p[0];
-        u2 = p[1];
-        w2 = p[2];
-    }
-    f3 A;
-    Frame cur = root_frame(rec, alpha, &A);
-    visit(0, 0, w->own[0], cur, A, d0, cur.Q, cur.W);
-    if (w->bslot[0] >= 0) {
-        pack_frame(cur, buf);
-        st.put(w->bslot[0], buf);
-    }
-    for (int i = 1; i < n; ++i) {
-        const D d = d1;
-        const float4 ra = a1, ru = u1, rw = w1;
-        d1 = d2;
-        a1 = a2;
-        u1 = u2;
-        w1 = w2;
-        if (i + 2 < n) {
-            d2 = w->own[i + 2] ? load(w->body[i + 2]) : D{};
-            const float4 *p = jr + 3 * (w->rec[i + 2] - 1);
-            a2 = p[0];
-            u2 = p[1];
-            w2 = p[2];
-        }
-        if (w->pslot[i] >= 0) {
-            st.get(w->pslot[i], buf);
-            cur = unpack_frame(buf);
-        }
-        const f3 off = mk3(w->offset[i][0], w->offset[i][1], w->offset[i][2]);
-        Frame c;
-        const f3 r = qrot(cur.Q, off);
-        c.P = cur.P + r;
-        c.V = cur.V + cross3(cur.W, r);
-        q4 ql = q4{1.0f, 0.0f, 0.0f, 0.0f};
-        f3 wl = mk3(0.0f, 0.0f, 0.0f);
-        if (w->jtype[i] == IM_JOINT_FIXED) {
-            c.Q = cur.Q;
-            c.W = cur.W;
-        } else {
-            ql = slerp_basis(ra, ru, alpha * rw.w);
-            wl = mk3(rw.x, rw.y, rw.z);
-            c.Q = qmul(cur.Q, ql);
-            c.W = cur.W + qrot(cur.Q, wl);
-        }
-        cur = c;
-        visit(i, w->body[i], w->own[i], cur, A, d, ql, wl);
-        if (w->bslot[i] >= 0) {
-            pack_frame(cur, buf);
-            st.put(w->bslot[i], buf);
-        }
-    }
+    walk_ring<WALK_RING, D>(w, rec, alpha, load, visit);
 }
 
 // Observation rows of the bodies a part walk owns, from the sim state (env
