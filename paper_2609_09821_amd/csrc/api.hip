@@ -292,11 +292,13 @@ std::string build_skeleton(const im_skeleton *sk, SkelTab *t, int *max_depth)
             }
         *slots = ns;
         w.n = (int)ordw.size();
+        w.n_own = 0;
         for (int i = 0; i < w.n; ++i) {
             const int b = ordw[i];
             w.body[i] = b;
             w.rec[i] = pos_of[b];
             w.own[i] = own_of[b] == h ? 1 : 0;
+            if (w.own[i]) w.own_body[w.n_own++] = b;
             w.bslot[i] = slotw[b];
             w.pslot[i] = -1;
             if (i > 0 && sk->parent[b] != ordw[i - 1]) {
@@ -755,7 +757,8 @@ im_status im_env_step_fused(im_ctx *c, const im_env_bufs *b, void *stream)
     if ((s = check_device(c)) != IM_OK) return s;
     EnvArgs a = env_args(c, b);
     // threads per env: the configured split, or by batch size (path walks for
-    // small batches, two halves up to SPLIT_ENV_MAX, then one thread)
+    // small batches, two halves up to SPLIT_ENV_MAX where a skeleton has no
+    // path split, then one thread)
     int split = c->cfg.env_split;
     if (split == IM_SPLIT_AUTO)
         split = (a.n <= PATH_ENV_MAX && c->n_paths >= 2) ? IM_SPLIT_PATHS

@@ -330,46 +330,97 @@ __device__ __forceinline__ void write_frame9(float *obs, int64_t ld, int64_t e, 
     o[8 * ld] = c1z;
 }
 
-// 15 observation rows of body b in the heading frame.
-__device__ __forceinline__ void write_obs_body(float *obs, int64_t ld, int64_t e, int b,
-                                               const Heading &h, f3 P, q4 Q, f3 V, f3 W)
+// The 15 observation rows of a body in the heading frame: position, the first
+// two columns of the rotation matrix, linear and angular velocity.
+__device__ __forceinline__ void obs_body_rows(const Heading &h, f3 P, q4 Q, f3 V, f3 W,
+                                              float (&o)[15])
 {
-    float *o = obs + (int64_t)(15 * b) * ld + e;
     const float px = P.x - h.ox, py = P.y - h.oy;
     o[0] = h.c * px + h.s * py;
-    o[ld] = h.c * py - h.s * px;
-    o[2 * ld] = P.z;
+    o[1] = h.c * py - h.s * px;
+    o[2] = P.z;
     const float c0x = 1.0f - 2.0f * (Q.y * Q.y + Q.z * Q.z);
     const float c0y = 2.0f * (Q.x * Q.y + Q.w * Q.z);
     const float c0z = 2.0f * (Q.x * Q.z - Q.w * Q.y);
     const float c1x = 2.0f * (Q.x * Q.y - Q.w * Q.z);
     const float c1y = 1.0f - 2.0f * (Q.x * Q.x + Q.z * Q.z);
     const float c1z = 2.0f * (Q.y * Q.z + Q.w * Q.x);
-    o[3 * ld] = h.c * c0x + h.s * c0y;
-    o[4 * ld] = h.c * c0y - h.s * c0x;
-    o[5 * ld] = c0z;
-    o[6 * ld] = h.c * c1x + h.s * c1y;
-    o[7 * ld] = h.c * c1y - h.s * c1x;
-    o[8 * ld] = c1z;
-    o[9 * ld] = h.c * V.x + h.s * V.y;
-    o[10 * ld] = h.c * V.y - h.s * V.x;
-    o[11 * ld] = V.z;
-    o[12 * ld] = h.c * W.x + h.s * W.y;
-    o[13 * ld] = h.c * W.y - h.s * W.x;
-    o[14 * ld] = W.z;
+    o[3] = h.c * c0x + h.s * c0y;
+    o[4] = h.c * c0y - h.s * c0x;
+    o[5] = c0z;
+    o[6] = h.c * c1x + h.s * c1y;
+    o[7] = h.c * c1y - h.s * c1x;
+    o[8] = c1z;
+    o[9] = h.c * V.x + h.s * V.y;
+    o[10] = h.c * V.y - h.s * V.x;
+    o[11] = V.z;
+    o[12] = h.c * W.x + h.s * W.y;
+    o[13] = h.c * W.y - h.s * W.x;
+    o[14] = W.z;
 }
 
-// Observation of env e from its (post-reset) sim state.  The body loop has
-// no dependency between iterations, so several bodies' loads are in flight.
+__device__ __forceinline__ void store_obs_body(float *obs, int64_t ld, int64_t e, int b,
+                                               const float (&o)[15])
+{
+    float *p = obs + (int64_t)(15 * b) * ld + e;
+#pragma unroll
+    for (int r = 0; r < 15; ++r) p[r * ld] = o[r];
+}
+
+// 15 observation rows of body b in the heading frame.
+__device__ __forceinline__ void write_obs_body(float *obs, int64_t ld, int64_t e, int b,
+                                               const Heading &h, f3 P, q4 Q, f3 V, f3 W)
+{
+    float o[15];
+    obs_body_rows(h, P, Q, V, W, o);
+    store_obs_body(obs, ld, e, b, o);
+}
+
+struct SimFull {
+    f3 P;
+    q4 Q;
+    f3 V, W;
+};
+
+// Observation of env e from its (post-reset) sim state.  A ring of three
+// slots holds the sim state of the next bodies: body b's rows are formed from
+// its slot, the slot is refilled with body b + 3, and only then are the rows
+// stored.  A wave counts its loads and stores in one in-order queue, so the
+// loads of a body issued after the previous body's stores (the plain loop)
+// wait for those stores to complete; issued before them, they wait only for
+// the stores of three bodies back.  Bodies past the last refetch it.
 __device__ __forceinline__ void obs_from_sim(const EnvArgs &a, int64_t e, float phase)
 {
     const int64_t ld = a.ld;
-    const Heading h = heading_of(ld4(a.quat, 0, ld, e), ld3(a.pos, 0, ld, e));
     const int B = a.sk->B;
-#pragma unroll 4
-    for (int b = 0; b < B; ++b)
-        write_obs_body(a.obs, ld, e, b, h, ld3(a.pos, b, ld, e), ld4(a.quat, b, ld, e),
-                       ld3(a.linvel, b, ld, e), ld3(a.angvel, b, ld, e));
+    auto fetch = [&](int b, SimFull &sf) {
+        const int q = b < B ? b : B - 1;
+        sf.P = ld3(a.pos, q, ld, e);
+        sf.Q = ld4(a.quat, q, ld, e);
+        sf.V = ld3(a.linvel, q, ld, e);
+        sf.W = ld3(a.angvel, q, ld, e);
+    };
+    SimFull sl[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) fetch(j, sl[j]);
+    const Heading h = heading_of(sl[0].Q, sl[0].P);
+    int b = 0;
+    for (; b + 3 <= B; b += 3) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            float o[15];
+            obs_body_rows(h, sl[j].P, sl[j].Q, sl[j].V, sl[j].W, o);
+            // the refill stays after the rows are formed, so that the slot
+            // keeps its registers across the loop
+            __builtin_amdgcn_sched_barrier(0);
+            fetch(b + j + 3, sl[j]);
+            __builtin_amdgcn_sched_barrier(0);
+            store_obs_body(a.obs, ld, e, b + j, o);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (b + j < B) write_obs_body(a.obs, ld, e, b + j, h, sl[j].P, sl[j].Q, sl[j].V, sl[j].W);
     a.obs[(int64_t)(15 * B) * ld + e] = phase;
 }
 
@@ -454,19 +505,41 @@ __device__ __forceinline__ void walk_part(const PartWalk *__restrict__ w, const 
 }
 
 // Observation rows of the bodies a part walk owns, from the sim state (env
-// not reset); h = the heading of the sim root.
-__device__ __forceinline__ void obs_part_from_sim(const EnvArgs &a, const PartWalk *__restrict__ w,
+// not reset); h = the heading of the sim root.  The same three-slot ring as
+// obs_from_sim, over the walk's owned bodies.
+__device__ __forceinline__ void obs_part_from_sim(const EnvArgs &a, const PartWalk *__restrict__ wg,
                                                   int64_t e, const Heading &h)
 {
+    const IM_CONST_AS PartWalk *w = (const IM_CONST_AS PartWalk *)wg;
     const int64_t ld = a.ld;
-    const int n = w->n;
-#pragma unroll 4
-    for (int i = 0; i < n; ++i) {
-        if (!w->own[i]) continue;
-        const int b = w->body[i];
-        write_obs_body(a.obs, ld, e, b, h, ld3(a.pos, b, ld, e), ld4(a.quat, b, ld, e),
-                       ld3(a.linvel, b, ld, e), ld3(a.angvel, b, ld, e));
+    const int n = w->n_own;
+    if (n <= 0) return;
+    auto fetch = [&](int j, SimFull &sf) {
+        const int b = w->own_body[j < n ? j : n - 1];
+        sf.P = ld3(a.pos, b, ld, e);
+        sf.Q = ld4(a.quat, b, ld, e);
+        sf.V = ld3(a.linvel, b, ld, e);
+        sf.W = ld3(a.angvel, b, ld, e);
+    };
+    SimFull sl[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) fetch(j, sl[j]);
+    int i = 0;
+    for (; i + 3 <= n; i += 3) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            float o[15];
+            obs_body_rows(h, sl[j].P, sl[j].Q, sl[j].V, sl[j].W, o);
+            __builtin_amdgcn_sched_barrier(0);
+            fetch(i + j + 3, sl[j]);
+            __builtin_amdgcn_sched_barrier(0);
+            store_obs_body(a.obs, ld, e, w->own_body[i + j], o);
+        }
     }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+        if (i + j < n)
+            write_obs_body(a.obs, ld, e, w->own_body[i + j], h, sl[j].P, sl[j].Q, sl[j].V, sl[j].W);
 }
 
 // Reference state initialisation of the bodies a part walk owns at (clip k,

@@ -12,8 +12,10 @@ namespace im {
 // Batches up to this many envs use smaller GEMM tiles so that every layer
 // still spreads over all 256 CUs.
 constexpr int64_t SMALL_BATCH = 16384;
-// Batches up to this many envs run the fused step on two threads per env.
-constexpr int64_t SPLIT_ENV_MAX = 32768;
+// Batches up to this many envs run the fused step on two threads per env when
+// the skeleton has no path split (with the walks' prefetch ring, one thread
+// per env is faster above it: 24576 and 32768 envs measured).
+constexpr int64_t SPLIT_ENV_MAX = 16384;
 // Batches up to this many envs run it on one thread per root-to-leaf path.
 constexpr int64_t PATH_ENV_MAX = 16384;
 

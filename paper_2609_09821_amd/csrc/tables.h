@@ -48,6 +48,8 @@ struct SkelTab {
         int32_t leaf[IM_MAX_BODIES];   // leaf of the whole skeleton (end effector)
         float offset[IM_MAX_BODIES][4];
         float massw[IM_MAX_BODIES];
+        int32_t n_own;                 // bodies this walk owns, in walk order
+        int32_t own_body[IM_MAX_BODIES];
     };
     int32_t half_slots;            // parked-frame slots needed by either half walk
     PartWalk half[2];

@@ -158,7 +158,8 @@ def test_policy_parity(cfg):
 
 @pytest.mark.parametrize("cfg", [2, 4, 6])
 def test_env_step_parity_large_batch_kernel(cfg):
-    # above 32768 envs the fused step runs one thread per env (below, two);
+    # above 16384 envs the fused step runs one thread per env (below, one per
+    # root-to-leaf path);
     # a ragged size so that its last block is partly empty
     N, T = 40037, 2
     d, w, ctx, bufs = _setup(cfg, N)
