@@ -58,8 +58,8 @@ TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act (a bf16 policy is one launch)
     "policy": {"sources": ["policy_kernels.hip", "device_math.h", "launch.h"], "sha": "8d96ff129a595a70", "workloads": {
         4: {"fetch": [109671.5], "write": [35584.0]}}},
-    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "820448a5956455ad", "workloads": {
-        4: {"fetch": [61765.8], "write": [169487.8]}}},
+    "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "eeed804b596bf8b3", "workloads": {
+        4: {"fetch": [61781.3], "write": [169488.8]}}},
 }
 
 
