@@ -1271,9 +1271,12 @@ __device__ __forceinline__ void fused_hidden(const FusedMlpArgs &f, int l, uint8
 }
 
 // Last layer and sampling.  The 32 MT padded actions of the 64 envs are 2 MT
-// MFMA tiles of 32 x 32, each computed over KS = 4 / MT slices of K (one at
-// MT = 3), so that every wave but two at MT = 3 takes one (tile, env half,
-// K slice).  The partial tiles go to LDS and all 512 threads then take one
+// MFMA tiles of 32 x 32.  Up to MT = 3 a wave takes one action tile for both
+// env halves over one of KS = 8 / MT slices of K (two at MT = 3), so that
+// each slice of the weights is loaded once per workgroup; at MT = 4, where
+// those partial tiles would not fit in LDS next to the mean and action rows,
+// a wave takes one (tile, env half) over the whole of K.  Every wave but two
+// at MT = 3 has work.  The partial tiles go to LDS and all 512 threads then take one
 // (env, block of four actions) at a time: the mean is the bias plus the
 // partials in slice order, the noise comes from Philox, action = mean +
 // sigma z, and each env's logp adds its blocks' sums in block order.  log
@@ -1283,8 +1286,12 @@ template <int MT>
 __device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, int rs, int64_t n0,
                                            int64_t nv, int wave, int tid)
 {
-    constexpr int KS = MT == 3 ? 1 : 4 / MT;
+    constexpr int TN = MT == 4 ? 1 : 2;                       // env halves per wave
+    constexpr int KS = MT == 4 ? 1 : (MT == 3 ? 2 : 8 / MT);  // K slices
     constexpr int MP = 32 * MT;
+    // partial tiles, mean and action rows and the per-block sums over the input rows
+    static_assert((KS * FUSED_BN * MP + 2 * FUSED_BN * MP + FUSED_BN * 33) * 4 <= FUSED_BN * FUSED_ROW,
+                  "last-layer LDS");
     const GemmArgs &g = f.out;
     const int l = f.L - 1, nks = f.K_pad[l] / 64, lane = tid & 63, A = g.A;
     __shared__ float sig[128], sbias[128], slp0;
@@ -1300,14 +1307,19 @@ __device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, 
     } else if (wave == 2 && lane < nv) {
         en = g.env_n[n0 + lane];
     }
-    f32x16_t acc[1][1];
+    f32x16_t acc[1][TN];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) acc[0][0][q] = 0.0f;
-    const int nt = wave & 1, mt = (wave >> 1) % MT, ksl = (wave >> 1) / MT;
-    const bool active = wave < 2 * MT * KS;
+    for (int nt = 0; nt < TN; ++nt)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[0][nt][q] = 0.0f;
+    // wave -> (env half when TN = 1, action tile, K slice)
+    const int nt0 = TN == 1 ? (wave & 1) : 0;
+    const int wt = TN == 1 ? (wave >> 1) : wave;
+    const int mt = wt % MT, ksl = wt / MT;
+    const bool active = wave < (2 / TN) * MT * KS;
     if (active)
-        fused_mma<1, 1, false>(f.w[l], f.w_bytes[l], 32 * mt, nks, ksl * nks / KS, (ksl + 1) * nks / KS,
-                               act, rs, 32 * nt, lane, acc);
+        fused_mma<1, TN, false>(f.w[l], f.w_bytes[l], 32 * mt, nks, ksl * nks / KS,
+                                (ksl + 1) * nks / KS, act, rs, 32 * nt0, lane, acc);
     __syncthreads();
     // the layer input is read: partial tiles [KS][64 envs][MP] fp32 (16-byte
     // units XOR-swizzled by env % 8), mean and action rows [64][A], and the
@@ -1317,13 +1329,16 @@ __device__ __forceinline__ void fused_last(const FusedMlpArgs &f, uint8_t *act, 
     float *sact = smean + FUSED_BN * A;
     float *slp = sact + FUSED_BN * A;
     if (active) {
-        const int e = 32 * nt + (lane & 31), h = lane >> 5;
 #pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-            const int unit = (8 * mt + 2 * grp + h) ^ (e & 7);
-            *(f32x4_t *)(part + (ksl * FUSED_BN + e) * MP + 4 * unit) =
-                f32x4_t{acc[0][0][4 * grp], acc[0][0][4 * grp + 1], acc[0][0][4 * grp + 2],
-                        acc[0][0][4 * grp + 3]};
+        for (int nt = 0; nt < TN; ++nt) {
+            const int e = 32 * (nt0 + nt) + (lane & 31), h = lane >> 5;
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const int unit = (8 * mt + 2 * grp + h) ^ (e & 7);
+                *(f32x4_t *)(part + (ksl * FUSED_BN + e) * MP + 4 * unit) =
+                    f32x4_t{acc[0][nt][4 * grp], acc[0][nt][4 * grp + 1], acc[0][nt][4 * grp + 2],
+                            acc[0][nt][4 * grp + 3]};
+            }
         }
     }
     if (wave == 0) {
