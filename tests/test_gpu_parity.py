@@ -104,6 +104,18 @@ def test_env_step_eight_leaf_tree(split):
     _step_parity(3, 700, 4, desc=d)
 
 
+# A 15-body tree with ten leaves (nine on the root, one two-body chain): no
+# path split, so the batch-size rule picks two halves up to 16384 envs and one
+# thread per env above.
+@pytest.mark.parametrize("N", [700, 16384 + 300])
+def test_env_step_ten_leaf_tree_auto_split(N):
+    d = synth.make_world(3, n_envs=N)
+    parent = np.array([-1, 0, 0, 0, 0, 0, 0, 1, 0, 0, 0, 0, 0, 0, 7], np.int32)
+    assert len(parent) == d["skeleton"]["n_bodies"]
+    d["skeleton"] = dict(d["skeleton"], parent=parent)
+    _step_parity(3, N, 3, desc=d)
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5, 6])
 def test_standin_parity(cfg):
     N = SIZES[cfg]
