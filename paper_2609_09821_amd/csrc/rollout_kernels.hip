@@ -128,9 +128,12 @@ __global__ __launch_bounds__(256) void value_head_obs_kernel(const float *__rest
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void gae_kernel(GaeArgs g)
 {
-    // steps are read in chunks of C whose loads are all issued before the
-    // chunk is processed: the walk is serial per env, the memory latency is
-    // paid once per chunk instead of once per step
+    // steps are read in chunks of C, two chunk buffers in turn: the loads of
+    // the next chunk are issued before the current one is processed (and,
+    // backwards, before its stores -- a wave counts loads and stores in one
+    // in-order queue, so loads issued after stores wait for them).  The loop
+    // is unrolled by two so that each buffer keeps its registers.  Steps
+    // outside [0, T) load step 0 or T - 1 and are not processed.
     constexpr int C = 8;
     __shared__ double red[IM_SUMMARY_FIELDS][256];
     const int tid = threadIdx.x;
@@ -141,19 +144,22 @@ __global__ __launch_bounds__(256) void gae_kernel(GaeArgs g)
     if (e < g.n) {
         const int64_t ld = g.ld;
         const int T = g.T;
-        float r[C], v[C];
-        uint8_t te[C], tr[C];
         if (g.summary) {
             float epr = g.ep_return[e];
             int32_t epl = g.ep_length[e];
-            for (int t0 = 0; t0 < T; t0 += C) {
+            float ra[C], rb[C];
+            uint8_t ta[C], tb[C], ua[C], ub[C];
+            auto load_fwd = [&](int t0, float (&r)[C], uint8_t (&te)[C], uint8_t (&tr)[C]) {
 #pragma unroll
                 for (int j = 0; j < C; ++j) {
-                    const int64_t i = (int64_t)(t0 + j < T ? t0 + j : T - 1) * ld + e;
+                    const int t = t0 + j < T ? t0 + j : T - 1;
+                    const int64_t i = (int64_t)t * ld + e;
                     r[j] = g.reward[i];
                     te[j] = g.term[i];
                     tr[j] = g.trunc[i];
                 }
+            };
+            auto fwd = [&](int t0, const float (&r)[C], const uint8_t (&te)[C], const uint8_t (&tr)[C]) {
 #pragma unroll
                 for (int j = 0; j < C; ++j) {
                     if (t0 + j >= T) break;
@@ -173,6 +179,13 @@ __global__ __launch_bounds__(256) void gae_kernel(GaeArgs g)
                         epl = 0;
                     }
                 }
+            };
+            load_fwd(0, ra, ta, ua);
+            for (int t0 = 0; t0 < T; t0 += 2 * C) {
+                load_fwd(t0 + C, rb, tb, ub);
+                fwd(t0, ra, ta, ua);
+                load_fwd(t0 + 2 * C, ra, ta, ua);
+                if (t0 + C < T) fwd(t0 + C, rb, tb, ub);
             }
             g.ep_return[e] = epr;
             g.ep_length[e] = epl;
@@ -182,16 +195,23 @@ __global__ __launch_bounds__(256) void gae_kernel(GaeArgs g)
             const double gam = g.gamma, gl = g.gamma * g.lambda;
             double adv = 0.0;
             double v_next = (double)g.value[(int64_t)T * ld + e];
-            for (int t1 = T; t1 > 0; t1 -= C) {
-                // chunk t1-C .. t1-1, walked backwards (j = 0 is step t1-1)
+            float ra[C], rb[C], va[C], vb[C];
+            uint8_t ta[C], tb[C], ua[C], ub[C];
+            // chunk ending at step t1 - 1, walked backwards (j = 0 is step t1 - 1)
+            auto load_bwd = [&](int t1, float (&r)[C], float (&v)[C], uint8_t (&te)[C],
+                                uint8_t (&tr)[C]) {
 #pragma unroll
                 for (int j = 0; j < C; ++j) {
-                    const int64_t i = (int64_t)(t1 - 1 - j >= 0 ? t1 - 1 - j : 0) * ld + e;
+                    const int t = t1 - 1 - j >= 0 ? t1 - 1 - j : 0;
+                    const int64_t i = (int64_t)t * ld + e;
                     r[j] = g.reward[i];
                     v[j] = g.value[i];
                     te[j] = g.term[i];
                     tr[j] = g.trunc[i];
                 }
+            };
+            auto bwd = [&](int t1, const float (&r)[C], const float (&v)[C], const uint8_t (&te)[C],
+                           const uint8_t (&tr)[C]) {
 #pragma unroll
                 for (int j = 0; j < C; ++j) {
                     const int t = t1 - 1 - j;
@@ -211,6 +231,13 @@ __global__ __launch_bounds__(256) void gae_kernel(GaeArgs g)
                     s[IM_SUM_RETURN] += (double)r32;
                     v_next = vt;
                 }
+            };
+            load_bwd(T, ra, va, ta, ua);
+            for (int t1 = T; t1 > 0; t1 -= 2 * C) {
+                load_bwd(t1 - C, rb, vb, tb, ub);
+                bwd(t1, ra, va, ta, ua);
+                load_bwd(t1 - 2 * C, ra, va, ta, ua);
+                if (t1 - C > 0) bwd(t1 - C, rb, vb, tb, ub);
             }
         }
     }
