@@ -12,6 +12,7 @@ import torch
 import oracle
 from paper_2609_09821_amd import binding, synth
 from tests import gpu_helpers as H
+from tests.worlds import clip_from_arrays, custom_world
 
 pytestmark = pytest.mark.gpu
 
@@ -114,6 +115,31 @@ def test_env_step_ten_leaf_tree_auto_split(N):
     assert len(parent) == d["skeleton"]["n_bodies"]
     d["skeleton"] = dict(d["skeleton"], parent=parent)
     _step_parity(3, N, 3, desc=d)
+
+
+def _tiny_world(B, N):
+    """A root alone (B = 1) or a root and one spherical child (B = 2), on a
+    40-frame clip that turns and bends, so that every walk and observation
+    loop runs its shortest form."""
+    F = 40
+    t = np.arange(F) / (F - 1)
+    root_pos = np.stack([0.8 * t, 0.1 * np.sin(3 * t), 0.9 + 0.05 * np.cos(2 * t)], 1)
+    th = 0.6 * t
+    root_quat = np.stack([np.cos(th / 2), 0 * t, 0 * t, np.sin(th / 2)], 1)
+    ph = 0.4 * np.sin(4 * t)
+    local = np.stack([np.cos(ph / 2), np.sin(ph / 2) * 0.6, np.sin(ph / 2) * 0.8, 0 * t], 1)
+    local = local[:, None, :].repeat(B - 1, 1)
+    d = custom_world(list(range(-1, B - 1)), [0] + [1] * (B - 1),
+                     [[0, 0, 0]] + [[0.3, 0, 0]] * (B - 1), [2.0] * B,
+                     [clip_from_arrays(root_pos, root_quat, local)])
+    d["n_envs"] = N
+    return d
+
+
+@pytest.mark.parametrize("B", [1, 2])
+@pytest.mark.parametrize("N", [300, 70001])
+def test_env_step_tiny_skeletons(B, N):
+    _step_parity(1, N, 3, desc=_tiny_world(B, N))
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5, 6])
