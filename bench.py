@@ -57,9 +57,11 @@ SHARED_SOURCES = []
 TRAFFIC_KIB = {
     # policy: one entry per launch of im_policy_act (a bf16 policy is one launch)
     "policy": {"sources": ["policy_kernels.hip", "device_math.h", "launch.h"], "sha": "057f2257ff61f4c1", "workloads": {
-        4: {"fetch": [109680.0], "write": [35584.0]}}},
+        4: {"fetch": [109680.0], "write": [35584.0]},
+        5: {"fetch": [140414.0], "write": [58368.0]}}},
     "env": {"sources": ["env_kernels.hip", "device_math.h", "tables.h"], "sha": "eeed804b596bf8b3", "workloads": {
-        4: {"fetch": [61765.5], "write": [169488.8]}}},
+        4: {"fetch": [61765.5], "write": [169488.8]},
+        5: {"fetch": [184002.8], "write": [413742.0]}}},
 }
 
 
